@@ -1,0 +1,209 @@
+/*
+ * hpd.h -- C ABI of the MI355X (gfx950) branch-parallel decode step.
+ *
+ * Method: "HPD-Parsing: Hierarchical Parallel Document Parsing"
+ * (arXiv 2607.18839).  In one decode step the main layout branch of a page and
+ * every content branch forked from it each bring k new (draft-verify) query
+ * tokens.  Every branch attends over the page's shared visual + structural
+ * prefix KV and over its own private (incremental) KV only, never over other
+ * branches' text (section "Layout-Coordinated Parallel Decoding", paragraph
+ * "Dynamic Branch Forking and Efficient Context Isolation").  The k drafts of a
+ * branch are verified together in one forward, so they are causal among
+ * themselves (section "Integration with P-MTP", last paragraph; Algorithm 1,
+ * the parallel draft over the active pool).  The decoder is a GQA / RMSNorm /
+ * SwiGLU stack (section "Overview", paragraph "LLM Decoder").
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Pure C.  No exception crosses the boundary; every call returns an
+ *    hpd_status and never aborts.  hpd_last_error_message() gives a
+ *    thread-local description of the last non-OK status of the calling thread.
+ *  - "Host" pointers are ordinary CPU memory, read only during the call.
+ *    "Device" pointers are GPU memory owned by the caller; the library never
+ *    allocates or frees device memory and never synchronises a stream.
+ *  - Streams are passed as `void *stream`, a hipStream_t (NULL = the null
+ *    stream).  Work is enqueued in stream order and runs asynchronously.
+ *  - Validation happens before any launch: a validation error writes nothing.
+ *    A HIP launch error returns HPD_ERR_HIP; outputs are then undefined.
+ *  - Tensors are row-major and contiguous:
+ *        q          [T][Hq][D]              token t = j-th new token of branch b
+ *                                            at t = q_row[b] + j
+ *        shared_k/v [shared rows][Hkv][D]   page p's prefix at rows
+ *                                            prefix_row[p] .. + P_p - 1
+ *        priv_k/v   [private rows][Hkv][D]  branch b's rows at priv_row[b] ..
+ *                                            + L_b + k_b - 1: its L_b past
+ *                                            tokens, then its k_b new tokens
+ *        out        [T][Hq][D]              out_dtype
+ *        lse        [T][Hq] float           natural-log log-sum-exp of the
+ *                                            scaled scores (nullable)
+ *    Query head h uses KV head h / (Hq / Hkv) (contiguous GQA groups).
+ *  - Visibility: new token j of branch b on page p sees shared rows
+ *    0 .. F_b - 1 of page p (F_b = P_p unless fork_len is given) and private
+ *    rows 0 .. L_b + j of branch b (bottom-right causal among the drafts).
+ */
+#ifndef HPD_H
+#define HPD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HPD_MAX_K 16        /* new tokens per branch per step (draft window) */
+#define HPD_HEAD_DIM 64     /* the only supported head dimension */
+#define HPD_MAX_Q_HEADS 64
+#define HPD_MAX_GROUP 32    /* Hq / Hkv */
+
+typedef enum {
+  HPD_OK = 0,
+  HPD_ERR_INVALID_ARGUMENT = 1,
+  HPD_ERR_UNSUPPORTED = 2,
+  HPD_ERR_WORKSPACE_TOO_SMALL = 3,
+  HPD_ERR_HIP = 4,
+  HPD_ERR_HOST_ALLOC = 5
+} hpd_status;
+
+typedef enum { HPD_F32 = 0, HPD_BF16 = 1 } hpd_dtype;
+
+/* One attention layer's shape. */
+typedef struct {
+  int32_t num_q_heads;   /* Hq, 1..HPD_MAX_Q_HEADS, Hq % Hkv == 0            */
+  int32_t num_kv_heads;  /* Hkv >= 1, Hq / Hkv <= HPD_MAX_GROUP               */
+  int32_t head_dim;      /* D; must be HPD_HEAD_DIM, else HPD_ERR_UNSUPPORTED */
+  float softmax_scale;   /* <= 0 selects 1 / sqrt(D)                          */
+  int32_t dtype;         /* hpd_dtype of q, shared_k/v, priv_k/v              */
+  int32_t out_dtype;     /* hpd_dtype of out                                  */
+} hpd_attn_desc;
+
+/* A ragged batch of pages and branches.  HOST arrays, read only inside
+ * hpd_plan_create.  Branches are grouped by page (branch_page non-decreasing);
+ * within a page the layout branch conventionally comes first. */
+typedef struct {
+  int32_t num_pages;          /* >= 1                                          */
+  const int32_t *prefix_len;  /* [num_pages] P_p >= 0                          */
+  const int64_t *prefix_row;  /* [num_pages] first shared row of page p;
+                                 NULL = packed (exclusive prefix sum of P_p)   */
+  int32_t num_branches;       /* >= 1                                          */
+  const int32_t *branch_page; /* [nb] page of branch b, non-decreasing         */
+  const int32_t *num_new;     /* [nb] k_b in 1..HPD_MAX_K                      */
+  const int32_t *past_len;    /* [nb] L_b >= 0 (excludes the k_b new tokens)   */
+  const int64_t *priv_row;    /* [nb] first private row of branch b;
+                                 NULL = packed (exclusive sum of L_b + k_b)    */
+  const int32_t *fork_len;    /* [nb] visible prefix F_b in 0..P_p; NULL = P_p */
+} hpd_batch_desc;
+
+/* Opaque, immutable execution plan: the canonical ragged bookkeeping (row
+ * offsets, visible-key counts) plus the work lists of the three attention
+ * kernels and the layout of their scratch partials.  Host memory. */
+typedef struct hpd_plan hpd_plan;
+
+/* Integer bookkeeping of a plan, for inspection and bit-exact tests.  The
+ * arrays point into the plan and live as long as it does. */
+typedef struct {
+  int32_t num_tokens;             /* T = sum k_b                               */
+  int32_t num_pages, num_branches;
+  const int32_t *q_row;           /* [nb] first token of branch b              */
+  const int64_t *priv_row;        /* [nb] first private row of branch b        */
+  const int64_t *prefix_row;      /* [num_pages] first shared row of page p    */
+  const int32_t *page_q_row;      /* [num_pages] first token of page p         */
+  const int32_t *page_T;          /* [num_pages] tokens of page p              */
+  const int32_t *visible;         /* [T] keys seen by token t: F_b + L_b + j + 1 */
+  int64_t shared_rows;            /* rows shared_k/v must hold (max end row)   */
+  int64_t priv_rows;              /* rows priv_k/v must hold (max end row)     */
+  int32_t num_shared_items;       /* work items of the shared-prefix kernel    */
+  int32_t num_private_items;      /* work items of the private kernel          */
+  const int32_t *shared_items;    /* [num_shared_items][8] see plan.cpp        */
+  const int32_t *private_items;   /* [num_private_items][8] see plan.cpp       */
+  const int32_t *token_slots;     /* [T][2] first partial slot, slot count     */
+  int64_t num_partial_slots;      /* partial (O, lse) rows = slots * Hq        */
+} hpd_plan_info;
+
+/* Build a plan: validates the descriptors (see each field above), computes
+ * the bookkeeping and the work lists.  On success *out owns a new plan that
+ * the caller releases with hpd_plan_destroy. */
+hpd_status hpd_plan_create(const hpd_attn_desc *attn, const hpd_batch_desc *batch,
+                           hpd_plan **out);
+void hpd_plan_destroy(hpd_plan *plan);
+
+/* Bytes of device workspace a step with this plan needs (work lists + the
+ * fp32 partials of the split softmax).  The workspace is caller-owned, at
+ * least 256-byte aligned, and must not be shared by steps that overlap. */
+size_t hpd_plan_workspace_bytes(const hpd_plan *plan);
+
+hpd_status hpd_plan_query(const hpd_plan *plan, hpd_plan_info *out);
+
+/* Copy the plan's work lists into the device workspace (asynchronous on
+ * `stream`).  Must precede the first step that uses this (plan, workspace)
+ * pair; the tables stay valid until the caller overwrites the workspace. */
+hpd_status hpd_plan_upload(const hpd_plan *plan, void *workspace, size_t workspace_bytes,
+                           void *stream);
+
+/* One attention layer of the branch-parallel decode step.
+ *
+ * Computes, for every new token of every branch and every query head, softmax
+ * attention over the branch's visible keys (see the conventions above) as
+ * three kernels: (1) the shared-prefix kernel stacks the query rows of all
+ * branches of a page that share a KV head into MFMA tiles, so each prefix K/V
+ * tile is read once per page and KV head; (2) the private kernel attends each
+ * branch's ragged private rows with the bottom-right causal mask; (3) the
+ * log-sum-exp merge combines all partial softmaxes into out and lse.
+ *
+ * q, shared_k, shared_v, priv_k, priv_v: device, attn->dtype, layouts above.
+ *   shared_k/v may be NULL only if every P_p is 0.
+ * out: device [T][Hq][D] in attn->out_dtype.  lse: device [T][Hq] or NULL.
+ * workspace: device, >= hpd_plan_workspace_bytes, uploaded with
+ *   hpd_plan_upload.  The step reads only the rows the plan names. */
+hpd_status hpd_branch_attn_step(const hpd_plan *plan, const void *q, const void *shared_k,
+                                const void *shared_v, const void *priv_k, const void *priv_v,
+                                void *out, float *lse, void *workspace, size_t workspace_bytes,
+                                void *stream);
+
+/* The synthetic decoder stack (pre-norm GQA transformer with RMSNorm and a
+ * SwiGLU MLP, section "Overview", paragraph "LLM Decoder").  Weights are bf16
+ * device arrays in torch Linear layout W[out][in]; each field points to a
+ * HOST array of num_layers device pointers. */
+typedef struct {
+  int32_t num_layers;
+  int32_t hidden;               /* multiple of 64                              */
+  int32_t intermediate;         /* multiple of 64                              */
+  float rms_eps;                /* RMSNorm epsilon                             */
+  const void *const *w_qkv;     /* [L] -> [(Hq + 2 Hkv) D][hidden]: q rows, then k, then v */
+  const void *const *w_o;       /* [L] -> [hidden][Hq D]                       */
+  const void *const *w_gate;    /* [L] -> [intermediate][hidden]               */
+  const void *const *w_up;      /* [L] -> [intermediate][hidden]               */
+  const void *const *w_down;    /* [L] -> [hidden][intermediate]               */
+  const void *const *g_attn_norm; /* [L] -> [hidden] bf16 RMSNorm gain; NULL = ones */
+  const void *const *g_mlp_norm;  /* [L] -> [hidden] bf16 RMSNorm gain; NULL = ones */
+} hpd_model_desc;
+
+/* Bytes of device workspace hpd_decode_step needs on top of
+ * hpd_plan_workspace_bytes (activations of the T tokens). */
+size_t hpd_decode_workspace_bytes(const hpd_model_desc *model, const hpd_plan *plan);
+
+/* One full decode step of the decoder stack for every new token of every
+ * branch.  For each layer l: x = RMSNorm(h); [q|k|v] = x W_qkv^T; k and v are
+ * rounded to bf16 and written into private rows priv_row[b] + L_b + j of
+ * priv_k[l] / priv_v[l] (no other row is written); a = attention as in
+ * hpd_branch_attn_step; h += a W_o^T; x = RMSNorm(h);
+ * h += (silu(x W_gate^T) * (x W_up^T)) W_down^T.
+ * hidden_in, hidden_out: device float [T][hidden] (may alias).
+ * shared_k/v, priv_k/v: HOST arrays of num_layers device pointers (bf16).
+ * The plan's dtype must be HPD_BF16, out_dtype HPD_BF16 or HPD_F32.
+ * workspace: >= hpd_plan_workspace_bytes + hpd_decode_workspace_bytes,
+ *   uploaded with hpd_plan_upload. */
+hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan,
+                           const float *hidden_in, float *hidden_out,
+                           const void *const *shared_k, const void *const *shared_v,
+                           void *const *priv_k, void *const *priv_v,
+                           void *workspace, size_t workspace_bytes, void *stream);
+
+const char *hpd_status_string(hpd_status status);
+const char *hpd_last_error_message(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HPD_H */

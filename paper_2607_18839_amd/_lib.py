@@ -1,0 +1,228 @@
+"""ctypes binding of libhpd.so: the C ABI of include/hpd.h, names unchanged.
+
+Argument marshalling only: every step of the decode path runs in the HIP
+kernels of the library.  Device pointers are plain integers (for torch
+tensors, ``tensor.data_ptr()``); streams are hipStream_t handles as integers
+(``torch.cuda.current_stream().cuda_stream``) or None for the null stream.
+There is no fallback: if the library is missing, loading fails loudly.
+"""
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libhpd.so")
+
+HPD_MAX_K = 16
+HPD_HEAD_DIM = 64
+HPD_F32, HPD_BF16 = 0, 1
+STATUS = {0: "HPD_OK", 1: "HPD_ERR_INVALID_ARGUMENT", 2: "HPD_ERR_UNSUPPORTED",
+          3: "HPD_ERR_WORKSPACE_TOO_SMALL", 4: "HPD_ERR_HIP", 5: "HPD_ERR_HOST_ALLOC"}
+
+# Work-item record widths and fields (paper_2607_18839_amd/csrc/plan.h).
+SI_NFIELDS = PI_NFIELDS = 12
+SI = dict(page=0, kvh=1, row0=2, nrows=3, key0=4, key1=5, slot=6, flags=7, prefix_row=8,
+          page_q_row=9, page_rows=10)
+PI = dict(branch=0, kvh=1, row0=2, nrows=3, key0=4, key1=5, slot=6, past=7, priv_row=8,
+          q_row=9, num_new=10)
+
+c_i32p = ctypes.POINTER(ctypes.c_int32)
+c_i64p = ctypes.POINTER(ctypes.c_int64)
+
+
+class HpdError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+class hpd_attn_desc(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
+                ("dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32)]
+
+
+class hpd_batch_desc(ctypes.Structure):
+    _fields_ = [("num_pages", ctypes.c_int32), ("prefix_len", c_i32p), ("prefix_row", c_i64p),
+                ("num_branches", ctypes.c_int32), ("branch_page", c_i32p), ("num_new", c_i32p),
+                ("past_len", c_i32p), ("priv_row", c_i64p), ("fork_len", c_i32p)]
+
+
+class hpd_plan_info(ctypes.Structure):
+    _fields_ = [("num_tokens", ctypes.c_int32), ("num_pages", ctypes.c_int32),
+                ("num_branches", ctypes.c_int32), ("q_row", c_i32p), ("priv_row", c_i64p),
+                ("prefix_row", c_i64p), ("page_q_row", c_i32p), ("page_T", c_i32p),
+                ("visible", c_i32p), ("shared_rows", ctypes.c_int64), ("priv_rows", ctypes.c_int64),
+                ("num_shared_items", ctypes.c_int32), ("num_private_items", ctypes.c_int32),
+                ("shared_items", c_i32p), ("private_items", c_i32p), ("token_slots", c_i32p),
+                ("num_partial_slots", ctypes.c_int64)]
+
+
+PP = ctypes.POINTER(ctypes.c_void_p)
+
+
+class hpd_model_desc(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("hidden", ctypes.c_int32),
+                ("intermediate", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("w_qkv", PP), ("w_o", PP), ("w_gate", PP), ("w_up", PP), ("w_down", PP),
+                ("g_attn_norm", PP), ("g_mlp_norm", PP)]
+
+
+# Every symbol include/hpd.h declares, with its ctypes signature.
+SIGNATURES = {
+    "hpd_plan_create": (ctypes.c_int, [ctypes.POINTER(hpd_attn_desc), ctypes.POINTER(hpd_batch_desc),
+                                       ctypes.POINTER(ctypes.c_void_p)]),
+    "hpd_plan_destroy": (None, [ctypes.c_void_p]),
+    "hpd_plan_workspace_bytes": (ctypes.c_size_t, [ctypes.c_void_p]),
+    "hpd_plan_query": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(hpd_plan_info)]),
+    "hpd_plan_upload": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "hpd_branch_attn_step": (ctypes.c_int, [ctypes.c_void_p] + [ctypes.c_void_p] * 6 +
+                             [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "hpd_decode_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(hpd_model_desc), ctypes.c_void_p]),
+    "hpd_decode_step": (ctypes.c_int, [ctypes.POINTER(hpd_model_desc), ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_void_p, PP, PP, PP, PP, ctypes.c_void_p, ctypes.c_size_t,
+                                       ctypes.c_void_p]),
+    "hpd_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "hpd_last_error_message": (ctypes.c_char_p, []),
+}
+
+_lib = None
+
+
+def load(path=LIB_PATH):
+    """Load libhpd.so once; raise if it is missing (there is no CPU fallback)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(path):
+            raise ImportError(f"{path} not built: run `python -m paper_2607_18839_amd.build` "
+                              "(the HIP library is required; there is no fallback path)")
+        lib = ctypes.CDLL(path)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def _check(status, what):
+    if status != 0:
+        msg = load().hpd_last_error_message().decode(errors="replace")
+        raise HpdError(status, msg if msg.startswith(what) else f"{what}: {msg}")
+
+
+def _i32(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _i64(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.int64)
+
+
+def _ptr(a, ty):
+    return None if a is None else a.ctypes.data_as(ty)
+
+
+class Plan:
+    """Owns an hpd_plan handle (host memory), built by hpd_plan_create."""
+
+    def __init__(self, handle, attn):
+        self.handle = handle
+        self.attn = attn
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.hpd_plan_destroy(self.handle)
+            self.handle = None
+
+    @property
+    def workspace_bytes(self):
+        return int(load().hpd_plan_workspace_bytes(self.handle))
+
+
+def hpd_plan_create(num_q_heads, num_kv_heads, prefix_len, branch_page, num_new, past_len,
+                    head_dim=HPD_HEAD_DIM, softmax_scale=0.0, dtype=HPD_BF16, out_dtype=None,
+                    prefix_row=None, priv_row=None, fork_len=None):
+    lib = load()
+    attn = hpd_attn_desc(num_q_heads, num_kv_heads, head_dim, softmax_scale, dtype,
+                         dtype if out_dtype is None else out_dtype)
+    arrs = dict(prefix_len=_i32(prefix_len), branch_page=_i32(branch_page), num_new=_i32(num_new),
+                past_len=_i32(past_len), prefix_row=_i64(prefix_row), priv_row=_i64(priv_row),
+                fork_len=_i32(fork_len))
+    batch = hpd_batch_desc(len(arrs["prefix_len"]), _ptr(arrs["prefix_len"], c_i32p),
+                           _ptr(arrs["prefix_row"], c_i64p), len(arrs["num_new"]),
+                           _ptr(arrs["branch_page"], c_i32p), _ptr(arrs["num_new"], c_i32p),
+                           _ptr(arrs["past_len"], c_i32p), _ptr(arrs["priv_row"], c_i64p),
+                           _ptr(arrs["fork_len"], c_i32p))
+    h = ctypes.c_void_p()
+    _check(lib.hpd_plan_create(ctypes.byref(attn), ctypes.byref(batch), ctypes.byref(h)), "hpd_plan_create")
+    return Plan(h, attn)
+
+
+def hpd_plan_query(plan):
+    """The plan's integer bookkeeping and work lists as numpy arrays (copies)."""
+    info = hpd_plan_info()
+    _check(load().hpd_plan_query(plan.handle, ctypes.byref(info)), "hpd_plan_query")
+    T, npg, nb = info.num_tokens, info.num_pages, info.num_branches
+
+    def arr(p, n, w=1):
+        if n * w == 0:
+            return np.zeros((n, w) if w > 1 else n, dtype=np.int64 if p._type_ is ctypes.c_int64 else np.int32)
+        a = np.ctypeslib.as_array(p, shape=(n * w,)).copy()
+        return a.reshape(n, w) if w > 1 else a
+
+    return dict(T=T, q_row=arr(info.q_row, nb), priv_row=arr(info.priv_row, nb),
+                prefix_row=arr(info.prefix_row, npg), page_q_row=arr(info.page_q_row, npg),
+                page_T=arr(info.page_T, npg), visible=arr(info.visible, T),
+                shared_rows=info.shared_rows, priv_rows=info.priv_rows,
+                shared_items=arr(info.shared_items, info.num_shared_items, SI_NFIELDS),
+                private_items=arr(info.private_items, info.num_private_items, PI_NFIELDS),
+                token_slots=arr(info.token_slots, T, 2), num_partial_slots=info.num_partial_slots)
+
+
+def hpd_plan_upload(plan, workspace, nbytes, stream=None):
+    _check(load().hpd_plan_upload(plan.handle, workspace, nbytes, stream), "hpd_plan_upload")
+
+
+def hpd_branch_attn_step(plan, q, shared_k, shared_v, priv_k, priv_v, out, lse, workspace,
+                         workspace_bytes, stream=None):
+    _check(load().hpd_branch_attn_step(plan.handle, q, shared_k, shared_v, priv_k, priv_v, out, lse,
+                                       workspace, workspace_bytes, stream), "hpd_branch_attn_step")
+
+
+def _ptr_array(ptrs):
+    if ptrs is None:
+        return None
+    return (ctypes.c_void_p * len(ptrs))(*ptrs)
+
+
+def model_desc(num_layers, hidden, intermediate, rms_eps, w_qkv, w_o, w_gate, w_up, w_down,
+               g_attn_norm=None, g_mlp_norm=None):
+    """hpd_model_desc from lists of device pointers; keeps the arrays alive."""
+    keep = [_ptr_array(x) for x in (w_qkv, w_o, w_gate, w_up, w_down, g_attn_norm, g_mlp_norm)]
+    cast = [None if k is None else ctypes.cast(k, PP) for k in keep]
+    d = hpd_model_desc(num_layers, hidden, intermediate, rms_eps, *cast)
+    d._keep = keep
+    return d
+
+
+def hpd_decode_workspace_bytes(model, plan):
+    return int(load().hpd_decode_workspace_bytes(ctypes.byref(model), plan.handle))
+
+
+def hpd_decode_step(model, plan, hidden_in, hidden_out, shared_k, shared_v, priv_k, priv_v,
+                    workspace, workspace_bytes, stream=None):
+    arrs = [_ptr_array(x) for x in (shared_k, shared_v, priv_k, priv_v)]
+    _check(load().hpd_decode_step(ctypes.byref(model), plan.handle, hidden_in, hidden_out,
+                                  *[ctypes.cast(a, PP) for a in arrs], workspace, workspace_bytes,
+                                  stream), "hpd_decode_step")
+
+
+def declared_symbols(header=None):
+    """Function names declared in include/hpd.h."""
+    import re
+    header = header or os.path.join(os.path.dirname(_HERE), "include", "hpd.h")
+    text = open(header).read()
+    return sorted(set(re.findall(r"\b(hpd_[a-z_]+)\s*\(", text)))

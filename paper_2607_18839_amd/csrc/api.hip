@@ -1,0 +1,132 @@
+// C ABI entry points (declared in include/hpd.h).  Validation happens here,
+// before any launch; nothing below throws across the boundary.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "hpd.h"
+#include "kernels.h"
+#include "plan.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+hpd_status set_err(hpd_status st, const std::string &msg) {
+  g_last_error = msg;
+  return st;
+}
+
+hpd_status hip_err(hipError_t e, const char *where) {
+  return set_err(HPD_ERR_HIP, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char *hpd_status_string(hpd_status s) {
+  switch (s) {
+    case HPD_OK: return "HPD_OK";
+    case HPD_ERR_INVALID_ARGUMENT: return "HPD_ERR_INVALID_ARGUMENT";
+    case HPD_ERR_UNSUPPORTED: return "HPD_ERR_UNSUPPORTED";
+    case HPD_ERR_WORKSPACE_TOO_SMALL: return "HPD_ERR_WORKSPACE_TOO_SMALL";
+    case HPD_ERR_HIP: return "HPD_ERR_HIP";
+    case HPD_ERR_HOST_ALLOC: return "HPD_ERR_HOST_ALLOC";
+  }
+  return "HPD_ERR_UNKNOWN";
+}
+
+const char *hpd_last_error_message(void) { return g_last_error.c_str(); }
+
+hpd_status hpd_plan_create(const hpd_attn_desc *attn, const hpd_batch_desc *batch, hpd_plan **out) {
+  if (!out) return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_plan_create: out is NULL");
+  *out = nullptr;
+  hpd_plan *p = new (std::nothrow) hpd_plan;
+  if (!p) return set_err(HPD_ERR_HOST_ALLOC, "hpd_plan_create: out of host memory");
+  std::string err;
+  hpd_status st;
+  try {
+    st = hpd::build_plan(attn, batch, &p->p, &err);
+  } catch (const std::bad_alloc &) {
+    delete p;
+    return set_err(HPD_ERR_HOST_ALLOC, "hpd_plan_create: out of host memory");
+  }
+  if (st != HPD_OK) {
+    delete p;
+    return set_err(st, "hpd_plan_create: " + err);
+  }
+  *out = p;
+  return HPD_OK;
+}
+
+void hpd_plan_destroy(hpd_plan *plan) { delete plan; }
+
+size_t hpd_plan_workspace_bytes(const hpd_plan *plan) { return plan ? plan->p.workspace_bytes : 0; }
+
+hpd_status hpd_plan_query(const hpd_plan *plan, hpd_plan_info *o) {
+  if (!plan || !o) return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_plan_query: NULL argument");
+  const hpd::Plan &P = plan->p;
+  o->num_tokens = P.T;
+  o->num_pages = P.num_pages;
+  o->num_branches = P.num_branches;
+  o->q_row = P.q_row.data();
+  o->priv_row = P.priv_row.data();
+  o->prefix_row = P.prefix_row.data();
+  o->page_q_row = P.page_q_row.data();
+  o->page_T = P.page_T.data();
+  o->visible = P.visible.data();
+  o->shared_rows = P.shared_rows;
+  o->priv_rows = P.priv_rows;
+  o->num_shared_items = P.num_shared_items();
+  o->num_private_items = P.num_private_items();
+  o->shared_items = P.shared_items.data();
+  o->private_items = P.private_items.data();
+  o->token_slots = P.token_slots.data();
+  o->num_partial_slots = P.num_slots;
+  return HPD_OK;
+}
+
+hpd_status hpd_plan_upload(const hpd_plan *plan, void *workspace, size_t bytes, void *stream) {
+  if (!plan || !workspace) return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_plan_upload: NULL argument");
+  if (!aligned(workspace, 256))
+    return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_plan_upload: workspace must be 256-byte aligned");
+  if (bytes < plan->p.workspace_bytes)
+    return set_err(HPD_ERR_WORKSPACE_TOO_SMALL, "hpd_plan_upload: workspace too small");
+  if (plan->p.table_bytes == 0) return HPD_OK;
+  hipError_t e = hipMemcpyAsync(workspace, plan->p.table_image.data(), plan->p.table_bytes,
+                                hipMemcpyHostToDevice, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_err(e, "hpd_plan_upload");
+  return HPD_OK;
+}
+
+hpd_status hpd_branch_attn_step(const hpd_plan *plan, const void *q, const void *shared_k,
+                                const void *shared_v, const void *priv_k, const void *priv_v,
+                                void *out, float *lse, void *workspace, size_t workspace_bytes,
+                                void *stream) {
+  if (!plan) return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_branch_attn_step: plan is NULL");
+  const hpd::Plan &P = plan->p;
+  if (!q || !priv_k || !priv_v || !out || !workspace)
+    return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_branch_attn_step: NULL tensor or workspace");
+  if (P.shared_rows > 0 && (!shared_k || !shared_v))
+    return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_branch_attn_step: shared_k/v NULL with a non-empty prefix");
+  if (!aligned(q, 16) || !aligned(priv_k, 16) || !aligned(priv_v, 16) || !aligned(out, 16) ||
+      (shared_k && !aligned(shared_k, 16)) || (shared_v && !aligned(shared_v, 16)) ||
+      (lse && !aligned(lse, 4)))
+    return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_branch_attn_step: tensors must be 16-byte aligned");
+  if (!aligned(workspace, 256))
+    return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_branch_attn_step: workspace must be 256-byte aligned");
+  if (workspace_bytes < P.workspace_bytes)
+    return set_err(HPD_ERR_WORKSPACE_TOO_SMALL, "hpd_branch_attn_step: workspace too small");
+  hipError_t e = hpd::launch_branch_attention(P, q, shared_k, shared_v, priv_k, priv_v, out, lse,
+                                              workspace, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_err(e, "hpd_branch_attn_step");
+  return HPD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,484 @@
+// gfx950 kernels of one branch-parallel attention layer.
+//
+// Every branch attends over its page's shared prefix and its own private rows
+// (section "Layout-Coordinated Parallel Decoding", paragraph "Dynamic Branch
+// Forking and Efficient Context Isolation"); the k drafts of a branch are
+// causal among themselves (section "Integration with P-MTP").  The layer is
+// computed in split form:
+//
+//   shared kernel   for each (page, kv head): the query rows of ALL branches
+//                   of the page that use this kv head are stacked into 32-row
+//                   MFMA tiles (row r = token r / G, head g * G + r % G), so a
+//                   prefix K/V tile is fetched once and used by every branch.
+//                   Each workgroup = 4 waves = 128 stacked rows over one key
+//                   range; it writes a partial (O, log2-sum-exp) per row.
+//   private kernel  for each (branch, kv head, key chunk): one wave attends
+//                   the branch's ragged private rows with the bottom-right
+//                   causal mask (draft j sees private keys 0 .. L_b + j).
+//   merge kernel    per (token, query head): log-sum-exp merge of all
+//                   partials into the output row and its natural-log lse.
+//
+// MFMA formulation (v_mfma_f32_32x32x16_bf16; fp32 inputs use eight
+// v_mfma_f32_32x32x2_f32 per step): scores are computed transposed,
+// S^T = K Q^T, so each lane owns one query (lane % 32) and 16 keys of every
+// 32-key block.  The row max then needs a single cross-lane exchange (lane ^
+// 32), the row sum none until the end, and the P^T registers are directly the
+// B operand of O^T += V^T P^T.  The contraction index of QK^T is permuted
+// (lane half h, step s -> dims 32h + 8s .. +7, identical for K and Q), and
+// V^T is stored in LDS with key bits 2 and 3 swapped so that each PV operand
+// is one contiguous 16-byte LDS read.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "kernels.h"
+
+namespace hpd {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr int D = HPD_HEAD_DIM;
+
+// ------------------------------------------------------------ MFMA operands
+
+template <typename T> struct Frag;                     // 8 contraction elements per lane
+template <> struct Frag<__bf16> { bf16x8 v; };
+template <> struct Frag<float> { f32x4 lo, hi; };
+
+__device__ __forceinline__ void mma(f32x16 &acc, const Frag<__bf16> &a, const Frag<__bf16> &b) {
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.v, b.v, acc, 0, 0, 0);
+}
+// fp32: lane half h holds contraction index 8h + e in element e; eight
+// 32x32x2 steps each take element e of both halves (indices e and 8 + e).
+__device__ __forceinline__ void mma(f32x16 &acc, const Frag<float> &a, const Frag<float> &b) {
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.lo[0], b.lo[0], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.lo[1], b.lo[1], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.lo[2], b.lo[2], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.lo[3], b.lo[3], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.hi[0], b.hi[0], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.hi[1], b.hi[1], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.hi[2], b.hi[2], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a.hi[3], b.hi[3], acc, 0, 0, 0);
+}
+
+__device__ __forceinline__ void ld16(Frag<__bf16> &f, const __bf16 *p) { f.v = *(const bf16x8 *)p; }
+__device__ __forceinline__ void ld16(Frag<float> &f, const float *p) {
+  f.lo = *(const f32x4 *)p;
+  f.hi = *(const f32x4 *)(p + 4);
+}
+
+__device__ __forceinline__ void zero(Frag<__bf16> &f) {
+  for (int e = 0; e < 8; ++e) f.v[e] = (__bf16)0.f;
+}
+__device__ __forceinline__ void zero(Frag<float> &f) {
+  f.lo = f32x4{0.f, 0.f, 0.f, 0.f};
+  f.hi = f.lo;
+}
+
+// Eight fp32 probabilities -> B operand.
+__device__ __forceinline__ void from_f32(Frag<__bf16> &f, const float *x) {
+  for (int e = 0; e < 8; ++e) f.v[e] = (__bf16)x[e];
+}
+__device__ __forceinline__ void from_f32(Frag<float> &f, const float *x) {
+  f.lo = f32x4{x[0], x[1], x[2], x[3]};
+  f.hi = f32x4{x[4], x[5], x[6], x[7]};
+}
+
+// ------------------------------------------------------------ LDS tiles
+//
+// K tile: [64 keys][64 dims], 16-byte chunks XOR-swizzled per row so that the
+// 16 lanes of one LDS cycle (16 keys, same logical chunk) hit 64 banks.
+// V^T tile: [64 dims][64 keys + 16 B pad], keys stored at swap23(key).
+
+template <typename T> struct Tile {
+  static constexpr int kRowBytes = D * (int)sizeof(T);           // K row
+  static constexpr int kChunks = kRowBytes / 16;                 // 16-B chunks per K row
+  static constexpr int kVRowBytes = 64 * (int)sizeof(T) + 16;    // V^T row (one dim)
+  static constexpr int kKBytes = 64 * kRowBytes;
+  static constexpr int kVBytes = D * kVRowBytes;
+  static constexpr int kBytes = kKBytes + kVBytes;
+  __device__ static __forceinline__ int kchunk(int key, int q) {
+    if constexpr (sizeof(T) == 2) return q ^ ((key >> 1) & 7);
+    else return q ^ (key & 15);
+  }
+};
+
+__device__ __forceinline__ int swap23(int k) { return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1); }
+
+// Cooperative global -> register -> LDS staging of one 64-key K/V tile by NT
+// threads.  Keys at or beyond `nkeys` (relative to the tile) are zero-filled
+// and never read from memory.
+template <typename T, int NT> struct TileLoader {
+  using Tl = Tile<T>;
+  static constexpr int kKTasks = 64 * Tl::kChunks / NT;   // K chunks per thread
+  static constexpr int kVTasks = 32 * Tl::kChunks / NT;   // V key-pair chunks per thread
+  static_assert(kKTasks >= 1 && kVTasks >= 1, "tile loader thread count");
+  u32x4 kr[kKTasks];
+  u32x4 vr[kVTasks][2];
+
+  // rows: pointer to element [key 0][0] of this kv head; row stride in elements.
+  __device__ __forceinline__ void load(const T *rows, int64_t stride, int nkeys, int tid) {
+#pragma unroll
+    for (int i = 0; i < kKTasks; ++i) {
+      const int idx = tid + i * NT, key = idx / Tl::kChunks, q = idx % Tl::kChunks;
+      kr[i] = key < nkeys ? *(const u32x4 *)((const char *)(rows + key * stride) + 16 * q)
+                          : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  __device__ __forceinline__ void load_v(const T *rows, int64_t stride, int nkeys, int tid) {
+#pragma unroll
+    for (int i = 0; i < kVTasks; ++i) {
+      const int idx = tid + i * NT, m = idx / Tl::kChunks, q = idx % Tl::kChunks;
+      const int k0 = 2 * m, k1 = 2 * m + 1;
+      vr[i][0] = k0 < nkeys ? *(const u32x4 *)((const char *)(rows + k0 * stride) + 16 * q)
+                            : u32x4{0u, 0u, 0u, 0u};
+      vr[i][1] = k1 < nkeys ? *(const u32x4 *)((const char *)(rows + k1 * stride) + 16 * q)
+                            : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  __device__ __forceinline__ void store(unsigned char *lds, int tid) const {
+#pragma unroll
+    for (int i = 0; i < kKTasks; ++i) {
+      const int idx = tid + i * NT, key = idx / Tl::kChunks, q = idx % Tl::kChunks;
+      *(u32x4 *)(lds + key * Tl::kRowBytes + 16 * Tl::kchunk(key, q)) = kr[i];
+    }
+    unsigned char *vt = lds + Tl::kKBytes;
+#pragma unroll
+    for (int i = 0; i < kVTasks; ++i) {
+      const int idx = tid + i * NT, m = idx / Tl::kChunks, q = idx % Tl::kChunks;
+      const int pos = swap23(2 * m);
+      if constexpr (sizeof(T) == 2) {
+        // chunk = 8 bf16 dims of key 2m (vr[i][0]) and of key 2m+1 (vr[i][1])
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const unsigned w0 = vr[i][0][e / 2], w1 = vr[i][1][e / 2];
+          const unsigned lo = (e & 1) ? (w0 >> 16) : (w0 & 0xffffu);
+          const unsigned hi = (e & 1) ? (w1 & 0xffff0000u) : (w1 << 16);
+          *(unsigned *)(vt + (q * 8 + e) * Tl::kVRowBytes + pos * 2) = lo | hi;
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          *(u32x2 *)(vt + (q * 4 + e) * Tl::kVRowBytes + pos * 4) = u32x2{vr[i][0][e], vr[i][1][e]};
+      }
+    }
+  }
+};
+
+// ------------------------------------------------------------ wave state
+
+// One wave: 32 query rows (lane % 32) against the keys of successive tiles.
+template <typename T> struct WaveAttn {
+  Frag<T> qf[4];      // Q^T operand for the 4 contraction steps of D = 64
+  f32x16 o[2];        // O^T accumulators: dims 0..31 and 32..63
+  float m;            // running max of the scaled log2 scores of this query
+  float l;            // this lane's share of the running sum
+  int half;           // lane / 32
+
+  __device__ __forceinline__ void init(const T *qrow, bool valid, int lane) {
+    half = lane >> 5;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (valid) ld16(qf[s], qrow + 32 * half + 8 * s);
+      else zero(qf[s]);
+    }
+    for (int r = 0; r < 16; ++r) { o[0][r] = 0.f; o[1][r] = 0.f; }
+    m = -INFINITY;
+    l = 0.f;
+  }
+
+  // Processes one LDS tile whose first key has index key0; keys with index
+  // >= limit are masked for this lane's query.  `masked` is wave-uniform:
+  // false when every key of the tile is visible to every row of the wave.
+  __device__ __forceinline__ void tile(const unsigned char *lds, int key0, int limit, bool masked,
+                                       float c, int lane) {
+    using Tl = Tile<T>;
+    const int kr = lane & 31;
+    f32x16 s[2];
+    for (int r = 0; r < 16; ++r) { s[0][r] = 0.f; s[1][r] = 0.f; }
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const int key = 32 * kb + kr;
+      const unsigned char *row = lds + key * Tl::kRowBytes;
+#pragma unroll
+      for (int st = 0; st < 4; ++st) {
+        Frag<T> a;
+        if constexpr (sizeof(T) == 2) {
+          ld16(a, (const T *)(row + 16 * Tl::kchunk(key, 4 * half + st)));
+        } else {
+          a.lo = *(const f32x4 *)(row + 16 * Tl::kchunk(key, 8 * half + 2 * st));
+          a.hi = *(const f32x4 *)(row + 16 * Tl::kchunk(key, 8 * half + 2 * st + 1));
+        }
+        mma(s[kb], a, qf[st]);
+      }
+    }
+    if (masked) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = key0 + 32 * kb + (r >> 2) * 8 + 4 * half + (r & 3);
+          if (key >= limit) s[kb][r] = -INFINITY;
+        }
+    }
+    float mx = s[0][0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m, mx * c);
+    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = __builtin_amdgcn_exp2f(m - m_use);
+    m = m_new;
+    float p[32];
+    float sum = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      p[r] = __builtin_amdgcn_exp2f(fmaf(s[0][r], c, -m_use));
+      p[16 + r] = __builtin_amdgcn_exp2f(fmaf(s[1][r], c, -m_use));
+    }
+#pragma unroll
+    for (int r = 0; r < 32; ++r) sum += p[r];
+    l = fmaf(l, alpha, sum);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) { o[0][r] *= alpha; o[1][r] *= alpha; }
+    Frag<T> pf[4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) from_f32(pf[st], p + 8 * st);
+    const unsigned char *vt = lds + Tl::kKBytes;
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const unsigned char *vrow = vt + (32 * b + kr) * Tl::kVRowBytes;
+#pragma unroll
+      for (int st = 0; st < 4; ++st) {
+        Frag<T> a;
+        ld16(a, (const T *)(vrow + (16 * st + 8 * half) * (int)sizeof(T)));
+        mma(o[b], a, pf[st]);
+      }
+    }
+  }
+
+  // Normalises and writes this lane's half of the partial row.
+  __device__ __forceinline__ void write(float *part_o, float *part_lse, int64_t prow, bool valid) {
+    const float l_tot = l + __shfl_xor(l, 32);
+    if (!valid) return;
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    float *dst = part_o + prow * D;
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int d = 32 * b + 8 * j + 4 * half;
+        *(f32x4 *)(dst + d) = f32x4{o[b][4 * j] * inv, o[b][4 * j + 1] * inv,
+                                    o[b][4 * j + 2] * inv, o[b][4 * j + 3] * inv};
+      }
+    if (half == 0) part_lse[prow] = l_tot > 0.f ? m + __builtin_amdgcn_logf(l_tot) : -INFINITY;
+  }
+};
+
+__device__ __forceinline__ int wave_min(int v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = min(v, __shfl_xor(v, off));
+  return v;
+}
+
+// ------------------------------------------------------------ shared kernel
+
+struct AttnArgs {
+  const void *q, *shared_k, *shared_v, *priv_k, *priv_v;
+  PlanDev dev;
+  int n_shared, n_private;
+  int Hq, Hkv, G;
+  float c;   // softmax scale * log2(e)
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
+  constexpr int NT = 256;
+  using Tl = Tile<T>;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[2][Tl::kBytes];
+
+  // XCD-aware order: consecutive workgroup ids go round-robin over the 8
+  // XCDs; give each XCD a contiguous run of items, so items that read the
+  // same key range share one L2.
+  const int per_xcd = gridDim.x / 8;
+  const int item = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (item >= a.n_shared) return;
+  const int32_t *it = a.dev.shared_items + (int64_t)item * SI_NFIELDS;
+  const int g = it[SI_KVH], row0 = it[SI_ROW0], nrows = it[SI_NROWS];
+  const int key0 = it[SI_KEY0], key1 = it[SI_KEY1], slot = it[SI_SLOT], flags = it[SI_FLAGS];
+  const int prefix_row = it[SI_PREFIX_ROW], page_q_row = it[SI_PAGE_Q_ROW];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int rloc = wave * 32 + (lane & 31);
+  const bool valid = rloc < nrows;
+  const int R = row0 + rloc;                           // stacked row of (page, g)
+  const int t = page_q_row + (valid ? R / a.G : 0);
+  const int hq = g * a.G + (valid ? R % a.G : 0);
+  int limit = key1;
+  if ((flags & SI_FLAG_FORK) && valid) limit = min(limit, a.dev.token_fork[t]);
+  const bool wave_active = wave * 32 < nrows;
+  const int wmin = wave_min(valid ? limit : key1);
+
+  const int64_t stride = (int64_t)a.Hkv * D;
+  const T *kbase = (const T *)a.shared_k + ((int64_t)prefix_row * a.Hkv + g) * D;
+  const T *vbase = (const T *)a.shared_v + ((int64_t)prefix_row * a.Hkv + g) * D;
+
+  WaveAttn<T> w;
+  w.init((const T *)a.q + ((int64_t)t * a.Hq + hq) * D, valid, lane);
+
+  TileLoader<T, NT> ld;
+  const int ntiles = (key1 - key0 + 63) / 64;
+  ld.load(kbase + (int64_t)key0 * stride, stride, key1 - key0, tid);
+  ld.load_v(vbase + (int64_t)key0 * stride, stride, key1 - key0, tid);
+  ld.store(lds[0], tid);
+  __syncthreads();
+  for (int i = 0; i < ntiles; ++i) {
+    const int k0 = key0 + 64 * i;
+    if (i + 1 < ntiles) {
+      ld.load(kbase + (int64_t)(k0 + 64) * stride, stride, key1 - k0 - 64, tid);
+      ld.load_v(vbase + (int64_t)(k0 + 64) * stride, stride, key1 - k0 - 64, tid);
+    }
+    if (wave_active) w.tile(lds[i & 1], k0, limit, k0 + 64 > wmin, a.c, lane);
+    if (i + 1 < ntiles) ld.store(lds[(i + 1) & 1], tid);
+    __syncthreads();
+  }
+  const int64_t prow = valid ? ((int64_t)a.dev.token_slots[2 * t] + slot) * a.Hq + hq : 0;
+  if (wave_active) w.write(a.dev.part_o, a.dev.part_lse, prow, valid);
+}
+
+// ------------------------------------------------------------ private kernel
+
+template <typename T>
+__global__ __launch_bounds__(64) void private_kernel(AttnArgs a) {
+  constexpr int NT = 64;
+  using Tl = Tile<T>;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[Tl::kBytes];
+  const int item = blockIdx.x;
+  if (item >= a.n_private) return;
+  const int32_t *it = a.dev.private_items + (int64_t)item * PI_NFIELDS;
+  const int g = it[PI_KVH], row0 = it[PI_ROW0], nrows = it[PI_NROWS];
+  const int key0 = it[PI_KEY0], key1 = it[PI_KEY1], slot = it[PI_SLOT], past = it[PI_PAST];
+  const int priv_row = it[PI_PRIV_ROW], q_row = it[PI_Q_ROW];
+
+  const int lane = threadIdx.x;
+  const int rloc = lane & 31;
+  const bool valid = rloc < nrows;
+  const int R = row0 + rloc;                            // stacked row of (branch, g)
+  const int j = valid ? R / a.G : 0;                    // draft index within the branch
+  const int t = q_row + j;
+  const int hq = g * a.G + (valid ? R % a.G : 0);
+  const int limit = valid ? min(key1, past + j + 1) : key1;   // bottom-right causal
+  const int wmin = wave_min(limit);
+
+  const int64_t stride = (int64_t)a.Hkv * D;
+  const T *kbase = (const T *)a.priv_k + ((int64_t)priv_row * a.Hkv + g) * D;
+  const T *vbase = (const T *)a.priv_v + ((int64_t)priv_row * a.Hkv + g) * D;
+
+  WaveAttn<T> w;
+  w.init((const T *)a.q + ((int64_t)t * a.Hq + hq) * D, valid, lane);
+  TileLoader<T, NT> ld;
+  for (int k0 = key0; k0 < key1; k0 += 64) {
+    ld.load(kbase + (int64_t)k0 * stride, stride, key1 - k0, lane);
+    ld.load_v(vbase + (int64_t)k0 * stride, stride, key1 - k0, lane);
+    __syncthreads();   // previous tile fully consumed
+    ld.store(lds, lane);
+    __syncthreads();
+    w.tile(lds, k0, limit, k0 + 64 > wmin, a.c, lane);
+  }
+  const int64_t prow = valid ? ((int64_t)a.dev.token_slots[2 * t] + slot) * a.Hq + hq : 0;
+  w.write(a.dev.part_o, a.dev.part_lse, prow, valid);
+}
+
+// ------------------------------------------------------------ merge kernel
+
+// 16 threads per (token, head) row, 4 dims each.  Partial lse values are in
+// log2 units; the exported lse is natural-log.
+template <typename TO>
+__global__ __launch_bounds__(256) void merge_kernel(PlanDev dev, TO *out, float *lse, int T, int Hq) {
+  const int row = blockIdx.x * 16 + (threadIdx.x >> 4);
+  if (row >= T * Hq) return;
+  const int sub = threadIdx.x & 15;
+  const int t = row / Hq, h = row % Hq;
+  const int first = dev.token_slots[2 * t], cnt = dev.token_slots[2 * t + 1];
+  float mx = -INFINITY;
+  for (int i = 0; i < cnt; ++i) mx = fmaxf(mx, dev.part_lse[(int64_t)(first + i) * Hq + h]);
+  const float m_use = mx == -INFINITY ? 0.f : mx;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float wsum = 0.f;
+  for (int i = 0; i < cnt; ++i) {
+    const int64_t pr = (int64_t)(first + i) * Hq + h;
+    const float wgt = __builtin_amdgcn_exp2f(dev.part_lse[pr] - m_use);
+    const f32x4 v = *(const f32x4 *)(dev.part_o + pr * D + 4 * sub);
+    wsum += wgt;
+    acc += wgt * v;
+  }
+  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  TO *dst = out + (int64_t)row * D + 4 * sub;
+  if constexpr (sizeof(TO) == 2) {
+    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+    bf16x4 r;
+    for (int e = 0; e < 4; ++e) r[e] = (__bf16)(acc[e] * inv);
+    *(bf16x4 *)dst = r;
+  } else {
+    *(f32x4 *)dst = acc * inv;
+  }
+  if (lse && sub == 0) lse[row] = wsum > 0.f ? (mx + __builtin_amdgcn_logf(wsum)) * kLn2 : -INFINITY;
+}
+
+}  // namespace
+
+PlanDev plan_dev(const Plan &P, void *workspace) {
+  unsigned char *ws = (unsigned char *)workspace;
+  PlanDev d;
+  d.shared_items = (const int32_t *)(ws + P.off_shared_items);
+  d.private_items = (const int32_t *)(ws + P.off_private_items);
+  d.token_slots = (const int32_t *)(ws + P.off_token_slots);
+  d.token_fork = (const int32_t *)(ws + P.off_token_fork);
+  d.part_o = (float *)(ws + P.off_part_o);
+  d.part_lse = (float *)(ws + P.off_part_lse);
+  return d;
+}
+
+hipError_t launch_branch_attention(const Plan &P, const void *q, const void *shared_k,
+                                   const void *shared_v, const void *priv_k, const void *priv_v,
+                                   void *out, float *lse, void *workspace, hipStream_t stream) {
+  AttnArgs a;
+  a.q = q; a.shared_k = shared_k; a.shared_v = shared_v; a.priv_k = priv_k; a.priv_v = priv_v;
+  a.dev = plan_dev(P, workspace);
+  a.n_shared = P.num_shared_items();
+  a.n_private = P.num_private_items();
+  a.Hq = P.attn.num_q_heads;
+  a.Hkv = P.attn.num_kv_heads;
+  a.G = P.G;
+  a.c = P.scale * kLog2e;
+  const bool bf16 = P.attn.dtype == HPD_BF16;
+  if (a.n_shared > 0) {
+    const int grid = (a.n_shared + 7) / 8 * 8;
+    if (bf16) hipLaunchKernelGGL(shared_prefix_kernel<__bf16>, dim3(grid), dim3(256), 0, stream, a);
+    else hipLaunchKernelGGL(shared_prefix_kernel<float>, dim3(grid), dim3(256), 0, stream, a);
+  }
+  if (a.n_private > 0) {
+    if (bf16) hipLaunchKernelGGL(private_kernel<__bf16>, dim3(a.n_private), dim3(64), 0, stream, a);
+    else hipLaunchKernelGGL(private_kernel<float>, dim3(a.n_private), dim3(64), 0, stream, a);
+  }
+  const int rows = P.T * P.attn.num_q_heads;
+  const int mgrid = (rows + 15) / 16;
+  if (P.attn.out_dtype == HPD_BF16)
+    hipLaunchKernelGGL(merge_kernel<__bf16>, dim3(mgrid), dim3(256), 0, stream, a.dev, (__bf16 *)out, lse,
+                       P.T, P.attn.num_q_heads);
+  else
+    hipLaunchKernelGGL(merge_kernel<float>, dim3(mgrid), dim3(256), 0, stream, a.dev, (float *)out, lse,
+                       P.T, P.attn.num_q_heads);
+  return hipGetLastError();
+}
+
+}  // namespace hpd

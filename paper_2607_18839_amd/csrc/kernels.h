@@ -1,0 +1,28 @@
+// Internal launchers of the gfx950 kernels (not part of the public ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "plan.h"
+
+namespace hpd {
+
+// Device views of the plan tables inside a workspace.
+struct PlanDev {
+  const int32_t *shared_items;
+  const int32_t *private_items;
+  const int32_t *token_slots;
+  const int32_t *token_fork;
+  float *part_o;
+  float *part_lse;
+};
+
+PlanDev plan_dev(const Plan &P, void *workspace);
+
+// One attention layer: shared-prefix kernel, private kernel, merge kernel.
+// q/k/v in P.attn.dtype; out in P.attn.out_dtype; lse may be NULL.
+hipError_t launch_branch_attention(const Plan &P, const void *q, const void *shared_k,
+                                   const void *shared_v, const void *priv_k, const void *priv_v,
+                                   void *out, float *lse, void *workspace, hipStream_t stream);
+
+}  // namespace hpd

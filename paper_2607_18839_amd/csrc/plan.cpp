@@ -1,0 +1,238 @@
+// Host planner of the branch-parallel decode step (plain C++17, no HIP).
+//
+// Turns a ragged batch description into the canonical bookkeeping of one step
+// and the work lists of the attention kernels.  The method batches every
+// active branch of every page into one forward (Algorithm 1, the parallel
+// draft over the active pool); each branch sees its page's shared prefix and
+// its own rows only (section "Layout-Coordinated Parallel Decoding",
+// paragraph "Dynamic Branch Forking and Efficient Context Isolation"), and its
+// k drafts are causal among themselves (section "Integration with P-MTP").
+//
+// Partial softmax slots: every (token, query head) output row receives one
+// partial (O, lse) per shared key split of its page and one per private key
+// chunk of its branch.  token_slots[t] = (first slot, slot count); partial row
+// index = (first + i) * Hq + h.  The merge kernel reduces them.
+#include "plan.h"
+
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <cstring>
+
+namespace hpd {
+namespace {
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+hpd_status fail(std::string *err, hpd_status st, const std::string &msg) {
+  if (err) *err = msg;
+  return st;
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace
+
+hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Plan *out,
+                      std::string *err) {
+  if (!attn || !batch || !out) return fail(err, HPD_ERR_INVALID_ARGUMENT, "NULL descriptor");
+  const hpd_attn_desc &a = *attn;
+  if (a.head_dim != HPD_HEAD_DIM)
+    return fail(err, HPD_ERR_UNSUPPORTED, "head_dim must be 64, got " + std::to_string(a.head_dim));
+  if (a.num_q_heads < 1 || a.num_q_heads > HPD_MAX_Q_HEADS)
+    return fail(err, HPD_ERR_INVALID_ARGUMENT, "num_q_heads out of range");
+  if (a.num_kv_heads < 1 || a.num_q_heads % a.num_kv_heads != 0)
+    return fail(err, HPD_ERR_INVALID_ARGUMENT, "num_q_heads must be a positive multiple of num_kv_heads");
+  if (a.num_q_heads / a.num_kv_heads > HPD_MAX_GROUP)
+    return fail(err, HPD_ERR_UNSUPPORTED, "num_q_heads / num_kv_heads exceeds HPD_MAX_GROUP");
+  if ((a.dtype != HPD_F32 && a.dtype != HPD_BF16) || (a.out_dtype != HPD_F32 && a.out_dtype != HPD_BF16))
+    return fail(err, HPD_ERR_INVALID_ARGUMENT, "dtype / out_dtype must be HPD_F32 or HPD_BF16");
+  if (std::isnan(a.softmax_scale) || std::isinf(a.softmax_scale))
+    return fail(err, HPD_ERR_INVALID_ARGUMENT, "softmax_scale is not finite");
+
+  const hpd_batch_desc &b = *batch;
+  if (b.num_pages < 1) return fail(err, HPD_ERR_INVALID_ARGUMENT, "num_pages must be >= 1");
+  if (b.num_branches < 1) return fail(err, HPD_ERR_INVALID_ARGUMENT, "num_branches must be >= 1");
+  if (!b.prefix_len || !b.branch_page || !b.num_new || !b.past_len)
+    return fail(err, HPD_ERR_INVALID_ARGUMENT, "NULL required batch array");
+
+  Plan P;
+  P.attn = a;
+  P.G = a.num_q_heads / a.num_kv_heads;
+  P.scale = a.softmax_scale > 0.f ? a.softmax_scale : 1.0f / std::sqrt((float)a.head_dim);
+  P.num_pages = b.num_pages;
+  P.num_branches = b.num_branches;
+  const int np = b.num_pages, nb = b.num_branches, Hq = a.num_q_heads, Hkv = a.num_kv_heads,
+            G = P.G;
+
+  P.prefix_len.assign(b.prefix_len, b.prefix_len + np);
+  P.branch_page.assign(b.branch_page, b.branch_page + nb);
+  P.num_new.assign(b.num_new, b.num_new + nb);
+  P.past_len.assign(b.past_len, b.past_len + nb);
+
+  // ---- validation of the ragged structure
+  for (int p = 0; p < np; ++p)
+    if (P.prefix_len[p] < 0)
+      return fail(err, HPD_ERR_INVALID_ARGUMENT, "prefix_len[" + std::to_string(p) + "] < 0");
+  for (int i = 0; i < nb; ++i) {
+    const std::string at = "[" + std::to_string(i) + "]";
+    if (P.branch_page[i] < 0 || P.branch_page[i] >= np)
+      return fail(err, HPD_ERR_INVALID_ARGUMENT, "branch_page" + at + " out of range");
+    if (i > 0 && P.branch_page[i] < P.branch_page[i - 1])
+      return fail(err, HPD_ERR_INVALID_ARGUMENT, "branch_page must be non-decreasing");
+    if (P.num_new[i] < 1 || P.num_new[i] > HPD_MAX_K)
+      return fail(err, HPD_ERR_INVALID_ARGUMENT, "num_new" + at + " must be in 1..HPD_MAX_K");
+    if (P.past_len[i] < 0) return fail(err, HPD_ERR_INVALID_ARGUMENT, "past_len" + at + " < 0");
+  }
+  P.fork.resize(nb);
+  P.has_fork = b.fork_len != nullptr;
+  for (int i = 0; i < nb; ++i) {
+    const int Pp = P.prefix_len[P.branch_page[i]];
+    int F = Pp;
+    if (b.fork_len) {
+      F = b.fork_len[i];
+      if (F < 0 || F > Pp)
+        return fail(err, HPD_ERR_INVALID_ARGUMENT,
+                    "fork_len[" + std::to_string(i) + "] must be in 0..prefix_len of its page");
+    }
+    P.fork[i] = F;
+  }
+
+  // ---- canonical bookkeeping
+  P.prefix_row.resize(np);
+  int64_t acc = 0;
+  for (int p = 0; p < np; ++p) {
+    P.prefix_row[p] = b.prefix_row ? b.prefix_row[p] : acc;
+    if (P.prefix_row[p] < 0) return fail(err, HPD_ERR_INVALID_ARGUMENT, "prefix_row < 0");
+    acc += P.prefix_len[p];
+    P.shared_rows = std::max<int64_t>(P.shared_rows, P.prefix_row[p] + P.prefix_len[p]);
+  }
+  P.priv_row.resize(nb);
+  P.q_row.resize(nb);
+  acc = 0;
+  int64_t tacc = 0;
+  for (int i = 0; i < nb; ++i) {
+    const int64_t rows = (int64_t)P.past_len[i] + P.num_new[i];
+    P.priv_row[i] = b.priv_row ? b.priv_row[i] : acc;
+    if (P.priv_row[i] < 0) return fail(err, HPD_ERR_INVALID_ARGUMENT, "priv_row < 0");
+    acc += rows;
+    P.priv_rows = std::max<int64_t>(P.priv_rows, P.priv_row[i] + rows);
+    P.q_row[i] = (int32_t)tacc;
+    tacc += P.num_new[i];
+    if (tacc > INT32_MAX / HPD_MAX_Q_HEADS)
+      return fail(err, HPD_ERR_INVALID_ARGUMENT, "too many query tokens");
+  }
+  if (P.shared_rows > INT32_MAX || P.priv_rows > INT32_MAX)
+    return fail(err, HPD_ERR_INVALID_ARGUMENT, "K/V row index exceeds 2^31 - 1");
+  P.T = (int)tacc;
+  P.page_T.assign(np, 0);
+  for (int i = 0; i < nb; ++i) P.page_T[P.branch_page[i]] += P.num_new[i];
+  P.page_q_row.resize(np);
+  int32_t qacc = 0;
+  for (int p = 0; p < np; ++p) {
+    P.page_q_row[p] = qacc;
+    qacc += P.page_T[p];
+  }
+  P.visible.resize(P.T);
+  P.token_fork.resize(P.T);
+  for (int i = 0; i < nb; ++i)
+    for (int j = 0; j < P.num_new[i]; ++j) {
+      P.visible[P.q_row[i] + j] = P.fork[i] + P.past_len[i] + j + 1;
+      P.token_fork[P.q_row[i] + j] = P.fork[i];
+    }
+
+  // ---- partial slots per token
+  std::vector<int32_t> page_splits(np);
+  for (int p = 0; p < np; ++p)
+    page_splits[p] = (int32_t)ceil_div(P.prefix_len[p], kSharedSplitKeys);
+  P.token_slots.resize(2 * (size_t)P.T);
+  int64_t slot = 0;
+  for (int i = 0; i < nb; ++i) {
+    const int chunks = (int)ceil_div((int64_t)P.past_len[i] + P.num_new[i], kPrivateChunkKeys);
+    const int cnt = page_splits[P.branch_page[i]] + chunks;
+    for (int j = 0; j < P.num_new[i]; ++j) {
+      P.token_slots[2 * (size_t)(P.q_row[i] + j)] = (int32_t)slot;
+      P.token_slots[2 * (size_t)(P.q_row[i] + j) + 1] = cnt;
+      slot += cnt;
+    }
+  }
+  P.num_slots = slot;
+  if (P.num_slots * Hq > INT32_MAX)
+    return fail(err, HPD_ERR_INVALID_ARGUMENT, "too many partial rows");
+
+  // ---- shared-prefix work items: (page, kv head, key split, row group);
+  // items that read the same key range are adjacent.
+  const int group_rows = kSharedWaves * kTileRows;
+  for (int p = 0; p < np; ++p) {
+    const int Pp = P.prefix_len[p];
+    const int R = P.page_T[p] * G;
+    if (Pp == 0 || R == 0) continue;
+    for (int g = 0; g < Hkv; ++g)
+      for (int s = 0; s < page_splits[p]; ++s)
+        for (int r0 = 0; r0 < R; r0 += group_rows) {
+          const int nr = std::min(group_rows, R - r0);
+          const int k0 = s * kSharedSplitKeys, k1 = std::min(Pp, k0 + kSharedSplitKeys);
+          int flags = 0;
+          if (P.has_fork)
+            for (int r = r0; r < r0 + nr; ++r)
+              if (P.token_fork[P.page_q_row[p] + r / G] < k1) flags |= SI_FLAG_FORK;
+          int32_t it[SI_NFIELDS] = {};
+          it[SI_PAGE] = p; it[SI_KVH] = g; it[SI_ROW0] = r0; it[SI_NROWS] = nr;
+          it[SI_KEY0] = k0; it[SI_KEY1] = k1; it[SI_SLOT] = s; it[SI_FLAGS] = flags;
+          it[SI_PREFIX_ROW] = (int32_t)P.prefix_row[p]; it[SI_PAGE_Q_ROW] = P.page_q_row[p];
+          it[SI_PAGE_ROWS] = R;
+          P.shared_items.insert(P.shared_items.end(), it, it + SI_NFIELDS);
+        }
+  }
+
+  // ---- private work items: (branch, kv head, row tile, key chunk)
+  for (int i = 0; i < nb; ++i) {
+    const int keys = P.past_len[i] + P.num_new[i];
+    const int R = P.num_new[i] * G;
+    const int splits = page_splits[P.branch_page[i]];
+    for (int g = 0; g < Hkv; ++g)
+      for (int r0 = 0; r0 < R; r0 += kTileRows)
+        for (int c = 0; c * kPrivateChunkKeys < keys; ++c) {
+          int32_t it[PI_NFIELDS] = {};
+          it[PI_BRANCH] = i; it[PI_KVH] = g; it[PI_ROW0] = r0;
+          it[PI_NROWS] = std::min(kTileRows, R - r0);
+          it[PI_KEY0] = c * kPrivateChunkKeys;
+          it[PI_KEY1] = std::min(keys, (c + 1) * kPrivateChunkKeys);
+          it[PI_SLOT] = splits + c; it[PI_PAST] = P.past_len[i];
+          it[PI_PRIV_ROW] = (int32_t)P.priv_row[i]; it[PI_Q_ROW] = P.q_row[i];
+          it[PI_NUM_NEW] = P.num_new[i];
+          P.private_items.insert(P.private_items.end(), it, it + PI_NFIELDS);
+        }
+  }
+
+  // ---- workspace layout: tables (uploaded once) then partials
+  size_t off = 0;
+  P.off_shared_items = off;
+  off = align256(off + P.shared_items.size() * sizeof(int32_t));
+  P.off_private_items = off;
+  off = align256(off + P.private_items.size() * sizeof(int32_t));
+  P.off_token_slots = off;
+  off = align256(off + P.token_slots.size() * sizeof(int32_t));
+  P.off_token_fork = off;
+  off = align256(off + P.token_fork.size() * sizeof(int32_t));
+  P.table_bytes = off;
+  P.off_part_o = off;
+  off = align256(off + (size_t)P.num_slots * Hq * HPD_HEAD_DIM * sizeof(float));
+  P.off_part_lse = off;
+  off = align256(off + (size_t)P.num_slots * Hq * sizeof(float));
+  P.workspace_bytes = off;
+
+  P.table_image.assign(P.table_bytes, 0);
+  auto put = [&](size_t at, const std::vector<int32_t> &v) {
+    if (!v.empty()) std::memcpy(P.table_image.data() + at, v.data(), v.size() * sizeof(int32_t));
+  };
+  put(P.off_shared_items, P.shared_items);
+  put(P.off_private_items, P.private_items);
+  put(P.off_token_slots, P.token_slots);
+  put(P.off_token_fork, P.token_fork);
+
+  *out = std::move(P);
+  return HPD_OK;
+}
+
+}  // namespace hpd

@@ -1,0 +1,74 @@
+// Internal plan structure shared by the planner (host C++) and the launchers.
+// Not part of the public ABI: callers see only the opaque hpd_plan.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "hpd.h"
+
+namespace hpd {
+
+// Work item of the shared-prefix kernel: one workgroup of kSharedWaves waves,
+// each wave one 32-row tile of the stacked query rows of (page, kv head), all
+// of them over the same prefix key range [key_begin, key_end).
+// Stacked row r of (page p, kv head g) is query head g * G + r % G of token
+// page_q_row[p] + r / G.
+enum SharedItemField {
+  SI_PAGE = 0, SI_KVH, SI_ROW0, SI_NROWS, SI_KEY0, SI_KEY1, SI_SLOT, SI_FLAGS,
+  SI_PREFIX_ROW, SI_PAGE_Q_ROW, SI_PAGE_ROWS, SI_RESERVED, SI_NFIELDS
+};
+// Work item of the private kernel: one wave, one 32-row tile of the stacked
+// rows of (branch, kv head), private keys [key_begin, key_end) of the branch.
+// Stacked row r of (branch b, kv head g) is query head g * G + r % G of the
+// branch's new token j = r / G, which sees private keys 0 .. L_b + j.
+enum PrivateItemField {
+  PI_BRANCH = 0, PI_KVH, PI_ROW0, PI_NROWS, PI_KEY0, PI_KEY1, PI_SLOT, PI_PAST,
+  PI_PRIV_ROW, PI_Q_ROW, PI_NUM_NEW, PI_RESERVED, PI_NFIELDS
+};
+
+constexpr int kSharedWaves = 4;      // waves per shared-prefix workgroup
+constexpr int kTileRows = 32;        // stacked query rows per wave (MFMA 32x32)
+constexpr int kKeyTile = 64;         // keys per LDS tile
+constexpr int kSharedSplitKeys = 256;   // prefix keys per shared work item
+constexpr int kPrivateChunkKeys = 128;  // private keys per private work item
+constexpr int SI_FLAG_FORK = 1;      // rows have their own fork limits
+
+struct Plan {
+  hpd_attn_desc attn{};
+  int G = 0;                // query heads per kv head
+  float scale = 0.f;        // softmax scale actually used
+  int T = 0, num_pages = 0, num_branches = 0;
+  bool has_fork = false;
+
+  std::vector<int32_t> prefix_len, branch_page, num_new, past_len, fork;
+  std::vector<int64_t> prefix_row, priv_row;
+  std::vector<int32_t> q_row, page_q_row, page_T, visible;
+  int64_t shared_rows = 0, priv_rows = 0;
+
+  std::vector<int32_t> shared_items, private_items;   // [n][SI_NFIELDS / PI_NFIELDS]
+  std::vector<int32_t> token_slots;                   // [T][2]: first slot, count
+  std::vector<int32_t> token_fork;                    // [T] visible prefix per token
+  int64_t num_slots = 0;                              // partial rows = num_slots * Hq
+
+  // device workspace layout (byte offsets, 256-aligned)
+  size_t off_shared_items = 0, off_private_items = 0, off_token_slots = 0,
+         off_token_fork = 0, off_part_o = 0, off_part_lse = 0, table_bytes = 0,
+         workspace_bytes = 0;
+  std::vector<unsigned char> table_image;             // host copy of [0, table_bytes)
+
+  int num_shared_items() const { return (int)(shared_items.size() / SI_NFIELDS); }
+  int num_private_items() const { return (int)(private_items.size() / PI_NFIELDS); }
+};
+
+// Builds the plan; on failure returns a status and sets *err.
+hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Plan *out,
+                      std::string *err);
+
+}  // namespace hpd
+
+struct hpd_plan {
+  hpd::Plan p;
+};

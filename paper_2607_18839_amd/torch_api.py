@@ -1,0 +1,56 @@
+"""torch-facing wrappers: allocate device memory with torch, call the C ABI.
+
+Nothing here computes any part of the step; it only sizes and allocates
+buffers and passes pointers and the current HIP stream.
+"""
+import torch
+
+from . import _lib
+
+DT = {torch.bfloat16: _lib.HPD_BF16, torch.float32: _lib.HPD_F32}
+
+
+def _stream(stream):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _p(t):
+    return None if t is None else t.data_ptr()
+
+
+class BranchAttention:
+    """One attention layer of the branch-parallel step for a fixed batch shape.
+
+    The plan (bookkeeping + work lists) is built once on the host and copied
+    into a torch-allocated device workspace; each call launches the kernels.
+    """
+
+    def __init__(self, num_q_heads, num_kv_heads, prefix_len, branch_page, num_new, past_len,
+                 dtype=torch.bfloat16, out_dtype=None, fork_len=None, prefix_row=None,
+                 priv_row=None, softmax_scale=0.0, device="cuda", stream=None):
+        self.dtype = dtype
+        self.out_dtype = dtype if out_dtype is None else out_dtype
+        self.num_q_heads = num_q_heads
+        self.plan = _lib.hpd_plan_create(num_q_heads, num_kv_heads, prefix_len, branch_page, num_new,
+                                         past_len, softmax_scale=softmax_scale, dtype=DT[dtype],
+                                         out_dtype=DT[self.out_dtype], prefix_row=prefix_row,
+                                         priv_row=priv_row, fork_len=fork_len)
+        self.info = _lib.hpd_plan_query(self.plan)
+        self.T = self.info["T"]
+        self.ws_bytes = self.plan.workspace_bytes
+        self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=device)
+        _lib.hpd_plan_upload(self.plan, self.workspace.data_ptr(), self.ws_bytes, _stream(stream))
+
+    def __call__(self, q, shared_k, shared_v, priv_k, priv_v, out=None, lse=None, stream=None):
+        if out is None:
+            out = torch.empty((self.T, self.num_q_heads, _lib.HPD_HEAD_DIM), dtype=self.out_dtype,
+                              device=q.device)
+        for name, t in (("q", q), ("shared_k", shared_k), ("shared_v", shared_v), ("priv_k", priv_k),
+                        ("priv_v", priv_v)):
+            if t is not None and (t.dtype != self.dtype or not t.is_contiguous()):
+                raise ValueError(f"{name} must be a contiguous {self.dtype} tensor")
+        _lib.hpd_branch_attn_step(self.plan, _p(q), _p(shared_k), _p(shared_v), _p(priv_k), _p(priv_v),
+                                  _p(out), _p(lse), self.workspace.data_ptr(), self.ws_bytes,
+                                  _stream(stream))
+        return out

@@ -1,0 +1,150 @@
+"""C ABI without a GPU: symbols, host planner bookkeeping and validation."""
+
+import ctypes
+
+import numpy as np
+import pytest
+
+from oracle.plan import canonical_plan
+from paper_2607_18839_amd import _lib
+from workloads import get_config, make_structure
+
+from ._pins import tiny_structures
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return _lib.load()
+
+
+def test_library_exports_every_declared_symbol(lib):
+    names = _lib.declared_symbols()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), n
+        assert n in _lib.SIGNATURES, n
+
+
+def _structures():
+    out = [("tiny%d" % i, st) for i, st in enumerate(tiny_structures())]
+    for name in ("c1", "c2", "c3", "c5"):
+        for seed in (0, 1, 2):
+            out.append((f"{name}/{seed}", make_structure(get_config(name), np.random.default_rng(seed))))
+    return out
+
+
+def _plan(st, Hq=16, Hkv=2, **kw):
+    return _lib.hpd_plan_create(Hq, Hkv, st["prefix_len"], st["branch_page"], st["num_new"],
+                                st["past_len"], **kw)
+
+
+@pytest.mark.parametrize("name,st", _structures(), ids=lambda x: x if isinstance(x, str) else "")
+def test_bookkeeping_bit_exact_vs_oracle(name, st):
+    info = _lib.hpd_plan_query(_plan(st))
+    cp = canonical_plan(st["prefix_len"], st["branch_page"], st["num_new"], st["past_len"])
+    assert info["T"] == cp["T"]
+    for k in ("q_row", "priv_row", "prefix_row", "page_q_row", "page_T", "visible"):
+        got = info[k].astype(np.int64)
+        assert got.dtype == cp[k].dtype and np.array_equal(got, cp[k]), k
+    assert info["priv_rows"] == cp["priv_rows_total"]
+    assert info["shared_rows"] == cp["shared_rows_total"]
+
+
+@pytest.mark.parametrize("name,st", _structures(), ids=lambda x: x if isinstance(x, str) else "")
+@pytest.mark.parametrize("Hq,Hkv", [(16, 2), (8, 2), (4, 4)])
+def test_work_lists_cover_every_key_once(name, st, Hq, Hkv):
+    """Each (token, query head) row meets each visible shared key and each of
+    its branch's private keys in exactly one work item, and each of its
+    partial slots is written by exactly one item."""
+    G = Hq // Hkv
+    info = _lib.hpd_plan_query(_plan(st, Hq, Hkv))
+    T = info["T"]
+    P = st["prefix_len"].astype(np.int64)
+    cp = canonical_plan(st["prefix_len"], st["branch_page"], st["num_new"], st["past_len"])
+    slot_writes = np.zeros((info["num_partial_slots"], Hq), np.int64)
+    shared_cov = [np.zeros((Hq, P[cp["token_branch"][t] * 0 + st["branch_page"][cp["token_branch"][t]]]), np.int64)
+                  for t in range(T)]
+    S, Pi = _lib.SI, _lib.PI
+    for it in info["shared_items"]:
+        p, g = it[S["page"]], it[S["kvh"]]
+        assert it[S["page_q_row"]] == cp["page_q_row"][p] and it[S["prefix_row"]] == cp["prefix_row"][p]
+        for r in range(it[S["row0"]], it[S["row0"]] + it[S["nrows"]]):
+            t = cp["page_q_row"][p] + r // G
+            h = g * G + r % G
+            assert st["branch_page"][cp["token_branch"][t]] == p
+            shared_cov[t][h, it[S["key0"]]:it[S["key1"]]] += 1
+            first, cnt = info["token_slots"][t]
+            assert 0 <= it[S["slot"]] < cnt
+            slot_writes[first + it[S["slot"]], h] += 1
+    priv_cov = [np.zeros((Hq, st["past_len"][cp["token_branch"][t]] + st["num_new"][cp["token_branch"][t]]), np.int64)
+                for t in range(T)]
+    for it in info["private_items"]:
+        b, g = it[Pi["branch"]], it[Pi["kvh"]]
+        assert it[Pi["priv_row"]] == cp["priv_row"][b] and it[Pi["q_row"]] == cp["q_row"][b]
+        assert it[Pi["past"]] == st["past_len"][b] and it[Pi["num_new"]] == st["num_new"][b]
+        for r in range(it[Pi["row0"]], it[Pi["row0"]] + it[Pi["nrows"]]):
+            t = cp["q_row"][b] + r // G
+            h = g * G + r % G
+            priv_cov[t][h, it[Pi["key0"]]:it[Pi["key1"]]] += 1
+            first, cnt = info["token_slots"][t]
+            assert 0 <= it[Pi["slot"]] < cnt
+            slot_writes[first + it[Pi["slot"]], h] += 1
+    for t in range(T):
+        assert np.all(shared_cov[t] == 1) and np.all(priv_cov[t] == 1)
+    assert np.all(slot_writes == 1)
+    first = info["token_slots"][:, 0]
+    assert first[0] == 0 and np.all(first[1:] == first[:-1] + info["token_slots"][:-1, 1])
+
+
+BAD = [
+    (dict(num_kv_heads=3), "multiple"),
+    (dict(head_dim=128), "head_dim"),
+    (dict(num_new=[0, 4, 4]), "num_new"),
+    (dict(num_new=[17, 4, 4]), "num_new"),
+    (dict(past_len=[-1, 4, 4]), "past_len"),
+    (dict(branch_page=[0, 1, 0], prefix_len=[8, 8]), "non-decreasing"),
+    (dict(branch_page=[0, 0, 5]), "branch_page"),
+    (dict(prefix_len=[-5]), "prefix_len"),
+    (dict(fork_len=[9, 0, 0]), "fork_len"),
+    (dict(fork_len=[-1, 0, 0]), "fork_len"),
+    (dict(dtype=7), "dtype"),
+    (dict(num_q_heads=128, num_kv_heads=2), "num_q_heads"),
+    (dict(num_q_heads=64, num_kv_heads=1), "HPD_MAX_GROUP"),
+    (dict(priv_row=[0, 5, -3]), "priv_row"),
+    (dict(priv_row=[0, 5, 2 ** 31]), "2^31"),
+    (dict(softmax_scale=float("nan")), "finite"),
+]
+
+
+@pytest.mark.parametrize("over,needle", BAD, ids=[n for _, n in BAD])
+def test_validation_errors(over, needle):
+    kw = dict(num_q_heads=16, num_kv_heads=2, prefix_len=[8], branch_page=[0, 0, 0],
+              num_new=[1, 4, 4], past_len=[3, 0, 5])
+    kw.update(over)
+    with pytest.raises(_lib.HpdError) as e:
+        _lib.hpd_plan_create(**kw)
+    assert needle in str(e.value)
+    assert e.value.status in (1, 2)
+
+
+def test_null_arguments_are_rejected(lib):
+    assert lib.hpd_plan_create(None, None, None) == 1
+    assert lib.hpd_plan_query(None, None) == 1
+    plan = _plan(tiny_structures()[0])
+    assert lib.hpd_branch_attn_step(plan.handle, None, None, None, None, None, None, None, None, 0, None) == 1
+    assert b"NULL" in lib.hpd_last_error_message()
+    # a workspace that is too small is reported before anything is launched
+    fake = ctypes.c_void_p(256)
+    assert lib.hpd_branch_attn_step(plan.handle, fake, fake, fake, fake, fake, fake, None, fake, 16, None) == 3
+    assert lib.hpd_status_string(3) == b"HPD_ERR_WORKSPACE_TOO_SMALL"
+    assert lib.hpd_plan_upload(plan.handle, fake, 16, None) == 3
+
+
+def test_custom_row_offsets_are_kept():
+    st = tiny_structures()[1]
+    pr = np.array([100, 7, 40], np.int64)
+    vr = np.array([0, 30, 60, 90], np.int64)
+    info = _lib.hpd_plan_query(_plan(st, 4, 2, prefix_row=pr, priv_row=vr))
+    assert np.array_equal(info["prefix_row"], pr) and np.array_equal(info["priv_row"], vr)
+    assert info["shared_rows"] == max(pr + st["prefix_len"])
+    assert info["priv_rows"] == max(vr + st["past_len"] + st["num_new"])
