@@ -114,8 +114,8 @@ typedef struct {
   int64_t priv_rows;              /* rows priv_k/v must hold (max end row)     */
   int32_t num_shared_items;       /* work items of the shared-prefix kernel    */
   int32_t num_private_items;      /* work items of the private kernel          */
-  const int32_t *shared_items;    /* [num_shared_items][8] see plan.cpp        */
-  const int32_t *private_items;   /* [num_private_items][8] see plan.cpp       */
+  const int32_t *shared_items;    /* [num_shared_items][12] fields: csrc/plan.h  */
+  const int32_t *private_items;   /* [num_private_items][12] fields: csrc/plan.h */
   const int32_t *token_slots;     /* [T][2] first partial slot, slot count     */
   int64_t num_partial_slots;      /* partial (O, lse) rows = slots * Hq        */
 } hpd_plan_info;
@@ -198,6 +198,26 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan,
                            const void *const *shared_k, const void *const *shared_v,
                            void *const *priv_k, void *const *priv_v,
                            void *workspace, size_t workspace_bytes, void *stream);
+
+/* ---- Benchmark support: per-kernel timing with HIP events.
+ * When enabled, every kernel a step enqueues is bracketed by a pair of HIP
+ * events recorded on that kernel's own stream; hpd_kernel_times_read waits
+ * for them and returns, per kernel kind, the number of launches and the sum
+ * of their elapsed times since the previous read.  The event pool
+ * (max_launches pairs) is created by hpd_kernel_timing(1, n), outside any
+ * timed region; launches beyond it are counted in `dropped`.  Timing adds
+ * two event records per launch and must not be enabled under graph capture. */
+#define HPD_NUM_KERNEL_KINDS 8
+typedef struct {
+  int64_t count[HPD_NUM_KERNEL_KINDS];
+  double total_ms[HPD_NUM_KERNEL_KINDS];
+  int64_t dropped;
+} hpd_kernel_times;
+hpd_status hpd_kernel_timing(int enable, int max_launches);
+hpd_status hpd_kernel_times_read(hpd_kernel_times *out);
+/* Kind k: 0 shared_prefix, 1 private, 2 merge, 3 gemm_qkv, 4 gemm_o,
+ * 5 gemm_gate_up, 6 gemm_down, 7 norm. */
+const char *hpd_kernel_kind_name(int kind);
 
 const char *hpd_status_string(hpd_status status);
 const char *hpd_last_error_message(void);

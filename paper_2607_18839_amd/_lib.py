@@ -84,6 +84,9 @@ SIGNATURES = {
     "hpd_decode_step": (ctypes.c_int, [ctypes.POINTER(hpd_model_desc), ctypes.c_void_p, ctypes.c_void_p,
                                        ctypes.c_void_p, PP, PP, PP, PP, ctypes.c_void_p, ctypes.c_size_t,
                                        ctypes.c_void_p]),
+    "hpd_kernel_timing": (ctypes.c_int, [ctypes.c_int, ctypes.c_int]),
+    "hpd_kernel_times_read": (ctypes.c_int, [ctypes.c_void_p]),
+    "hpd_kernel_kind_name": (ctypes.c_char_p, [ctypes.c_int]),
     "hpd_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "hpd_last_error_message": (ctypes.c_char_p, []),
 }
@@ -218,6 +221,29 @@ def hpd_decode_step(model, plan, hidden_in, hidden_out, shared_k, shared_v, priv
     _check(load().hpd_decode_step(ctypes.byref(model), plan.handle, hidden_in, hidden_out,
                                   *[ctypes.cast(a, PP) for a in arrs], workspace, workspace_bytes,
                                   stream), "hpd_decode_step")
+
+
+HPD_NUM_KERNEL_KINDS = 8
+
+
+class hpd_kernel_times(ctypes.Structure):
+    _fields_ = [("count", ctypes.c_int64 * HPD_NUM_KERNEL_KINDS),
+                ("total_ms", ctypes.c_double * HPD_NUM_KERNEL_KINDS), ("dropped", ctypes.c_int64)]
+
+
+def hpd_kernel_timing(enable, max_launches=8192):
+    _check(load().hpd_kernel_timing(int(bool(enable)), max_launches), "hpd_kernel_timing")
+
+
+def hpd_kernel_times_read():
+    """{kind name: (launch count, total ms)} since the previous read."""
+    t = hpd_kernel_times()
+    _check(load().hpd_kernel_times_read(ctypes.byref(t)), "hpd_kernel_times_read")
+    lib = load()
+    out = {lib.hpd_kernel_kind_name(k).decode(): (int(t.count[k]), float(t.total_ms[k]))
+           for k in range(HPD_NUM_KERNEL_KINDS)}
+    out["_dropped"] = (int(t.dropped), 0.0)
+    return out
 
 
 def declared_symbols(header=None):

@@ -19,7 +19,7 @@ LIB = os.path.join(PKG, "libhpd.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-HIP_SOURCES = ["attn_kernels.hip", "gemm_kernels.hip", "decode.hip", "api.hip"]
+HIP_SOURCES = ["attn_kernels.hip", "gemm_kernels.hip", "decode.hip", "timing.hip", "api.hip"]
 CXX_SOURCES = ["plan.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-I" + os.path.join(ROOT, "include"), "-I" + CSRC]

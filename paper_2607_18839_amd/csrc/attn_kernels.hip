@@ -463,21 +463,27 @@ hipError_t launch_branch_attention(const Plan &P, const void *q, const void *sha
   const bool bf16 = P.attn.dtype == HPD_BF16;
   if (a.n_shared > 0) {
     const int grid = (a.n_shared + 7) / 8 * 8;
+    timed_begin(KK_SHARED, stream);
     if (bf16) hipLaunchKernelGGL(shared_prefix_kernel<__bf16>, dim3(grid), dim3(256), 0, stream, a);
     else hipLaunchKernelGGL(shared_prefix_kernel<float>, dim3(grid), dim3(256), 0, stream, a);
+    timed_end(stream);
   }
   if (a.n_private > 0) {
+    timed_begin(KK_PRIVATE, stream);
     if (bf16) hipLaunchKernelGGL(private_kernel<__bf16>, dim3(a.n_private), dim3(64), 0, stream, a);
     else hipLaunchKernelGGL(private_kernel<float>, dim3(a.n_private), dim3(64), 0, stream, a);
+    timed_end(stream);
   }
   const int rows = P.T * P.attn.num_q_heads;
   const int mgrid = (rows + 15) / 16;
+  timed_begin(KK_MERGE, stream);
   if (P.attn.out_dtype == HPD_BF16)
     hipLaunchKernelGGL(merge_kernel<__bf16>, dim3(mgrid), dim3(256), 0, stream, a.dev, (__bf16 *)out, lse,
                        P.T, P.attn.num_q_heads);
   else
     hipLaunchKernelGGL(merge_kernel<float>, dim3(mgrid), dim3(256), 0, stream, a.dev, (float *)out, lse,
                        P.T, P.attn.num_q_heads);
+  timed_end(stream);
   return hipGetLastError();
 }
 

@@ -19,6 +19,12 @@ struct PlanDev {
 
 PlanDev plan_dev(const Plan &P, void *workspace);
 
+// Kernel kinds of the optional benchmark timing (hpd_kernel_timing).
+enum KernelKind { KK_SHARED = 0, KK_PRIVATE, KK_MERGE, KK_GEMM_QKV, KK_GEMM_O, KK_GEMM_GATE_UP,
+                  KK_GEMM_DOWN, KK_NORM };
+void timed_begin(int kind, hipStream_t stream);
+void timed_end(hipStream_t stream);
+
 // One attention layer: shared-prefix kernel, private kernel, merge kernel.
 // q/k/v in P.attn.dtype; out in P.attn.out_dtype; lse may be NULL.
 hipError_t launch_branch_attention(const Plan &P, const void *q, const void *shared_k,

@@ -1,0 +1,104 @@
+// Optional per-kernel timing with HIP events, for benchmarks.
+//
+// When enabled, every launcher brackets each kernel it enqueues with a pair
+// of events recorded on the kernel's own stream.  Events come from a pool
+// created when timing is switched on, so the timed region creates nothing.
+#include <hip/hip_runtime.h>
+
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+
+namespace hpd {
+namespace {
+
+struct Pair {
+  hipEvent_t start, stop;
+  int kind;
+};
+
+std::mutex g_mu;
+bool g_enabled = false;
+std::vector<Pair> g_pool;
+size_t g_used = 0;
+double g_total_ms[HPD_NUM_KERNEL_KINDS] = {};
+int64_t g_count[HPD_NUM_KERNEL_KINDS] = {};
+int64_t g_dropped = 0;
+thread_local int t_open = -1;   // pool index of the pair opened by this thread
+
+const char *kKindNames[HPD_NUM_KERNEL_KINDS] = {
+    "shared_prefix", "private", "merge", "gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down", "norm"};
+
+}  // namespace
+
+void timed_begin(int kind, hipStream_t stream) {
+  if (!g_enabled) return;
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (g_used >= g_pool.size()) {
+    ++g_dropped;
+    t_open = -1;
+    return;
+  }
+  t_open = (int)g_used++;
+  g_pool[t_open].kind = kind;
+  hipEventRecord(g_pool[t_open].start, stream);
+}
+
+void timed_end(hipStream_t stream) {
+  if (!g_enabled || t_open < 0) return;
+  hipEventRecord(g_pool[t_open].stop, stream);
+  t_open = -1;
+}
+
+}  // namespace hpd
+
+extern "C" {
+
+hpd_status hpd_kernel_timing(int enable, int max_launches) {
+  std::lock_guard<std::mutex> lk(hpd::g_mu);
+  if (enable) {
+    if (max_launches < 1) return HPD_ERR_INVALID_ARGUMENT;
+    for (auto &p : hpd::g_pool) { hipEventDestroy(p.start); hipEventDestroy(p.stop); }
+    hpd::g_pool.assign(max_launches, hpd::Pair{});
+    for (auto &p : hpd::g_pool) {
+      if (hipEventCreate(&p.start) != hipSuccess || hipEventCreate(&p.stop) != hipSuccess)
+        return HPD_ERR_HIP;
+    }
+    hpd::g_used = 0;
+    hpd::g_enabled = true;
+  } else {
+    hpd::g_enabled = false;
+  }
+  return HPD_OK;
+}
+
+hpd_status hpd_kernel_times_read(hpd_kernel_times *out) {
+  if (!out) return HPD_ERR_INVALID_ARGUMENT;
+  std::lock_guard<std::mutex> lk(hpd::g_mu);
+  for (size_t i = 0; i < hpd::g_used; ++i) {
+    hpd::Pair &p = hpd::g_pool[i];
+    if (hipEventSynchronize(p.stop) != hipSuccess) return HPD_ERR_HIP;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, p.start, p.stop) != hipSuccess) return HPD_ERR_HIP;
+    hpd::g_total_ms[p.kind] += ms;
+    hpd::g_count[p.kind] += 1;
+  }
+  hpd::g_used = 0;
+  for (int k = 0; k < HPD_NUM_KERNEL_KINDS; ++k) {
+    out->total_ms[k] = hpd::g_total_ms[k];
+    out->count[k] = hpd::g_count[k];
+    hpd::g_total_ms[k] = 0.0;
+    hpd::g_count[k] = 0;
+  }
+  out->dropped = hpd::g_dropped;
+  hpd::g_dropped = 0;
+  return HPD_OK;
+}
+
+const char *hpd_kernel_kind_name(int kind) {
+  return (kind >= 0 && kind < HPD_NUM_KERNEL_KINDS) ? hpd::kKindNames[kind] : "unknown";
+}
+
+}  // extern "C"
