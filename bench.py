@@ -202,8 +202,102 @@ def cpu_attention(b, budget_s, T):
             "cpu": model, "cpus_available": ncpu}
 
 
+def gemm_work(T, Hq, Hkv, D, H, I):
+    """Algorithmic bytes of one launch of each projection kernel: weights once,
+    activations in and outputs out for the T real token rows."""
+    nq, nkv = Hq * D, Hkv * D
+    return {
+        "gemm_qkv": (nq + 2 * nkv) * H * 2 + T * H * 2 + T * (nq + 2 * nkv) * 2,
+        "gemm_o": H * nq * 2 + T * nq * 2 + 2 * T * H * 4,
+        "gemm_gate_up": 2 * I * H * 2 + 2 * T * H * 2 + 2 * T * I * 2,
+        "gemm_down": H * I * 2 + 2 * T * I * 2 + 2 * T * H * 4,
+        "norm": T * H * 4 + 2 * T * H * 2,
+    }
+
+
 def bench_decode(args, torch, _lib):
-    raise SystemExit("decode-step benchmark not built yet")
+    from paper_2607_18839_amd.torch_api import DecodeStep
+    from workloads import make_decode_inputs
+    inp = make_decode_inputs("c4", args.seed, num_layers=args.layers)
+
+    def dev(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    w = {k: [dev(a) for a in getattr(inp, k)] for k in ("w_qkv", "w_o", "w_gate", "w_up", "w_down")}
+    sk = [dev(a) for a in inp.shared_k]
+    sv = [dev(a) for a in inp.shared_v]
+    pk = [dev(a) for a in inp.priv_k]
+    pv = [dev(a) for a in inp.priv_v]
+    step_obj = DecodeStep(inp.num_q_heads, inp.num_kv_heads, inp.prefix_len, inp.branch_page, inp.num_new,
+                          inp.past_len, w, inp.hidden, inp.intermediate, inp.rms_eps)
+    h_in = torch.from_numpy(inp.hidden_in).cuda()
+    h_out = torch.empty_like(h_in)
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        step_obj(h_in, sk, sv, pk, pv, hidden_out=h_out)
+
+    ms = _time_steps(torch, step, args.steps, args.warmup, stream)
+    kern = _kernel_pass(torch, _lib, step, args.steps, args.warmup)
+    T, Hq, Hkv, D, H, I = step_obj.T, inp.num_q_heads, inp.num_kv_heads, 64, inp.hidden, inp.intermediate
+    aw = attn_work(inp.prefix_len, inp.branch_page, inp.num_new, inp.past_len, Hq, Hkv, D, 2, 2)
+    gw = gemm_work(T, Hq, Hkv, D, H, I)
+    for name, k in kern.items():
+        us = k["avg_us"]
+        if name == "shared_prefix":
+            k.update(bound="mfma", flop=aw["shared_flop"], tflops=aw["shared_flop"] / us / 1e6,
+                     frac=aw["shared_flop"] / us / 1e6 / BF16_PEAK_TFLOPS)
+        elif name == "private":
+            k.update(bound="hbm", bytes=aw["private_bytes"], gbs=aw["private_bytes"] / us / 1e3,
+                     frac=aw["private_bytes"] / us / 1e3 / HBM_PEAK_GBS)
+        elif name in gw:
+            k.update(bound="hbm", bytes=gw[name], gbs=gw[name] / us / 1e3, frac=gw[name] / us / 1e3 / HBM_PEAK_GBS)
+        k["total_us_per_step"] = us * k["launches"] / args.steps
+    dom = max(kern, key=lambda n: kern[n]["total_us_per_step"])
+    d = kern[dom]
+    if d.get("bound") == "mfma":
+        roof = {"bound": "mfma", "kernel": dom, "achieved": d["tflops"], "peak": BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": d["frac"], "traffic": None, "algorithmic_per_launch": d["flop"]}
+    else:
+        roof = {"bound": "hbm", "kernel": dom, "achieved": d.get("gbs"), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": d.get("frac"), "traffic": None, "algorithmic_per_launch": d.get("bytes")}
+    res = {
+        "metric": "branch-tokens/s per decode step", "value": T / (ms / 1e3), "unit": "branch-tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) KV and hidden, N(0,0.02) bf16 weights)",
+        "config": {"workload": "c4: full decode step, 18-layer synthetic decoder, 1 page, "
+                               "1 layout (k=1) + 32 content (k=4) branches, 4096-token shared prefix",
+                   "layers": inp.num_layers, "hidden": H, "intermediate": I, "heads": [Hq, Hkv, D],
+                   "branch_tokens": T, "branches": int(len(inp.num_new)), "prefix_len": int(inp.prefix_len[0]),
+                   "private_rows": int((inp.past_len + inp.num_new).sum())},
+        "roofline": roof, "kernels": kern,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_decode(inp, args.cpu_seconds, T)
+    return res
+
+
+def cpu_decode(inp, budget_s, T):
+    """The fp64 oracle on the first n layers of the same step (n sized to the
+    time budget), scaled to a whole step."""
+    from oracle.decode import decode_step
+    model, ncpu = _cpu_info()
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = ncpu
+    t0 = time.perf_counter()
+    decode_step(inp, num_layers=1)
+    t1 = time.perf_counter() - t0
+    n = int(max(1, min(inp.num_layers, budget_s // max(t1, 1e-3))))
+    t0 = time.perf_counter()
+    decode_step(inp, num_layers=n)
+    t = (time.perf_counter() - t0) * inp.num_layers / n
+    return {"value": T / t, "unit": "branch-tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {n} of {inp.num_layers} layers of the same step (fp64 numpy, BLAS matmuls), "
+                      f"scaled to the full step: {t:.2f} s/step",
+            "cpu": model, "cpus_available": ncpu}
 
 
 if __name__ == "__main__":

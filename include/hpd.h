@@ -165,10 +165,10 @@ hpd_status hpd_branch_attn_step(const hpd_plan *plan, const void *q, const void 
  * device arrays in torch Linear layout W[out][in]; each field points to a
  * HOST array of num_layers device pointers. */
 typedef struct {
-  int32_t num_layers;
-  int32_t hidden;               /* multiple of 64                              */
-  int32_t intermediate;         /* multiple of 64                              */
-  float rms_eps;                /* RMSNorm epsilon                             */
+  int32_t num_layers;           /* >= 1                                        */
+  int32_t hidden;               /* positive multiple of 128                    */
+  int32_t intermediate;         /* positive multiple of 128                    */
+  float rms_eps;                /* RMSNorm epsilon, 0..1                       */
   const void *const *w_qkv;     /* [L] -> [(Hq + 2 Hkv) D][hidden]: q rows, then k, then v */
   const void *const *w_o;       /* [L] -> [hidden][Hq D]                       */
   const void *const *w_gate;    /* [L] -> [intermediate][hidden]               */
@@ -179,7 +179,8 @@ typedef struct {
 } hpd_model_desc;
 
 /* Bytes of device workspace hpd_decode_step needs on top of
- * hpd_plan_workspace_bytes (activations of the T tokens). */
+ * hpd_plan_workspace_bytes (activations of the T tokens and split-K
+ * partials of the projections). */
 size_t hpd_decode_workspace_bytes(const hpd_model_desc *model, const hpd_plan *plan);
 
 /* One full decode step of the decoder stack for every new token of every
@@ -188,11 +189,19 @@ size_t hpd_decode_workspace_bytes(const hpd_model_desc *model, const hpd_plan *p
  * priv_k[l] / priv_v[l] (no other row is written); a = attention as in
  * hpd_branch_attn_step; h += a W_o^T; x = RMSNorm(h);
  * h += (silu(x W_gate^T) * (x W_up^T)) W_down^T.
- * hidden_in, hidden_out: device float [T][hidden] (may alias).
- * shared_k/v, priv_k/v: HOST arrays of num_layers device pointers (bf16).
- * The plan's dtype must be HPD_BF16, out_dtype HPD_BF16 or HPD_F32.
+ * hidden_in, hidden_out: device float [T][hidden], 16-byte aligned; the
+ *   step copies hidden_in to hidden_out first and then updates hidden_out
+ *   in place (they may be the same buffer).
+ * shared_k/v, priv_k/v: HOST arrays of num_layers device pointers (bf16,
+ *   16-byte aligned) in the layouts of hpd_branch_attn_step.
+ * The plan's dtype and out_dtype must be HPD_BF16 and Hq * 64 a multiple of
+ * 128 (else HPD_ERR_UNSUPPORTED).
  * workspace: >= hpd_plan_workspace_bytes + hpd_decode_workspace_bytes,
- *   uploaded with hpd_plan_upload. */
+ *   256-byte aligned, uploaded with hpd_plan_upload.
+ * Numerics: weights bf16; q, k, v, the attention output and the attention
+ * input norm enter their products as bf16; the MLP input norm and the SwiGLU
+ * product as two bf16 terms (hi + lo); all accumulation and the residual
+ * stream in fp32. */
 hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan,
                            const float *hidden_in, float *hidden_out,
                            const void *const *shared_k, const void *const *shared_v,

@@ -28,6 +28,10 @@ bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
 
 }  // namespace
 
+namespace hpd {
+void set_last_error(const std::string &msg) { g_last_error = msg; }
+}  // namespace hpd
+
 extern "C" {
 
 const char *hpd_status_string(hpd_status s) {

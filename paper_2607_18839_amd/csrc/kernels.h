@@ -13,6 +13,8 @@ struct PlanDev {
   const int32_t *private_items;
   const int32_t *token_slots;
   const int32_t *token_fork;
+  const int32_t *token_dest;
+  int32_t *counters;
   float *part_o;
   float *part_lse;
 };

@@ -135,10 +135,12 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   }
   P.visible.resize(P.T);
   P.token_fork.resize(P.T);
+  P.token_dest.resize(P.T);
   for (int i = 0; i < nb; ++i)
     for (int j = 0; j < P.num_new[i]; ++j) {
       P.visible[P.q_row[i] + j] = P.fork[i] + P.past_len[i] + j + 1;
       P.token_fork[P.q_row[i] + j] = P.fork[i];
+      P.token_dest[P.q_row[i] + j] = (int32_t)(P.priv_row[i] + P.past_len[i] + j);
     }
 
   // ---- partial slots per token
@@ -215,6 +217,10 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   off = align256(off + P.token_slots.size() * sizeof(int32_t));
   P.off_token_fork = off;
   off = align256(off + P.token_fork.size() * sizeof(int32_t));
+  P.off_token_dest = off;
+  off = align256(off + P.token_dest.size() * sizeof(int32_t));
+  P.off_counters = off;   // zeroed by the upload; every user resets what it uses
+  off = align256(off + kNumCounters * sizeof(int32_t));
   P.table_bytes = off;
   P.off_part_o = off;
   off = align256(off + (size_t)P.num_slots * Hq * HPD_HEAD_DIM * sizeof(float));
@@ -230,6 +236,7 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   put(P.off_private_items, P.private_items);
   put(P.off_token_slots, P.token_slots);
   put(P.off_token_fork, P.token_fork);
+  put(P.off_token_dest, P.token_dest);
 
   *out = std::move(P);
   return HPD_OK;

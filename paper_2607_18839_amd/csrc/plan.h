@@ -35,6 +35,7 @@ constexpr int kKeyTile = 64;         // keys per LDS tile
 constexpr int kSharedSplitKeys = 256;   // prefix keys per shared work item
 constexpr int kPrivateChunkKeys = 128;  // private keys per private work item
 constexpr int SI_FLAG_FORK = 1;      // rows have their own fork limits
+constexpr int kNumCounters = 8192;   // self-resetting arrival counters (split-K / merges)
 
 struct Plan {
   hpd_attn_desc attn{};
@@ -51,11 +52,12 @@ struct Plan {
   std::vector<int32_t> shared_items, private_items;   // [n][SI_NFIELDS / PI_NFIELDS]
   std::vector<int32_t> token_slots;                   // [T][2]: first slot, count
   std::vector<int32_t> token_fork;                    // [T] visible prefix per token
+  std::vector<int32_t> token_dest;                    // [T] private row of token t: priv_row + L + j
   int64_t num_slots = 0;                              // partial rows = num_slots * Hq
 
   // device workspace layout (byte offsets, 256-aligned)
   size_t off_shared_items = 0, off_private_items = 0, off_token_slots = 0,
-         off_token_fork = 0, off_part_o = 0, off_part_lse = 0, table_bytes = 0,
+         off_token_fork = 0, off_token_dest = 0, off_counters = 0, off_part_o = 0, off_part_lse = 0, table_bytes = 0,
          workspace_bytes = 0;
   std::vector<unsigned char> table_image;             // host copy of [0, table_bytes)
 

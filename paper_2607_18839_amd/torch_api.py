@@ -54,3 +54,43 @@ class BranchAttention:
                                   _p(out), _p(lse), self.workspace.data_ptr(), self.ws_bytes,
                                   _stream(stream))
         return out
+
+
+class DecodeStep:
+    """One decode step of the decoder stack for a fixed batch shape.
+
+    ``weights`` maps 'w_qkv', 'w_o', 'w_gate', 'w_up', 'w_down' (and
+    optionally 'g_attn_norm', 'g_mlp_norm') to lists of per-layer bf16 device
+    tensors in torch Linear layout.  The tensors must stay alive while the
+    step is used.
+    """
+
+    def __init__(self, num_q_heads, num_kv_heads, prefix_len, branch_page, num_new, past_len,
+                 weights, hidden, intermediate, rms_eps=1e-6, prefix_row=None, priv_row=None,
+                 device="cuda", stream=None):
+        self.attn = BranchAttention(num_q_heads, num_kv_heads, prefix_len, branch_page, num_new, past_len,
+                                    dtype=torch.bfloat16, prefix_row=prefix_row, priv_row=priv_row,
+                                    device=device, stream=stream)
+        self.T = self.attn.T
+        self.hidden = hidden
+        self.num_layers = len(weights["w_qkv"])
+        ptrs = {k: [t.data_ptr() for t in v] for k, v in weights.items()}
+        self.model = _lib.model_desc(self.num_layers, hidden, intermediate, rms_eps, ptrs["w_qkv"], ptrs["w_o"],
+                                     ptrs["w_gate"], ptrs["w_up"], ptrs["w_down"], ptrs.get("g_attn_norm"),
+                                     ptrs.get("g_mlp_norm"))
+        self.plan_bytes = self.attn.ws_bytes
+        self.ws_bytes = self.plan_bytes + _lib.hpd_decode_workspace_bytes(self.model, self.attn.plan)
+        # one workspace holding the plan tables (uploaded) and the step's scratch
+        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        _lib.hpd_plan_upload(self.attn.plan, self.workspace.data_ptr(), self.ws_bytes, _stream(stream))
+
+    def __call__(self, hidden_in, shared_k, shared_v, priv_k, priv_v, hidden_out=None, stream=None):
+        if hidden_out is None:
+            hidden_out = torch.empty_like(hidden_in)
+        if hidden_in.dtype != torch.float32 or hidden_in.shape != (self.T, self.hidden):
+            raise ValueError("hidden_in must be float32 [T, hidden]")
+        _lib.hpd_decode_step(self.model, self.attn.plan, hidden_in.data_ptr(), hidden_out.data_ptr(),
+                             [t.data_ptr() for t in shared_k], [t.data_ptr() for t in shared_v],
+                             [t.data_ptr() for t in priv_k], [t.data_ptr() for t in priv_v],
+                             self.workspace.data_ptr(), self.ws_bytes, _stream(stream))
+        return hidden_out

@@ -1,0 +1,124 @@
+"""GPU parity of the full decode step (hpd_decode_step) against the fp64 oracle."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle.decode import decode_step
+from workloads import get_config, make_decode_inputs
+from workloads.gen import DecodeInputs
+
+from ._gpu import BF16_MAX_ABS, BF16_REL_L2, announce, errors, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def run_decode(inp, canary=True):
+    """Runs hpd_decode_step on the inputs; returns (h_out, priv_k list, priv_v list) as numpy."""
+    from paper_2607_18839_amd.torch_api import DecodeStep
+    w = {k: [to_dev(a, "bf16") for a in getattr(inp, k)] for k in ("w_qkv", "w_o", "w_gate", "w_up", "w_down")}
+    step = DecodeStep(inp.num_q_heads, inp.num_kv_heads, inp.prefix_len, inp.branch_page, inp.num_new,
+                      inp.past_len, w, inp.hidden, inp.intermediate, inp.rms_eps)
+    sk = [to_dev(a, "bf16") for a in inp.shared_k]
+    sv = [to_dev(a, "bf16") for a in inp.shared_v]
+    pk_np = [a.copy() for a in inp.priv_k]
+    pv_np = [a.copy() for a in inp.priv_v]
+    if canary:   # the slots the step must fill start as NaN
+        rows = np.concatenate([np.arange(r + L, r + L + k) for r, L, k in
+                               zip(np.concatenate([[0], np.cumsum(inp.past_len + inp.num_new)[:-1]]),
+                                   inp.past_len, inp.num_new)])
+        for a in pk_np + pv_np:
+            a[rows] = np.uint16(0x7FC0)
+    pk = [to_dev(a, "bf16") for a in pk_np]
+    pv = [to_dev(a, "bf16") for a in pv_np]
+    h = torch.from_numpy(inp.hidden_in).cuda()
+    out = step(h, sk, sv, pk, pv)
+    torch.cuda.synchronize()
+    back = lambda ts: [t.view(torch.int16).cpu().numpy().view(np.uint16) for t in ts]
+    return out.double().cpu().numpy(), back(pk), back(pv)
+
+
+def small_inputs(seed, layers=2):
+    cfg = get_config("c4", num_q_heads=4, num_kv_heads=2, num_pages=1, prefix=("fixed", 300),
+                     layout=dict(k=1, past=("fixed", 70)), content_count=("fixed", 5), content_k=4,
+                     content_past=("lognormal", 40.0, 1.0, 0, 200),
+                     model=dict(num_layers=layers, hidden=256, intermediate=384, weight_std=0.05, rms_eps=1e-6))
+    return make_decode_inputs(cfg, seed)
+
+
+def _check_cache(inp, pk, pv, nk, nv):
+    """New rows match the oracle's bf16 K/V within the parity bar; every
+    other row is bit-identical to the input."""
+    starts = np.concatenate([[0], np.cumsum(inp.past_len + inp.num_new)[:-1]])
+    dest = np.concatenate([np.arange(r + L, r + L + k) for r, L, k in zip(starts, inp.past_len, inp.num_new)])
+    keep = np.ones(pk[0].shape[0], bool)
+    keep[dest] = False
+    val = lambda b: (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    for l in range(inp.num_layers):
+        assert np.array_equal(pk[l][keep], inp.priv_k[l][keep]) and np.array_equal(pv[l][keep], inp.priv_v[l][keep])
+        for got, want in ((pk[l][dest], nk[l]), (pv[l][dest], nv[l])):
+            mx, rl = errors(val(got), val(want))
+            assert mx <= BF16_MAX_ABS * 5 and rl <= BF16_REL_L2, f"layer {l} cache rows: {mx:.3e} {rl:.3e}"
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_small_stack(seed):
+    announce(f"decode small seed {seed}")
+    inp = small_inputs(seed)
+    h, pk, pv = run_decode(inp)
+    ref, nk, nv = decode_step(inp)
+    mx, rl = errors(h, ref)
+    print(f"small stack seed {seed}: max abs {mx:.3e} rel L2 {rl:.3e}")
+    assert np.all(np.isfinite(h))
+    assert mx <= BF16_MAX_ABS and rl <= BF16_REL_L2, (mx, rl)
+    _check_cache(inp, pk, pv, nk, nv)
+
+
+def _sub_batch(inp, branches):
+    """Inputs restricted to some branches of the page (their outputs depend on
+    nothing else: context isolation)."""
+    starts_t = np.concatenate([[0], np.cumsum(inp.num_new)])
+    starts_r = np.concatenate([[0], np.cumsum(inp.past_len + inp.num_new)])
+    tok = np.concatenate([np.arange(starts_t[b], starts_t[b + 1]) for b in branches])
+    rows = np.concatenate([np.arange(starts_r[b], starts_r[b + 1]) for b in branches])
+    sub = DecodeInputs(name=inp.name + "-sub", seed=inp.seed, num_q_heads=inp.num_q_heads,
+                       num_kv_heads=inp.num_kv_heads, head_dim=inp.head_dim, num_layers=inp.num_layers,
+                       hidden=inp.hidden, intermediate=inp.intermediate, rms_eps=inp.rms_eps,
+                       prefix_len=inp.prefix_len, branch_page=inp.branch_page[branches],
+                       num_new=inp.num_new[branches], past_len=inp.past_len[branches],
+                       is_layout=inp.is_layout[branches], hidden_in=inp.hidden_in[tok],
+                       shared_k=inp.shared_k, shared_v=inp.shared_v,
+                       priv_k=[a[rows] for a in inp.priv_k], priv_v=[a[rows] for a in inp.priv_v],
+                       w_qkv=inp.w_qkv, w_o=inp.w_o, w_gate=inp.w_gate, w_up=inp.w_up, w_down=inp.w_down)
+    return sub, tok
+
+
+def test_full_c4_sampled_branches():
+    """c4 at full size (18 layers, 33 branches, 4096-token prefix) in the
+    configuration the benchmark times; the oracle recomputes 3 sampled
+    branches (layout, the longest and one more content branch) on their own."""
+    announce("decode c4 full, sampled branches")
+    inp = make_decode_inputs("c4", 0)
+    h, pk, pv = run_decode(inp, canary=False)
+    longest = int(np.argmax(np.where(inp.is_layout, -1, inp.past_len)))
+    sample = sorted({0, longest, 7})
+    sub, tok = _sub_batch(inp, sample)
+    ref, _, _ = decode_step(sub)
+    mx, rl = errors(h[tok], ref)
+    print(f"c4 sampled branches {sample}: max abs {mx:.3e} rel L2 {rl:.3e}")
+    assert np.all(np.isfinite(h))
+    assert mx <= BF16_MAX_ABS and rl <= BF16_REL_L2, (mx, rl)
+
+
+def test_decode_deterministic_and_hidden_alias():
+    announce("decode determinism + in-place")
+    inp = small_inputs(5, layers=3)
+    h1, pk1, _ = run_decode(inp)
+    h2, pk2, _ = run_decode(inp)
+    assert np.array_equal(h1, h2) and all(np.array_equal(a, b) for a, b in zip(pk1, pk2))
