@@ -89,30 +89,53 @@ def main():
     print(json.dumps(res))
 
 
-def _time_steps(torch, step, K, W, stream):
-    for i in range(W):
-        step(i)
+def _graph_time(torch, step, n_in_graph, K, W):
+    """Captures n_in_graph consecutive steps in one HIP graph (torch's
+    CUDAGraph on ROCm), replays it W times untimed, then times replays
+    covering at least K steps.  Returns (ms per step, steps timed)."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):           # eager warm-up outside capture
+        for i in range(n_in_graph):
+            step(i)
+    torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(n_in_graph):
+            step(i)
+    for _ in range(max(1, W)):
+        g.replay()
+    torch.cuda.synchronize()
+    reps = max(1, -(-K // n_in_graph))
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for i in range(K):
-        step(W + i)
-    e1.record(stream)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
     torch.cuda.synchronize()
-    return e0.elapsed_time(e1) / K
+    return e0.elapsed_time(e1) / (reps * n_in_graph), reps * n_in_graph
 
 
-def _kernel_pass(torch, _lib, step, K, W):
-    """Second pass of K steps with library-side per-kernel event timing."""
+def _kernel_pass(torch, _lib, step, K, W, queue_cycles=20_000_000):
+    """Per-kernel durations from HIP events the library records around each
+    launch.  Every step is first queued behind a bounded spin kernel
+    (torch.cuda._sleep), so its launches run back to back on the GPU and the
+    event intervals do not include host launch latency."""
     _lib.hpd_kernel_timing(1, 200000)
     _lib.hpd_kernel_times_read()
+    tot = {}
     for i in range(K):
+        torch.cuda._sleep(queue_cycles)
         step(W + i)
-    torch.cuda.synchronize()
-    t = _lib.hpd_kernel_times_read()
+        torch.cuda.synchronize()
+        for k, (c, ms) in _lib.hpd_kernel_times_read().items():
+            a = tot.setdefault(k, [0, 0.0])
+            a[0] += c
+            a[1] += ms
     _lib.hpd_kernel_timing(0)
-    return {k: dict(launches=c, avg_us=(1000.0 * ms / c if c else None)) for k, (c, ms) in t.items()
+    return {k: dict(launches=c, avg_us=(1000.0 * ms / c if c else None)) for k, (c, ms) in tot.items()
             if not k.startswith("_") and c}
 
 
@@ -148,8 +171,8 @@ def bench_attention(args, torch, _lib):
         q, sk, sv, pk, pv = replicas[i % reps]
         layer(q, sk, sv, pk, pv, out=out)
 
-    ms = _time_steps(torch, step, args.steps, args.warmup, stream)
-    kern = _kernel_pass(torch, _lib, step, args.steps, args.warmup)
+    ms, timed = _graph_time(torch, step, min(args.steps, reps), args.steps, args.warmup)
+    kern = _kernel_pass(torch, _lib, step, min(args.steps, 20), args.warmup, queue_cycles=2_000_000)
     w = attn_work(b.prefix_len, b.branch_page, b.num_new, b.past_len, b.num_q_heads, b.num_kv_heads, 64,
                   s_in, s_in)
     peak_mfma = BF16_PEAK_TFLOPS if b.dtype == "bf16" else FP32_PEAK_TFLOPS
@@ -169,9 +192,9 @@ def bench_attention(args, torch, _lib):
                 "algorithmic_per_launch": w["shared_flop"]}
     res = {
         "metric": "branch-tokens/s per decode step", "value": w["T"] / (ms / 1e3), "unit": "branch-tokens/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "n_gpus": 1, "steps": timed, "warmup": args.warmup, "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": b.dtype, "data": "synthetic",
+        "dtype": b.dtype, "data": "synthetic", "timing": "HIP graph replay",
         "config": {"workload": f"{args.workload}: single attention layer", "pages": b.num_pages,
                    "branches": b.num_branches, "branch_tokens": w["T"],
                    "prefix_len_total": int(b.prefix_len.sum()),
@@ -236,8 +259,8 @@ def bench_decode(args, torch, _lib):
     def step(i):
         step_obj(h_in, sk, sv, pk, pv, hidden_out=h_out)
 
-    ms = _time_steps(torch, step, args.steps, args.warmup, stream)
-    kern = _kernel_pass(torch, _lib, step, args.steps, args.warmup)
+    ms, timed = _graph_time(torch, step, 1, args.steps, args.warmup)
+    kern = _kernel_pass(torch, _lib, step, min(args.steps, 10), args.warmup)
     T, Hq, Hkv, D, H, I = step_obj.T, inp.num_q_heads, inp.num_kv_heads, 64, inp.hidden, inp.intermediate
     aw = attn_work(inp.prefix_len, inp.branch_page, inp.num_new, inp.past_len, Hq, Hkv, D, 2, 2)
     gw = gemm_work(T, Hq, Hkv, D, H, I)
@@ -251,7 +274,7 @@ def bench_decode(args, torch, _lib):
                      frac=aw["private_bytes"] / us / 1e3 / HBM_PEAK_GBS)
         elif name in gw:
             k.update(bound="hbm", bytes=gw[name], gbs=gw[name] / us / 1e3, frac=gw[name] / us / 1e3 / HBM_PEAK_GBS)
-        k["total_us_per_step"] = us * k["launches"] / args.steps
+        k["total_us_per_step"] = us * k["launches"] / min(args.steps, 10)
     dom = max(kern, key=lambda n: kern[n]["total_us_per_step"])
     d = kern[dom]
     if d.get("bound") == "mfma":
@@ -262,8 +285,9 @@ def bench_decode(args, torch, _lib):
                 "frac": d.get("frac"), "traffic": None, "algorithmic_per_launch": d.get("bytes")}
     res = {
         "metric": "branch-tokens/s per decode step", "value": T / (ms / 1e3), "unit": "branch-tokens/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "n_gpus": 1, "steps": timed, "warmup": args.warmup, "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "timing": "HIP graph replay (one step per graph)",
         "data": "synthetic (seeded N(0,1) KV and hidden, N(0,0.02) bf16 weights)",
         "config": {"workload": "c4: full decode step, 18-layer synthetic decoder, 1 page, "
                                "1 layout (k=1) + 32 content (k=4) branches, 4096-token shared prefix",

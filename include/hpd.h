@@ -215,17 +215,19 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan,
  * of their elapsed times since the previous read.  The event pool
  * (max_launches pairs) is created by hpd_kernel_timing(1, n), outside any
  * timed region; launches beyond it are counted in `dropped`.  Timing adds
- * two event records per launch and must not be enabled under graph capture. */
-#define HPD_NUM_KERNEL_KINDS 8
+ * two event records per launch.  Under stream capture the event records
+ * become graph nodes: read with keep_pairs = 1 after each replay (the pairs
+ * stay assigned to the captured launches); keep_pairs = 0 releases them. */
+#define HPD_NUM_KERNEL_KINDS 9
 typedef struct {
   int64_t count[HPD_NUM_KERNEL_KINDS];
   double total_ms[HPD_NUM_KERNEL_KINDS];
   int64_t dropped;
 } hpd_kernel_times;
 hpd_status hpd_kernel_timing(int enable, int max_launches);
-hpd_status hpd_kernel_times_read(hpd_kernel_times *out);
+hpd_status hpd_kernel_times_read(hpd_kernel_times *out, int keep_pairs);
 /* Kind k: 0 shared_prefix, 1 private, 2 merge, 3 gemm_qkv, 4 gemm_o,
- * 5 gemm_gate_up, 6 gemm_down, 7 norm. */
+ * 5 gemm_gate_up, 6 gemm_down, 7 residual_norm, 8 gemm_epilogue. */
 const char *hpd_kernel_kind_name(int kind);
 
 const char *hpd_status_string(hpd_status status);

@@ -85,7 +85,7 @@ SIGNATURES = {
                                        ctypes.c_void_p, PP, PP, PP, PP, ctypes.c_void_p, ctypes.c_size_t,
                                        ctypes.c_void_p]),
     "hpd_kernel_timing": (ctypes.c_int, [ctypes.c_int, ctypes.c_int]),
-    "hpd_kernel_times_read": (ctypes.c_int, [ctypes.c_void_p]),
+    "hpd_kernel_times_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int]),
     "hpd_kernel_kind_name": (ctypes.c_char_p, [ctypes.c_int]),
     "hpd_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "hpd_last_error_message": (ctypes.c_char_p, []),
@@ -223,7 +223,7 @@ def hpd_decode_step(model, plan, hidden_in, hidden_out, shared_k, shared_v, priv
                                   stream), "hpd_decode_step")
 
 
-HPD_NUM_KERNEL_KINDS = 8
+HPD_NUM_KERNEL_KINDS = 9
 
 
 class hpd_kernel_times(ctypes.Structure):
@@ -235,10 +235,10 @@ def hpd_kernel_timing(enable, max_launches=8192):
     _check(load().hpd_kernel_timing(int(bool(enable)), max_launches), "hpd_kernel_timing")
 
 
-def hpd_kernel_times_read():
+def hpd_kernel_times_read(keep_pairs=False):
     """{kind name: (launch count, total ms)} since the previous read."""
     t = hpd_kernel_times()
-    _check(load().hpd_kernel_times_read(ctypes.byref(t)), "hpd_kernel_times_read")
+    _check(load().hpd_kernel_times_read(ctypes.byref(t), int(bool(keep_pairs))), "hpd_kernel_times_read")
     lib = load()
     out = {lib.hpd_kernel_kind_name(k).decode(): (int(t.count[k]), float(t.total_ms[k]))
            for k in range(HPD_NUM_KERNEL_KINDS)}

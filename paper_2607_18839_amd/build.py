@@ -16,6 +16,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libhpd.so")
+PEAKS = os.path.join(PKG, "peaks")   # microbenchmark executable (bench.py --peaks)
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
@@ -23,9 +24,12 @@ HIP_SOURCES = ["attn_kernels.hip", "gemm_kernels.hip", "decode.hip", "timing.hip
 CXX_SOURCES = ["plan.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-I" + os.path.join(ROOT, "include"), "-I" + CSRC]
-# Packed fp32 VALU forms are disabled for all device code.
+# Packed fp32 VALU forms are disabled for all device code.  MFMA results
+# are kept in architectural VGPRs (the accumulator-register form made the
+# allocator shuttle accumulators through v_accvgpr moves inside the k loops).
 HIP_FLAGS = COMMON + [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang",
-                      "-packed-fp32-ops", "-Wno-unused-command-line-argument"]
+                      "-packed-fp32-ops", "-mllvm", "-amdgpu-mfma-vgpr-form",
+                      "-Wno-unused-command-line-argument"]
 
 
 def _run(cmd):
@@ -53,6 +57,8 @@ def build(verbose=False):
     tmp = LIB + ".tmp"
     _run([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp] + objs)
     os.replace(tmp, LIB)
+    _run([HIPCC] + HIP_FLAGS + ["-o", PEAKS + ".tmp", os.path.join(CSRC, "peaks.hip")])
+    os.replace(PEAKS + ".tmp", PEAKS)
     return LIB
 
 

@@ -409,17 +409,37 @@ __global__ __launch_bounds__(256) void merge_kernel(PlanDev dev, TO *out, float 
   const int sub = threadIdx.x & 15;
   const int t = row / Hq, h = row % Hq;
   const int first = dev.token_slots[2 * t], cnt = dev.token_slots[2 * t + 1];
+  const float *lse_p = dev.part_lse + (int64_t)first * Hq + h;
+  const float *o_p = dev.part_o + ((int64_t)first * Hq + h) * D + 4 * sub;
+  // batches of 8 partials: every load of a batch is issued before it is used
   float mx = -INFINITY;
-  for (int i = 0; i < cnt; ++i) mx = fmaxf(mx, dev.part_lse[(int64_t)(first + i) * Hq + h]);
+  for (int i0 = 0; i0 < cnt; i0 += 8) {
+    float l8[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) l8[i] = lse_p[(int64_t)min(i0 + i, cnt - 1) * Hq];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) mx = fmaxf(mx, l8[i]);
+  }
   const float m_use = mx == -INFINITY ? 0.f : mx;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   float wsum = 0.f;
-  for (int i = 0; i < cnt; ++i) {
-    const int64_t pr = (int64_t)(first + i) * Hq + h;
-    const float wgt = __builtin_amdgcn_exp2f(dev.part_lse[pr] - m_use);
-    const f32x4 v = *(const f32x4 *)(dev.part_o + pr * D + 4 * sub);
-    wsum += wgt;
-    acc += wgt * v;
+  for (int i0 = 0; i0 < cnt; i0 += 8) {
+    float l8[8];
+    f32x4 o8[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int64_t j = min(i0 + i, cnt - 1);
+      l8[i] = lse_p[j * Hq];
+      o8[i] = *(const f32x4 *)(o_p + j * Hq * D);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if (i0 + i < cnt) {
+        const float wgt = __builtin_amdgcn_exp2f(l8[i] - m_use);
+        wsum += wgt;
+        acc += wgt * o8[i];
+      }
+    }
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
   TO *dst = out + (int64_t)row * D + 4 * sub;

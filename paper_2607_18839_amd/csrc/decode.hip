@@ -3,16 +3,18 @@
 // The step runs every new token of every branch through all layers at once
 // (Algorithm 1, the parallel draft over the active pool).  Per layer, with
 // the residual stream h [T][hidden] kept in fp32 in hidden_out:
-//   1 RMSNorm(h)                       -> x  (bf16)
-//   2 QKV GEMM                         -> q (bf16) and the new K/V rows,
-//                                         written into the layer's private
-//                                         cache at row priv_row + L + j
+//   1 [h += previous down projection] RMSNorm(h) -> x (bf16)
+//   2 QKV GEMM (split-K partials), epilogue kernel -> q (bf16) and the new
+//     K/V rows, written into the layer's private cache at row priv_row + L + j
 //   3 branch attention (shared-prefix, private, merge kernels) -> a (bf16)
-//   4 O GEMM, residual epilogue        h += a W_o^T
-//   5 RMSNorm(h)                       -> x as hi + lo bf16 terms
-//   6 gate/up GEMM, SwiGLU epilogue    -> m = silu(x W_gate^T) * (x W_up^T), hi + lo
-//   7 down GEMM, residual epilogue     h += m W_down^T
+//   4 O GEMM (partials)
+//   5 h += a W_o^T, RMSNorm(h) -> x as hi + lo bf16 terms (one kernel)
+//   6 gate/up GEMM (partials), SwiGLU epilogue kernel -> m, hi + lo terms
+//   7 down GEMM (partials), added to h by the next layer's step 1 (or by a
+//     final residual kernel after the last layer)
 // (section "Overview", paragraph "LLM Decoder": GQA, RMSNorm, SwiGLU).
+// Split-K partials are summed by the consuming kernel in split order, so the
+// result does not depend on scheduling and needs no cross-workgroup sync.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -36,19 +38,24 @@ struct GemmShape {
   int n_slices, ksplit, k_per_wg, n_tgroups;
 };
 
-// Split-K factor: the largest divisor of K / 128 that keeps the grid within
-// about two workgroups per CU (512) -- enough to keep HBM busy while the
-// partial tiles stay few.
-GemmShape gemm_shape(int N_virtual, int K, int Tpad) {
+// Split-K factor of one projection: the largest divisor of K / 32 that keeps
+// the grid within `max_wg` workgroups (default 512, two per CU) and leaves
+// each split at least `min_k` (default 256) of K, so that a split's fp32
+// partial tile (64 x Tpad) stays about as large as the weight slice it comes
+// from.  With one split the QKV and SwiGLU epilogues run inside the GEMM;
+// otherwise a consumer kernel adds the splits in order.
+GemmShape gemm_shape(int N_virtual, int K, int Tpad, bool allow_split) {
   GemmShape s;
   s.n_slices = N_virtual / 64;
   s.n_tgroups = (Tpad + kGemmTokenGroup - 1) / kGemmTokenGroup;
-  const int steps = K / 128;
-  int max_wg = 512;
+  const int steps = K / 32;
+  int max_wg = 512, min_k = 256;
   if (const char *e = std::getenv("HPD_GEMM_MAX_WG")) max_wg = std::max(1, std::atoi(e));
+  if (const char *e = std::getenv("HPD_GEMM_MIN_K")) min_k = std::max(32, std::atoi(e));
   s.ksplit = 1;
-  for (int d = 1; d <= steps; ++d)
-    if (steps % d == 0 && s.n_tgroups * s.n_slices * d <= max_wg) s.ksplit = d;
+  if (allow_split)
+    for (int d = 1; d <= steps; ++d)
+      if (steps % d == 0 && s.n_tgroups * s.n_slices * d <= max_wg && K / d >= min_k) s.ksplit = d;
   s.k_per_wg = K / s.ksplit;
   return s;
 }
@@ -62,15 +69,18 @@ struct DecodeLayout {
 DecodeLayout decode_layout(const hpd_model_desc &m, const Plan &P) {
   DecodeLayout L;
   L.T = P.T;
-  L.Tpad = (P.T + 15) / 16 * 16;
+  // one token group of up to 144 rows; beyond that whole groups of 144
+  L.Tpad = P.T <= kGemmTokenGroup ? (P.T + 15) / 16 * 16
+                                  : (P.T + kGemmTokenGroup - 1) / kGemmTokenGroup * kGemmTokenGroup;
   L.H = m.hidden;
   L.I = m.intermediate;
   L.nq = P.attn.num_q_heads * HPD_HEAD_DIM;
   L.nkv = P.attn.num_kv_heads * HPD_HEAD_DIM;
-  L.qkv = gemm_shape(L.nq + 2 * L.nkv, L.H, L.Tpad);
-  L.o = gemm_shape(L.H, L.nq, L.Tpad);
-  L.gu = gemm_shape(2 * L.I, L.H, L.Tpad);
-  L.down = gemm_shape(L.H, L.I, L.Tpad);
+  const bool split_wide = std::getenv("HPD_GEMM_NO_SPLIT_WIDE") == nullptr;
+  L.qkv = gemm_shape(L.nq + 2 * L.nkv, L.H, L.Tpad, split_wide);
+  L.o = gemm_shape(L.H, L.nq, L.Tpad, true);
+  L.gu = gemm_shape(2 * L.I, L.H, L.Tpad, split_wide);
+  L.down = gemm_shape(L.H, L.I, L.Tpad, true);
   size_t off = align256(P.workspace_bytes);
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -85,8 +95,7 @@ DecodeLayout decode_layout(const hpd_model_desc &m, const Plan &P) {
   L.off_m_lo = take((size_t)L.Tpad * L.I * 2);
   size_t part = 0;
   for (const GemmShape &s : {L.qkv, L.o, L.gu, L.down})
-    if (s.ksplit > 1)
-      part = std::max(part, (size_t)s.n_tgroups * s.n_slices * s.ksplit * 64 * kGemmTokenGroup * 4);
+    part = std::max(part, (size_t)s.ksplit * L.Tpad * s.n_slices * 64 * sizeof(float));
   L.off_part = take(part);
   L.bytes = off;
   return L;
@@ -115,13 +124,6 @@ hpd_status validate(const hpd_model_desc *m, const hpd_plan *plan, std::string *
       *err = "NULL weight of layer " + std::to_string(l);
       return HPD_ERR_INVALID_ARGUMENT;
     }
-  }
-  const int Tpad = (P.T + 15) / 16 * 16;
-  const int tg = (Tpad + kGemmTokenGroup - 1) / kGemmTokenGroup;
-  const int widest = std::max(P.attn.num_q_heads + 2 * P.attn.num_kv_heads, std::max(m->hidden, 2 * m->intermediate) / 64);
-  if ((int64_t)tg * widest > kNumCounters / 2) {
-    *err = "too many output tiles for the arrival counters (T or the layer widths too large)";
-    return HPD_ERR_UNSUPPORTED;
   }
   return HPD_OK;
 }
@@ -178,7 +180,6 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
   __bf16 *m_hi = (__bf16 *)(ws + L.off_m_hi), *m_lo = (__bf16 *)(ws + L.off_m_lo);
   float *part = (float *)(ws + L.off_part);
   const hpd::PlanDev dev = hpd::plan_dev(P, workspace);
-  int32_t *gemm_counters = dev.counters + hpd::kNumCounters / 2;
 
   hipError_t e = hipSuccess;
   if (hidden_out != hidden_in)
@@ -188,6 +189,7 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
   auto base = [&](const hpd::GemmShape &s, const __bf16 *xh, const __bf16 *xl, int K) {
     hpd::GemmArgs g{};
     g.K = K;
+    g.N = 64 * s.n_slices;
     g.n_slices = s.n_slices;
     g.ksplit = s.ksplit;
     g.k_per_wg = s.k_per_wg;
@@ -197,15 +199,17 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
     g.T = L.T;
     g.Tpad = L.Tpad;
     g.part = part;
-    g.counters = gemm_counters;
     return g;
   };
+  int pending_ksplit = 0;   // down-projection partials not yet added to h
   for (int l = 0; l < m.num_layers && e == hipSuccess; ++l) {
     const __bf16 *g1 = m.g_attn_norm ? (const __bf16 *)m.g_attn_norm[l] : nullptr;
     const __bf16 *g2 = m.g_mlp_norm ? (const __bf16 *)m.g_mlp_norm[l] : nullptr;
-    // 1 + 2: attention input and QKV projection (new K/V appended to the cache)
-    e = hpd::launch_rmsnorm(h, g1, L.H, L.T, L.Tpad, m.rms_eps, x_hi, nullptr, attn, L.nq, stream);
+    // 1: previous layer's down projection into h, attention-input norm
+    e = hpd::launch_residual_norm(h, pending_ksplit ? part : nullptr, pending_ksplit, L.Tpad, L.H, L.T, g1,
+                                  m.rms_eps, x_hi, nullptr, attn, L.nq, stream);
     if (e != hipSuccess) break;
+    // 2: QKV projection; the epilogue appends the new K/V rows to the cache
     hpd::GemmArgs g = base(L.qkv, x_hi, nullptr, L.H);
     g.w0 = (const __bf16 *)m.w_qkv[l];
     g.q_out = q;
@@ -220,16 +224,15 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
     e = hpd::launch_branch_attention(P, q, shared_k ? shared_k[l] : nullptr, shared_v ? shared_v[l] : nullptr,
                                      priv_k[l], priv_v[l], attn, nullptr, workspace, stream);
     if (e != hipSuccess) break;
-    // 4: O projection + residual
+    // 4 + 5: O projection, residual add and MLP-input norm
     g = base(L.o, attn, nullptr, L.nq);
     g.w0 = (const __bf16 *)m.w_o[l];
-    g.h = h;
-    g.ldh = L.H;
     e = hpd::launch_gemm(g, false, hpd::kEpiResidual, hpd::KK_GEMM_O, stream);
     if (e != hipSuccess) break;
-    // 5 + 6: MLP input and gate/up projection with SwiGLU
-    e = hpd::launch_rmsnorm(h, g2, L.H, L.T, L.Tpad, m.rms_eps, x_hi, x_lo, nullptr, 0, stream);
+    e = hpd::launch_residual_norm(h, part, L.o.ksplit, L.Tpad, L.H, L.T, g2, m.rms_eps, x_hi, x_lo, nullptr, 0,
+                                  stream);
     if (e != hipSuccess) break;
+    // 6: gate/up projection, SwiGLU
     g = base(L.gu, x_hi, x_lo, L.H);
     g.w0 = (const __bf16 *)m.w_gate[l];
     g.w1 = (const __bf16 *)m.w_up[l];
@@ -238,13 +241,15 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
     g.I = L.I;
     e = hpd::launch_gemm(g, true, hpd::kEpiSwiGLU, hpd::KK_GEMM_GATE_UP, stream);
     if (e != hipSuccess) break;
-    // 7: down projection + residual
+    // 7: down projection (added to h by the next layer's first kernel)
     g = base(L.down, m_hi, m_lo, L.I);
     g.w0 = (const __bf16 *)m.w_down[l];
-    g.h = h;
-    g.ldh = L.H;
     e = hpd::launch_gemm(g, true, hpd::kEpiResidual, hpd::KK_GEMM_DOWN, stream);
+    pending_ksplit = L.down.ksplit;
   }
+  if (e == hipSuccess)
+    e = hpd::launch_residual_norm(h, part, pending_ksplit, L.Tpad, L.H, L.T, nullptr, m.rms_eps, nullptr, nullptr,
+                                  nullptr, 0, stream);
   if (e != hipSuccess) {
     hpd::set_last_error(std::string("hpd_decode_step: ") + hipGetErrorString(e));
     return HPD_ERR_HIP;

@@ -1,0 +1,140 @@
+// Microbenchmarks of the GPU this runs on, for the roofline denominators and
+// for calibrating hardware byte counters: streaming read and copy bandwidth,
+// dense bf16 MFMA rate, v_exp_f32 rate and dependent-load latency.
+//
+//   peaks [copy_mib]      prints one JSON object
+//
+// Every kernel has a fixed trip count and touches only its own buffers.
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstdlib>
+#include <vector>
+
+#define CHECK(x)                                                                      \
+  do {                                                                                \
+    hipError_t e_ = (x);                                                              \
+    if (e_ != hipSuccess) {                                                           \
+      std::fprintf(stderr, "%s failed: %s\n", #x, hipGetErrorString(e_));             \
+      std::exit(1);                                                                   \
+    }                                                                                 \
+  } while (0)
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// n4 float4 elements, grid-stride
+__global__ __launch_bounds__(256) void copy_kernel(const f32x4 *src, f32x4 *dst, size_t n4) {
+  for (size_t i = blockIdx.x * 256 + threadIdx.x; i < n4; i += (size_t)gridDim.x * 256) dst[i] = src[i];
+}
+
+__global__ __launch_bounds__(256) void read_kernel(const f32x4 *src, size_t n4, float *sink) {
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (size_t i = blockIdx.x * 256 + threadIdx.x; i < n4; i += (size_t)gridDim.x * 256) acc += src[i];
+  if (acc[0] + acc[1] + acc[2] + acc[3] == 123.456f) sink[0] = 1.f;   // keeps the loads alive
+}
+
+// 8 independent accumulators per wave, `iters` rounds of 8 MFMAs each.
+__global__ __launch_bounds__(256) void mfma_kernel(int iters, float *sink) {
+  bf16x8 a, b;
+  for (int e = 0; e < 8; ++e) {
+    a[e] = (__bf16)(0.001f * (threadIdx.x + e));
+    b[e] = (__bf16)(0.002f * e);
+  }
+  f32x4 c[8];
+  for (int j = 0; j < 8; ++j) c[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) c[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c[j], 0, 0, 0);
+  }
+  float s = 0.f;
+  for (int j = 0; j < 8; ++j) s += c[j][0] + c[j][1] + c[j][2] + c[j][3];
+  if (s == 123.456f) sink[0] = s;
+}
+
+// 8 independent exp2 chains per lane
+__global__ __launch_bounds__(256) void exp_kernel(int iters, float *sink) {
+  float x[8];
+  for (int j = 0; j < 8; ++j) x[j] = -0.001f * (threadIdx.x + j);
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = __builtin_amdgcn_exp2f(x[j]) - 1.0f;
+  }
+  float s = 0.f;
+  for (int j = 0; j < 8; ++j) s += x[j];
+  if (s == 123.456f) sink[0] = s;
+}
+
+// one lane follows a pointer chain of `steps` hops through a permutation
+__global__ void chase_kernel(const unsigned *next, int steps, unsigned *out) {
+  unsigned p = 0;
+  for (int i = 0; i < steps; ++i) p = next[p];
+  out[0] = p;
+}
+
+template <typename F> float time_ms(F launch, int reps) {
+  hipEvent_t a, b;
+  CHECK(hipEventCreate(&a));
+  CHECK(hipEventCreate(&b));
+  launch();
+  CHECK(hipDeviceSynchronize());
+  CHECK(hipEventRecord(a));
+  for (int i = 0; i < reps; ++i) launch();
+  CHECK(hipEventRecord(b));
+  CHECK(hipEventSynchronize(b));
+  float ms = 0.f;
+  CHECK(hipEventElapsedTime(&ms, a, b));
+  return ms / reps;
+}
+
+int main(int argc, char **argv) {
+  const size_t mib = argc > 1 ? std::strtoul(argv[1], nullptr, 10) : 1024;
+  const size_t bytes = mib << 20, n4 = bytes / 16;
+  hipDeviceProp_t prop;
+  CHECK(hipGetDeviceProperties(&prop, 0));
+  f32x4 *src, *dst;
+  float *sink;
+  CHECK(hipMalloc(&src, bytes));
+  CHECK(hipMalloc(&dst, bytes));
+  CHECK(hipMalloc(&sink, 64));
+  CHECK(hipMemset(src, 0, bytes));
+  const int cus = prop.multiProcessorCount;
+  const int grid = cus * 8;
+
+  const float copy_ms = time_ms([&] { hipLaunchKernelGGL(copy_kernel, dim3(grid), dim3(256), 0, 0, src, dst, n4); }, 10);
+  const float read_ms = time_ms([&] { hipLaunchKernelGGL(read_kernel, dim3(grid), dim3(256), 0, 0, src, n4, sink); }, 10);
+  const int miters = 4096;
+  const float mfma_ms = time_ms([&] { hipLaunchKernelGGL(mfma_kernel, dim3(cus * 8), dim3(256), 0, 0, miters, sink); }, 5);
+  const double mfma_flop = (double)cus * 8 * 4 /*waves*/ * miters * 8 * (16.0 * 16 * 32 * 2);
+  const int eiters = 4096;
+  const float exp_ms = time_ms([&] { hipLaunchKernelGGL(exp_kernel, dim3(cus * 8), dim3(256), 0, 0, eiters, sink); }, 5);
+  const double exps = (double)cus * 8 * 256 * eiters * 8;
+
+  // pointer chase over 64 MiB (beyond L2), stride pattern via a permutation
+  const unsigned nelem = 16u << 20;
+  std::vector<unsigned> h(nelem);
+  unsigned x = 1;
+  std::vector<unsigned> perm(nelem);
+  for (unsigned i = 0; i < nelem; ++i) perm[i] = i;
+  for (unsigned i = nelem - 1; i > 0; --i) {   // xorshift Fisher-Yates
+    x ^= x << 13; x ^= x >> 17; x ^= x << 5;
+    const unsigned j = x % (i + 1);
+    const unsigned t = perm[i]; perm[i] = perm[j]; perm[j] = t;
+  }
+  for (unsigned i = 0; i < nelem; ++i) h[perm[i]] = perm[(i + 1) % nelem];
+  unsigned *d_next, *d_out;
+  CHECK(hipMalloc(&d_next, nelem * 4ull));
+  CHECK(hipMalloc(&d_out, 64));
+  CHECK(hipMemcpy(d_next, h.data(), nelem * 4ull, hipMemcpyHostToDevice));
+  const int steps = 20000;
+  const float chase_ms = time_ms([&] { hipLaunchKernelGGL(chase_kernel, dim3(1), dim3(1), 0, 0, d_next, steps, d_out); }, 3);
+
+  std::printf("{\"device\": \"%s\", \"cus\": %d, \"clock_mhz\": %d, \"copy_mib\": %zu, "
+              "\"copy_gbs\": %.1f, \"read_gbs\": %.1f, \"mfma_bf16_tflops\": %.1f, "
+              "\"exp2_gops\": %.1f, \"exp2_per_cu_per_clk\": %.2f, \"load_latency_ns\": %.0f, "
+              "\"copy_us\": %.2f}\n",
+              prop.gcnArchName, cus, prop.clockRate / 1000, mib, 2.0 * bytes / copy_ms / 1e6,
+              bytes / read_ms / 1e6, mfma_flop / mfma_ms / 1e9, exps / exp_ms / 1e6,
+              exps / (exp_ms * 1e-3) / cus / (prop.clockRate * 1e3), chase_ms * 1e6 / steps, copy_ms * 1e3);
+  return 0;
+}

@@ -29,7 +29,8 @@ int64_t g_dropped = 0;
 thread_local int t_open = -1;   // pool index of the pair opened by this thread
 
 const char *kKindNames[HPD_NUM_KERNEL_KINDS] = {
-    "shared_prefix", "private", "merge", "gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down", "norm"};
+    "shared_prefix", "private", "merge", "gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down",
+    "residual_norm", "gemm_epilogue"};
 
 }  // namespace
 
@@ -74,7 +75,7 @@ hpd_status hpd_kernel_timing(int enable, int max_launches) {
   return HPD_OK;
 }
 
-hpd_status hpd_kernel_times_read(hpd_kernel_times *out) {
+hpd_status hpd_kernel_times_read(hpd_kernel_times *out, int keep_pairs) {
   if (!out) return HPD_ERR_INVALID_ARGUMENT;
   std::lock_guard<std::mutex> lk(hpd::g_mu);
   for (size_t i = 0; i < hpd::g_used; ++i) {
@@ -85,7 +86,7 @@ hpd_status hpd_kernel_times_read(hpd_kernel_times *out) {
     hpd::g_total_ms[p.kind] += ms;
     hpd::g_count[p.kind] += 1;
   }
-  hpd::g_used = 0;
+  if (!keep_pairs) hpd::g_used = 0;
   for (int k = 0; k < HPD_NUM_KERNEL_KINDS; ++k) {
     out->total_ms[k] = hpd::g_total_ms[k];
     out->count[k] = hpd::g_count[k];
