@@ -52,6 +52,27 @@ __global__ __launch_bounds__(256) void mfma_kernel(int iters, float *sink) {
   if (s == 123.456f) sink[0] = s;
 }
 
+// 4 independent 32x32 accumulators per wave, `iters` rounds of 4 MFMAs.
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+__global__ __launch_bounds__(256) void mfma32_kernel(int iters, float *sink) {
+  bf16x8 a, b;
+  for (int e = 0; e < 8; ++e) {
+    a[e] = (__bf16)(0.001f * (threadIdx.x + e));
+    b[e] = (__bf16)(0.002f * e);
+  }
+  f32x16 c[4];
+  for (int j = 0; j < 4; ++j)
+    for (int r = 0; r < 16; ++r) c[j][r] = 0.f;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c[j], 0, 0, 0);
+  }
+  float s = 0.f;
+  for (int j = 0; j < 4; ++j)
+    for (int r = 0; r < 16; ++r) s += c[j][r];
+  if (s == 123.456f) sink[0] = s;
+}
+
 // 8 independent exp2 chains per lane
 __global__ __launch_bounds__(256) void exp_kernel(int iters, float *sink) {
   float x[8];
@@ -106,6 +127,8 @@ int main(int argc, char **argv) {
   const int miters = 4096;
   const float mfma_ms = time_ms([&] { hipLaunchKernelGGL(mfma_kernel, dim3(cus * 8), dim3(256), 0, 0, miters, sink); }, 5);
   const double mfma_flop = (double)cus * 8 * 4 /*waves*/ * miters * 8 * (16.0 * 16 * 32 * 2);
+  const float mfma32_ms = time_ms([&] { hipLaunchKernelGGL(mfma32_kernel, dim3(cus * 8), dim3(256), 0, 0, miters, sink); }, 5);
+  const double mfma32_flop = (double)cus * 8 * 4 * miters * 4 * (32.0 * 32 * 16 * 2);
   const int eiters = 4096;
   const float exp_ms = time_ms([&] { hipLaunchKernelGGL(exp_kernel, dim3(cus * 8), dim3(256), 0, 0, eiters, sink); }, 5);
   const double exps = (double)cus * 8 * 256 * eiters * 8;
@@ -131,10 +154,10 @@ int main(int argc, char **argv) {
 
   std::printf("{\"device\": \"%s\", \"cus\": %d, \"clock_mhz\": %d, \"copy_mib\": %zu, "
               "\"copy_gbs\": %.1f, \"read_gbs\": %.1f, \"mfma_bf16_tflops\": %.1f, "
-              "\"exp2_gops\": %.1f, \"exp2_per_cu_per_clk\": %.2f, \"load_latency_ns\": %.0f, "
+              "\"mfma32_bf16_tflops\": %.1f, \"exp2_gops\": %.1f, \"exp2_per_cu_per_clk\": %.2f, \"load_latency_ns\": %.0f, "
               "\"copy_us\": %.2f}\n",
               prop.gcnArchName, cus, prop.clockRate / 1000, mib, 2.0 * bytes / copy_ms / 1e6,
-              bytes / read_ms / 1e6, mfma_flop / mfma_ms / 1e9, exps / exp_ms / 1e6,
+              bytes / read_ms / 1e6, mfma_flop / mfma_ms / 1e9, mfma32_flop / mfma32_ms / 1e9, exps / exp_ms / 1e6,
               exps / (exp_ms * 1e-3) / cus / (prop.clockRate * 1e3), chase_ms * 1e6 / steps, copy_ms * 1e3);
   return 0;
 }

@@ -1,0 +1,28 @@
+"""bench.py command-line contract that needs no GPU."""
+
+import json
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    msg = json.loads(r.stdout.strip().splitlines()[-1])
+    assert "one GPU" in msg["error"]
+
+
+def test_algorithmic_work_of_c3():
+    sys.path.insert(0, ROOT)
+    import bench
+    from workloads import make_attn_batch
+    b = make_attn_batch("c3", 0)
+    w = bench.attn_work(b.prefix_len, b.branch_page, b.num_new, b.past_len, 16, 2, 64, 2, 2)
+    assert w["T"] == 129
+    assert w["shared_flop"] == 4 * 16 * 64 * 129 * 4096 == 2164260864
+    rows = int((b.past_len + b.num_new).sum())
+    assert w["private_bytes"] == 2 * rows * 2 * 64 * 2 + 2 * 129 * 16 * 64 * 2
