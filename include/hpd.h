@@ -199,9 +199,10 @@ size_t hpd_decode_workspace_bytes(const hpd_model_desc *model, const hpd_plan *p
  * workspace: >= hpd_plan_workspace_bytes + hpd_decode_workspace_bytes,
  *   256-byte aligned, uploaded with hpd_plan_upload.
  * Numerics: weights bf16; q, k, v, the attention output and the attention
- * input norm enter their products as bf16; the MLP input norm and the SwiGLU
- * product as two bf16 terms (hi + lo); all accumulation and the residual
- * stream in fp32. */
+ * input norm enter their products as bf16; the MLP projections run in fp16
+ * (the bf16 weights convert exactly, the MLP input norm and the SwiGLU
+ * product are rounded to fp16); all accumulation and the residual stream in
+ * fp32. */
 hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan,
                            const float *hidden_in, float *hidden_out,
                            const void *const *shared_k, const void *const *shared_v,
@@ -218,7 +219,7 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan,
  * two event records per launch.  Under stream capture the event records
  * become graph nodes: read with keep_pairs = 1 after each replay (the pairs
  * stay assigned to the captured launches); keep_pairs = 0 releases them. */
-#define HPD_NUM_KERNEL_KINDS 9
+#define HPD_NUM_KERNEL_KINDS 8
 typedef struct {
   int64_t count[HPD_NUM_KERNEL_KINDS];
   double total_ms[HPD_NUM_KERNEL_KINDS];
@@ -227,7 +228,7 @@ typedef struct {
 hpd_status hpd_kernel_timing(int enable, int max_launches);
 hpd_status hpd_kernel_times_read(hpd_kernel_times *out, int keep_pairs);
 /* Kind k: 0 shared_prefix, 1 private, 2 merge, 3 gemm_qkv, 4 gemm_o,
- * 5 gemm_gate_up, 6 gemm_down, 7 residual_norm, 8 gemm_epilogue. */
+ * 5 gemm_gate_up, 6 gemm_down, 7 residual_norm. */
 const char *hpd_kernel_kind_name(int kind);
 
 const char *hpd_status_string(hpd_status status);

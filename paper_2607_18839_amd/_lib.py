@@ -223,7 +223,7 @@ def hpd_decode_step(model, plan, hidden_in, hidden_out, shared_k, shared_v, priv
                                   stream), "hpd_decode_step")
 
 
-HPD_NUM_KERNEL_KINDS = 9
+HPD_NUM_KERNEL_KINDS = 8
 
 
 class hpd_kernel_times(ctypes.Structure):

@@ -4,21 +4,22 @@
 // (Algorithm 1, the parallel draft over the active pool).  Per layer, with
 // the residual stream h [T][hidden] kept in fp32 in hidden_out:
 //   1 [h += previous down projection] RMSNorm(h) -> x (bf16)
-//   2 QKV GEMM (split-K partials), epilogue kernel -> q (bf16) and the new
-//     K/V rows, written into the layer's private cache at row priv_row + L + j
+//   2 QKV GEMM -> q (bf16) and the new K/V rows (bf16), written into the
+//     layer's private cache at row priv_row + L + j
 //   3 branch attention (shared-prefix, private, merge kernels) -> a (bf16)
-//   4 O GEMM (partials)
-//   5 h += a W_o^T, RMSNorm(h) -> x as hi + lo bf16 terms (one kernel)
-//   6 gate/up GEMM (partials), SwiGLU epilogue kernel -> m, hi + lo terms
-//   7 down GEMM (partials), added to h by the next layer's step 1 (or by a
-//     final residual kernel after the last layer)
+//   4 O GEMM (split-K partials)
+//   5 h += a W_o^T, RMSNorm(h) -> x (fp16) (one kernel)
+//   6 gate/up GEMM (fp16), SwiGLU -> m (fp16)
+//   7 down GEMM (fp16, partials), added to h by the next layer's step 1 (or
+//     by a final residual kernel after the last layer)
 // (section "Overview", paragraph "LLM Decoder": GQA, RMSNorm, SwiGLU).
 // Split-K partials are summed by the consuming kernel in split order, so the
 // result does not depend on scheduling and needs no cross-workgroup sync.
+// Buffers: x, q, attn, m and the partials live in the workspace after the
+// attention plan's tables; rows T..Tpad-1 of x, attn and m are kept zero.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-#include <cstdlib>
 #include <string>
 
 #include "gemm.h"
@@ -34,68 +35,36 @@ namespace {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-struct GemmShape {
-  int n_slices, ksplit, k_per_wg, n_tgroups;
-};
-
-// Split-K factor of one projection: the largest divisor of K / 32 that keeps
-// the grid within `max_wg` workgroups (default 512, two per CU) and leaves
-// each split at least `min_k` (default 256) of K, so that a split's fp32
-// partial tile (64 x Tpad) stays about as large as the weight slice it comes
-// from.  With one split the QKV and SwiGLU epilogues run inside the GEMM;
-// otherwise a consumer kernel adds the splits in order.
-GemmShape gemm_shape(int N_virtual, int K, int Tpad, bool allow_split) {
-  GemmShape s;
-  s.n_slices = N_virtual / 64;
-  s.n_tgroups = (Tpad + kGemmTokenGroup - 1) / kGemmTokenGroup;
-  const int steps = K / 32;
-  int max_wg = 512, min_k = 256;
-  if (const char *e = std::getenv("HPD_GEMM_MAX_WG")) max_wg = std::max(1, std::atoi(e));
-  if (const char *e = std::getenv("HPD_GEMM_MIN_K")) min_k = std::max(32, std::atoi(e));
-  s.ksplit = 1;
-  if (allow_split)
-    for (int d = 1; d <= steps; ++d)
-      if (steps % d == 0 && s.n_tgroups * s.n_slices * d <= max_wg && K / d >= min_k) s.ksplit = d;
-  s.k_per_wg = K / s.ksplit;
-  return s;
-}
-
 struct DecodeLayout {
   int T, Tpad, H, I, nq, nkv;
   GemmShape qkv, o, gu, down;
-  size_t off_x_hi, off_x_lo, off_q, off_attn, off_m_hi, off_m_lo, off_part, bytes;
+  size_t off_x, off_q, off_attn, off_m, off_part, bytes;
 };
 
 DecodeLayout decode_layout(const hpd_model_desc &m, const Plan &P) {
   DecodeLayout L;
   L.T = P.T;
-  // one token group of up to 144 rows; beyond that whole groups of 144
-  L.Tpad = P.T <= kGemmTokenGroup ? (P.T + 15) / 16 * 16
-                                  : (P.T + kGemmTokenGroup - 1) / kGemmTokenGroup * kGemmTokenGroup;
+  L.Tpad = (P.T + kGemmTile - 1) / kGemmTile * kGemmTile;
   L.H = m.hidden;
   L.I = m.intermediate;
   L.nq = P.attn.num_q_heads * HPD_HEAD_DIM;
   L.nkv = P.attn.num_kv_heads * HPD_HEAD_DIM;
-  const bool split_wide = std::getenv("HPD_GEMM_NO_SPLIT_WIDE") == nullptr;
-  L.qkv = gemm_shape(L.nq + 2 * L.nkv, L.H, L.Tpad, split_wide);
-  L.o = gemm_shape(L.H, L.nq, L.Tpad, true);
-  L.gu = gemm_shape(2 * L.I, L.H, L.Tpad, split_wide);
-  L.down = gemm_shape(L.H, L.I, L.Tpad, true);
+  L.qkv = choose_gemm_shape(L.nq + 2 * L.nkv, L.H, L.Tpad, kEpiQKV);
+  L.o = choose_gemm_shape(L.H, L.nq, L.Tpad, kEpiResidual);
+  L.gu = choose_gemm_shape(2 * L.I, L.H, L.Tpad, kEpiSwiGLU);
+  L.down = choose_gemm_shape(L.H, L.I, L.Tpad, kEpiResidual);
   size_t off = align256(P.workspace_bytes);
   auto take = [&](size_t bytes) {
     const size_t at = off;
     off = align256(off + bytes);
     return at;
   };
-  L.off_x_hi = take((size_t)L.Tpad * L.H * 2);
-  L.off_x_lo = take((size_t)L.Tpad * L.H * 2);
+  L.off_x = take((size_t)L.Tpad * L.H * 2);
   L.off_q = take((size_t)L.T * L.nq * 2);
   L.off_attn = take((size_t)L.Tpad * L.nq * 2);
-  L.off_m_hi = take((size_t)L.Tpad * L.I * 2);
-  L.off_m_lo = take((size_t)L.Tpad * L.I * 2);
-  size_t part = 0;
-  for (const GemmShape &s : {L.qkv, L.o, L.gu, L.down})
-    part = std::max(part, (size_t)s.ksplit * L.Tpad * s.n_slices * 64 * sizeof(float));
+  L.off_m = take((size_t)L.Tpad * L.I * 2);
+  // partials of the residual projections (O, down); N = hidden for both
+  const size_t part = (size_t)std::max(L.o.ksplit, L.down.ksplit) * L.Tpad * L.H * sizeof(float);
   L.off_part = take(part);
   L.bytes = off;
   return L;
@@ -175,9 +144,9 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
   }
   hipStream_t stream = (hipStream_t)stream_;
   unsigned char *ws = (unsigned char *)workspace;
-  __bf16 *x_hi = (__bf16 *)(ws + L.off_x_hi), *x_lo = (__bf16 *)(ws + L.off_x_lo);
+  __bf16 *x = (__bf16 *)(ws + L.off_x);   // bf16 (attention input) or fp16 (MLP input)
   __bf16 *q = (__bf16 *)(ws + L.off_q), *attn = (__bf16 *)(ws + L.off_attn);
-  __bf16 *m_hi = (__bf16 *)(ws + L.off_m_hi), *m_lo = (__bf16 *)(ws + L.off_m_lo);
+  __bf16 *mlp = (__bf16 *)(ws + L.off_m);   // SwiGLU product, fp16 bits
   float *part = (float *)(ws + L.off_part);
   const hpd::PlanDev dev = hpd::plan_dev(P, workspace);
 
@@ -186,16 +155,16 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
     e = hipMemcpyAsync(hidden_out, hidden_in, (size_t)L.T * L.H * sizeof(float), hipMemcpyDeviceToDevice,
                        stream);
   float *h = hidden_out;
-  auto base = [&](const hpd::GemmShape &s, const __bf16 *xh, const __bf16 *xl, int K) {
+  auto base = [&](const hpd::GemmShape &s, const __bf16 *xh, int N, int K) {
     hpd::GemmArgs g{};
     g.K = K;
-    g.N = 64 * s.n_slices;
-    g.n_slices = s.n_slices;
+    g.N = N;
+    g.rg = s.rg;
+    g.n_slices = N / (hpd::kGemmTile * s.rg);
     g.ksplit = s.ksplit;
-    g.k_per_wg = s.k_per_wg;
-    g.n_tgroups = s.n_tgroups;
-    g.x_hi = xh;
-    g.x_lo = xl;
+    g.k_per_wg = K / s.ksplit;
+    g.n_ttiles = L.Tpad / hpd::kGemmTile;
+    g.x = xh;
     g.T = L.T;
     g.Tpad = L.Tpad;
     g.part = part;
@@ -205,12 +174,12 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
   for (int l = 0; l < m.num_layers && e == hipSuccess; ++l) {
     const __bf16 *g1 = m.g_attn_norm ? (const __bf16 *)m.g_attn_norm[l] : nullptr;
     const __bf16 *g2 = m.g_mlp_norm ? (const __bf16 *)m.g_mlp_norm[l] : nullptr;
-    // 1: previous layer's down projection into h, attention-input norm
+    // 1: previous layer's down projection into h, attention-input norm (bf16)
     e = hpd::launch_residual_norm(h, pending_ksplit ? part : nullptr, pending_ksplit, L.Tpad, L.H, L.T, g1,
-                                  m.rms_eps, x_hi, nullptr, attn, L.nq, stream);
+                                  m.rms_eps, x, false, attn, L.nq, stream);
     if (e != hipSuccess) break;
     // 2: QKV projection; the epilogue appends the new K/V rows to the cache
-    hpd::GemmArgs g = base(L.qkv, x_hi, nullptr, L.H);
+    hpd::GemmArgs g = base(L.qkv, x, L.nq + 2 * L.nkv, L.H);
     g.w0 = (const __bf16 *)m.w_qkv[l];
     g.q_out = q;
     g.n_q = L.nq;
@@ -224,31 +193,30 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
     e = hpd::launch_branch_attention(P, q, shared_k ? shared_k[l] : nullptr, shared_v ? shared_v[l] : nullptr,
                                      priv_k[l], priv_v[l], attn, nullptr, workspace, stream);
     if (e != hipSuccess) break;
-    // 4 + 5: O projection, residual add and MLP-input norm
-    g = base(L.o, attn, nullptr, L.nq);
+    // 4 + 5: O projection, residual add and MLP-input norm (fp16)
+    g = base(L.o, attn, L.H, L.nq);
     g.w0 = (const __bf16 *)m.w_o[l];
     e = hpd::launch_gemm(g, false, hpd::kEpiResidual, hpd::KK_GEMM_O, stream);
     if (e != hipSuccess) break;
-    e = hpd::launch_residual_norm(h, part, L.o.ksplit, L.Tpad, L.H, L.T, g2, m.rms_eps, x_hi, x_lo, nullptr, 0,
+    e = hpd::launch_residual_norm(h, part, L.o.ksplit, L.Tpad, L.H, L.T, g2, m.rms_eps, x, true, nullptr, 0,
                                   stream);
     if (e != hipSuccess) break;
-    // 6: gate/up projection, SwiGLU
-    g = base(L.gu, x_hi, x_lo, L.H);
+    // 6: gate/up projection, SwiGLU (fp16)
+    g = base(L.gu, x, 2 * L.I, L.H);
     g.w0 = (const __bf16 *)m.w_gate[l];
     g.w1 = (const __bf16 *)m.w_up[l];
-    g.m_hi = m_hi;
-    g.m_lo = m_lo;
+    g.m_out = mlp;
     g.I = L.I;
     e = hpd::launch_gemm(g, true, hpd::kEpiSwiGLU, hpd::KK_GEMM_GATE_UP, stream);
     if (e != hipSuccess) break;
-    // 7: down projection (added to h by the next layer's first kernel)
-    g = base(L.down, m_hi, m_lo, L.I);
+    // 7: down projection (fp16; added to h by the next layer's first kernel)
+    g = base(L.down, mlp, L.H, L.I);
     g.w0 = (const __bf16 *)m.w_down[l];
     e = hpd::launch_gemm(g, true, hpd::kEpiResidual, hpd::KK_GEMM_DOWN, stream);
     pending_ksplit = L.down.ksplit;
   }
   if (e == hipSuccess)
-    e = hpd::launch_residual_norm(h, part, pending_ksplit, L.Tpad, L.H, L.T, nullptr, m.rms_eps, nullptr, nullptr,
+    e = hpd::launch_residual_norm(h, part, pending_ksplit, L.Tpad, L.H, L.T, nullptr, m.rms_eps, nullptr, false,
                                   nullptr, 0, stream);
   if (e != hipSuccess) {
     hpd::set_last_error(std::string("hpd_decode_step: ") + hipGetErrorString(e));

@@ -3,25 +3,29 @@
 //
 // Every projection of the step is a skinny GEMM: T ~ 130 token rows against a
 // bf16 weight matrix W[N][K] that is streamed from HBM once per step.  It is
-// computed transposed, Y^T[N][T] = W X^T, on v_mfma_f32_16x16x32_bf16 with W
-// as the A operand (16 weight rows per tile, read straight from HBM into
-// registers) and the token rows X (bf16, [Tpad][K], L2-resident) as the B
-// operand, Tpad = T rounded up to 16.
+// computed transposed, Y^T[N][T] = W X^T, on v_mfma_f32_32x32x16 with W as the
+// A operand and the token rows X ([Tpad][K], L2-resident) as the B operand,
+// Tpad = T rounded up to 32.
 //
-// Workgroup = 4 waves = one 64-row slice of W over one range of K; the four
-// waves take consecutive quarters of that K range, each accumulating the full
-// 64 x Tpad tile (every activation fragment it loads feeds 4 MFMAs), and are
-// summed through LDS in a fixed order.  Large K ranges are split over several
-// workgroups ("split-K"); the last workgroup of a slice to arrive (arrival
-// counter) adds the partial tiles in split order and runs the epilogue, so
-// results do not depend on scheduling.
+// Work decomposition.  The cost of such a GEMM is the bytes each CU must pull
+// in (its weight rows plus the token rows it multiplies them with), not the
+// MFMA work, so the tiles are small: each wave owns one 32 x 32 output tile
+// (32 weight rows x 32 tokens) over a K range.  The 4 waves of a workgroup
+// split either the rows (rg = 4: the token tile is shared), or K (rg = 1: four
+// K quarters, added through LDS at the end, in wave order), or both (rg = 2).
+// Operands stream through a 4-step LDS ring filled by direct global -> LDS
+// copies (8 rows x 128 bytes per instruction), 3 steps ahead of the MFMAs.
+// Residual projections may also split K over workgroups ("split-K"); those
+// partial tiles are added, in split order, by the residual + RMSNorm kernel,
+// so there is no cross-workgroup synchronisation and the result does not
+// depend on scheduling.  The QKV and SwiGLU epilogues run in the GEMM.
 //
-// Activations that feed the MLP (RMSNorm output and the SwiGLU product) are
-// carried as two bf16 terms hi + lo (lo = x - hi rounded to bf16) and
-// multiplied with two MFMAs, which keeps them at ~16 significant bits;
-// rounding them to one bf16 term costs ~1e-2 of absolute error on the
-// residual stream after 18 layers.  The QKV and O projections take a single
-// bf16 term (their rounding costs ~5e-4).
+// Precision: the QKV and O projections take bf16 activations (rounding them
+// costs ~5e-4 of absolute error on the residual stream after 18 layers).  The
+// MLP projections are sensitive (a single bf16 rounding of their inputs costs
+// ~1e-2), so they run in fp16: the bf16 weights convert to fp16 exactly (all
+// normal-range values; |w| < 2^-14 lose at most 2^-25 absolutely) and the
+// activations carry 11 significant bits.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -35,172 +39,198 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-constexpr int kMaxTPW = 3;   // token tiles per wave (a group of 9 tiles -> 3 waves of 3)
-
-__device__ __forceinline__ f32x4 mma16(const bf16x8 &a, const bf16x8 &b, const f32x4 &c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 // ------------------------------------------------------------ GEMM
 
-// Fragments of one 32-wide k step of one wave: the 4 weight tiles of the
-// workgroup's 64 rows and the wave's TPW token tiles, x2 when the activations
-// carry hi + lo terms.
-template <int kTPW, bool SPLIT> struct StepFrags {
-  bf16x8 a[4];
-  bf16x8 b[kTPW];
-  bf16x8 bl[SPLIT ? kTPW : 1];
-};
-
-template <int kTPW, bool SPLIT>
-__device__ __forceinline__ void load_step(StepFrags<kTPW, SPLIT> &f, const __bf16 *const *wrow,
-                                          const __bf16 *const *xh, const __bf16 *const *xl, int k) {
+// 8 bf16 -> 8 fp16 (round to nearest even; exact for |w| >= 2^-14).
+__device__ __forceinline__ u32x4 bf16x8_to_f16x8(u32x4 v) {
+  u32x4 r;
 #pragma unroll
-  for (int nt = 0; nt < 4; ++nt) f.a[nt] = *(const bf16x8 *)(wrow[nt] + k);
-#pragma unroll
-  for (int j = 0; j < kTPW; ++j) {
-    f.b[j] = *(const bf16x8 *)(xh[j] + k);
-    if constexpr (SPLIT) f.bl[j] = *(const bf16x8 *)(xl[j] + k);
+  for (int i = 0; i < 4; ++i) {
+    const float lo = __uint_as_float(v[i] << 16), hi = __uint_as_float(v[i] & 0xffff0000u);
+    const _Float16 l16 = (_Float16)lo, h16 = (_Float16)hi;
+    r[i] = (unsigned)__builtin_bit_cast(unsigned short, l16) | ((unsigned)__builtin_bit_cast(unsigned short, h16) << 16);
   }
+  return r;
 }
 
-// hi terms of every tile first, then the lo terms: consecutive MFMAs never
-// update the same accumulator.  No branches: a tile beyond the group's last
-// one repeats that tile and is simply not stored.
-template <int kTPW, bool SPLIT>
-__device__ __forceinline__ void mma_step(f32x4 (&acc)[4][kTPW], const StepFrags<kTPW, SPLIT> &f) {
-#pragma unroll
-  for (int j = 0; j < kTPW; ++j)
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt) acc[nt][j] = mma16(f.a[nt], f.b[j], acc[nt][j]);
-  if constexpr (SPLIT) {
-#pragma unroll
-    for (int j = 0; j < kTPW; ++j)
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt) acc[nt][j] = mma16(f.a[nt], f.bl[j], acc[nt][j]);
-  }
+// LDS rows are 128 bytes (64 K values); 16-byte piece q of row r is stored at
+// piece q ^ ((r >> 1) & 7), so the 16 lanes of one LDS cycle (16 consecutive
+// rows, same logical piece) cover all 64 banks.
+__device__ __forceinline__ int swz(int row, int q) { return q ^ ((row >> 1) & 7); }
+
+// Direct global -> LDS copy of 16 bytes per lane: lane i of the wave writes
+// lds_base + 16 i (the LDS address must be wave-uniform).
+__device__ __forceinline__ void dma16(const void *src, void *lds_base) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)lds_base, 16, 0, 0);
 }
 
-// Workgroup = ceil(tiles / TPW) waves = 64 weight rows x one token group (up
-// to 9 tiles of 16 tokens) x one K range.  The waves split the token tiles
-// (TPW each) and each runs the whole K range, so a wave holds 4 x TPW
-// accumulator tiles and nothing has to be reduced across waves; the waves
-// read the same weight fragments at the same time (L1 hits after the first).
-// Split-K partials: part[ks][t][n] (fp32, row-major by token), added in
-// split order by the consumer.
-template <int kTPW, bool SPLIT, int EPI>
+// s_waitcnt vmcnt(n) with expcnt and lgkmcnt left free.
+template <int N> __device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier of the LDS ring: completes this wave's LDS reads but not
+// its in-flight global -> LDS copies (those are waited for by count).
+__device__ __forceinline__ void ring_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+constexpr int kRing = 4;   // LDS ring depth in pipeline steps
+
+// Each step (64 K) of a K group lands in LDS as RG weight tiles and one token
+// tile of [32 rows][128 bytes].  The copies are spread over the group's waves
+// with 8 rows x 128 bytes per instruction (8 cache lines), S - 1 steps ahead
+// of the MFMAs; each wave then reads its fragments from LDS.
+//
+// Fragments: lane l reads row l % 32, K values 32 (l / 32) + 8 j .. + 7 for
+// MFMA j of the step.  MFMA j thus contracts, in lane half h, the K values
+// 32 h + 8 j .. of the step: a permutation of the step's 64 K values that the
+// A (weight) and B (token) operands share, leaving the dot products unchanged.
+//
+// Output layout (v_mfma_f32_32x32x16): lane l holds, for token 32 tt + l % 32,
+// the weight rows 8 (r / 4) + 4 (l / 32) + r % 4 of the tile, r = 0..15.
+// SwiGLU tiles put 16 gate rows i0..i0+15 in tile rows 0..15 and the matching
+// up rows in tile rows 16..31, so gate register r pairs with up register
+// r + 8 of the same lane.
+template <int RG, bool F16, int EPI>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
-  constexpr bool SWIGLU = EPI == kEpiSwiGLU;
-  const int nwg = g.n_tgroups * g.n_slices * g.ksplit;
+  constexpr int KG = 4 / RG, S = kRing;
+  constexpr int kTileBytes = kGemmTile * 128;
+  constexpr int kGroupBytes = (RG + 1) * kTileBytes;
+  constexpr int kStageBytes = KG * kGroupBytes;
+  constexpr int kInstr = (RG + 1) * 4 / RG;   // copy instructions per wave per step
+  __shared__ __attribute__((aligned(16))) unsigned char lds[S * kStageBytes];
+
+  const int nwg = g.n_slices * g.n_ttiles * g.ksplit;
   const int per_xcd = gridDim.x / 8;
-  // XCD-aware order: consecutive logical tiles share an XCD (and its L2).
+  // XCD-aware order: consecutive logical tiles share an XCD (and its L2); the
+  // token tiles of one weight slice are consecutive, so the slice is fetched
+  // from HBM once per XCD.
   const int logical = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
   if (logical >= nwg) return;
-  const int tile_id = logical / g.ksplit, ks = logical % g.ksplit;   // tile = (token group, slice)
-  const int tg = tile_id / g.n_slices, slice = tile_id % g.n_slices;
+  const int ks = logical % g.ksplit, rest = logical / g.ksplit;
+  const int tt = rest % g.n_ttiles, slice = rest / g.n_ttiles;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  // token tiles of this group: wave w takes tiles w TPW .. w TPW + TPW - 1
-  const int ntt = min(kGemmMaxTokenTiles, g.Tpad / 16 - tg * kGemmMaxTokenTiles);
-  const int tt0 = wave * kTPW;
-  if (tt0 >= ntt) return;
-  const int ntw = min(kTPW, ntt - tt0);            // tiles this wave stores
-  const int t0 = tg * kGemmTokenGroup + 16 * tt0;   // first token of the wave's first tile
-  const int kbeg = ks * g.k_per_wg, kend = kbeg + g.k_per_wg;
+  const int rg = wave % RG, kgi = wave / RG;
+  const int kw = g.k_per_wg / KG;   // K per wave
+  const int nsteps = kw / kGemmKStep;
+  const int64_t kbase = (int64_t)ks * g.k_per_wg + (int64_t)kgi * kw;
 
-  const __bf16 *wrow[4];
+  // copy sources: instruction q of the K group covers tile q / 4 (row group
+  // q / 4 < RG, else the token tile), rows 8 (q % 4) + lane / 8
+  const __bf16 *src[kInstr];
+  int dst[kInstr];
 #pragma unroll
-  for (int nt = 0; nt < 4; ++nt) {
-    int64_t r;
-    const __bf16 *base = g.w0;
-    if constexpr (SWIGLU) {
-      // tiles 0, 1: gate rows i0 .. i0 + 31; tiles 2, 3: up rows, same i
-      r = (int64_t)slice * 32 + 16 * (nt & 1) + (lane & 15);
-      if (nt >= 2) base = g.w1;
+  for (int j = 0; j < kInstr; ++j) {
+    const int q = rg * kInstr + j, ti = q / 4;
+    const int row = 8 * (q % 4) + (lane >> 3), piece = swz(row, lane & 7);
+    const __bf16 *p;
+    if (ti < RG) {
+      const int tile = slice * RG + ti;
+      if constexpr (EPI == kEpiSwiGLU) p = (row < 16 ? g.w0 : g.w1) + (int64_t)(tile * 16 + (row & 15)) * g.K;
+      else p = g.w0 + (int64_t)(tile * kGemmTile + row) * g.K;
     } else {
-      r = (int64_t)slice * 64 + 16 * nt + (lane & 15);
+      p = g.x + (int64_t)(tt * kGemmTile + row) * g.K;
     }
-    wrow[nt] = base + r * g.K + 8 * (lane >> 4);
+    src[j] = p + kbase + 8 * piece;
+    dst[j] = kgi * kGroupBytes + q * 1024;
   }
-  const __bf16 *xh[kTPW], *xl[kTPW];
+  auto issue = [&](int c) {
+    unsigned char *st = lds + (c % S) * kStageBytes;
 #pragma unroll
-  for (int j = 0; j < kTPW; ++j) {
-    const int jj = min(j, ntw - 1);   // absent tiles re-read the last present one
-    const int64_t off = (int64_t)(t0 + 16 * jj + (lane & 15)) * g.K + 8 * (lane >> 4);
-    xh[j] = g.x_hi + off;
-    xl[j] = SPLIT ? g.x_lo + off : nullptr;
-  }
+    for (int j = 0; j < kInstr; ++j) dma16(src[j] + c * kGemmKStep, st + dst[j]);
+  };
+  // wait until this wave's copies of the current step have landed, with
+  // `ahead` later steps still in flight
+  auto wait_step = [&](int ahead) {
+    if (ahead >= 2) wait_vm<2 * kInstr>();
+    else if (ahead == 1) wait_vm<kInstr>();
+    else wait_vm<0>();
+  };
 
-  f32x4 acc[4][kTPW];
+  f32x16 acc;
 #pragma unroll
-  for (int nt = 0; nt < 4; ++nt)
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  const int frow = lane & 31, half = lane >> 5;
+  const int a_off = kgi * kGroupBytes + rg * kTileBytes + frow * 128;
+  const int b_off = kgi * kGroupBytes + RG * kTileBytes + frow * 128;
 #pragma unroll
-    for (int j = 0; j < kTPW; ++j) acc[nt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // two k steps in flight; scheduling barriers keep each load batch ahead of
-  // the MFMAs that precede its use
-  StepFrags<kTPW, SPLIT> f0, f1;
-  load_step<kTPW, SPLIT>(f0, wrow, xh, xl, kbeg);
-  int k = kbeg;
-  for (; k + 64 <= kend; k += 64) {
-    load_step<kTPW, SPLIT>(f1, wrow, xh, xl, k + 32);
-    __builtin_amdgcn_sched_barrier(0);
-    mma_step<kTPW, SPLIT>(acc, f0);
-    __builtin_amdgcn_sched_barrier(0);
-    // unconditional (clamped in range on the last pass) so that the waits
-    // the compiler derives never have to cover a skipped batch
-    load_step<kTPW, SPLIT>(f0, wrow, xh, xl, k + 64 < kend ? k + 64 : k);
-    __builtin_amdgcn_sched_barrier(0);
-    mma_step<kTPW, SPLIT>(acc, f1);
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  if (k < kend) mma_step<kTPW, SPLIT>(acc, f0);
-
-  // lane holds virtual columns n = 64 slice + 16 nt + 4 (lane / 16) + r of
-  // token t0 + 16 j + lane % 16
-  const int nq = 4 * (lane >> 4);
-  if (g.ksplit > 1 || EPI == kEpiResidual) {
-    float *part = g.part + (int64_t)ks * g.Tpad * g.N;
+  for (int c = 0; c < S - 1; ++c)
+    if (c < nsteps) issue(c);
+  for (int c = 0; c < nsteps; ++c) {
+    wait_step(min(nsteps - 1 - c, S - 2));
+    ring_barrier();   // step c visible to every wave; the slot of step c - 1 is free
+    if (c + S - 1 < nsteps) issue(c + S - 1);
+    const unsigned char *st = lds + (c % S) * kStageBytes;
+    u32x4 av[4], bv[4];   // all fragments of the step are read before the first MFMA
 #pragma unroll
-    for (int j = 0; j < kTPW; ++j) {
-      if (j >= ntw) continue;
-      const int t = t0 + 16 * j + (lane & 15);
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
-        *(f32x4 *)(part + (int64_t)t * g.N + slice * 64 + 16 * nt + nq) = acc[nt][j];
+    for (int j = 0; j < 4; ++j) {
+      av[j] = *(const u32x4 *)(st + a_off + 16 * swz(frow, 4 * half + j));
+      bv[j] = *(const u32x4 *)(st + b_off + 16 * swz(frow, 4 * half + j));
     }
-    return;
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if constexpr (F16)
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, bf16x8_to_f16x8(av[j])),
+                                                     __builtin_bit_cast(f16x8, bv[j]), acc, 0, 0, 0);
+      else
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av[j]),
+                                                      __builtin_bit_cast(bf16x8, bv[j]), acc, 0, 0, 0);
+    }
   }
-  // whole K in this workgroup: the epilogue runs here
+  const int tile = slice * RG + rg;   // 32-row tile of the output columns
+
+  if constexpr (KG > 1) {
+    // K groups 1.. hand their tiles to K group 0, which adds them in order
+    // (through the ring's LDS, once every wave is done with it).
+    float *red = (float *)lds;
+    ring_barrier();
+    if (kgi > 0) {
 #pragma unroll
-  for (int j = 0; j < kTPW; ++j) {
-    if (j >= ntw) continue;
-    const int t = t0 + 16 * j + (lane & 15);
-    if constexpr (EPI == kEpiQKV) {
-      if (t >= g.T) continue;
+      for (int r = 0; r < 16; ++r) red[(((kgi - 1) * RG + rg) * 16 + r) * 64 + lane] = acc[r];
+    }
+    __syncthreads();
+    if (kgi > 0) return;
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        const int n = slice * 64 + 16 * nt + nq;
-        bf16x4 v;
-        for (int r = 0; r < 4; ++r) v[r] = (__bf16)acc[nt][j][r];
-        if (n < g.n_q) *(bf16x4 *)(g.q_out + (int64_t)t * g.n_q + n) = v;
-        else if (n < g.n_q + g.n_kv) *(bf16x4 *)(g.k_cache + (int64_t)g.dest[t] * g.n_kv + (n - g.n_q)) = v;
-        else *(bf16x4 *)(g.v_cache + (int64_t)g.dest[t] * g.n_kv + (n - g.n_q - g.n_kv)) = v;
+    for (int k = 0; k < KG - 1; ++k)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[r] += red[((k * RG + rg) * 16 + r) * 64 + lane];
+  }
+
+  const int t = tt * kGemmTile + frow;
+  if constexpr (EPI == kEpiResidual) {
+    if (t >= g.T) return;
+    float *dst = g.part + ((int64_t)ks * g.Tpad + t) * g.N + tile * kGemmTile + 4 * half;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *(f32x4 *)(dst + 8 * i) = f32x4{acc[4 * i], acc[4 * i + 1], acc[4 * i + 2], acc[4 * i + 3]};
+  } else if constexpr (EPI == kEpiQKV) {
+    if (t >= g.T) return;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int n = tile * kGemmTile + 8 * i + 4 * half;   // 4-runs never straddle q / k / v
+      bf16x4 v;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) v[r] = (__bf16)acc[4 * i + r];
+      if (n < g.n_q) *(bf16x4 *)(g.q_out + (int64_t)t * g.n_q + n) = v;
+      else if (n < g.n_q + g.n_kv) *(bf16x4 *)(g.k_cache + (int64_t)g.dest[t] * g.n_kv + (n - g.n_q)) = v;
+      else *(bf16x4 *)(g.v_cache + (int64_t)g.dest[t] * g.n_kv + (n - g.n_q - g.n_kv)) = v;
+    }
+  } else {   // SwiGLU: m = silu(gate) * up, fp16; rows t >= T are written as zeros
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      f16x4 mv;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float gt = acc[4 * i + r], up = acc[4 * i + 8 + r];
+        mv[r] = (_Float16)(t < g.T ? gt / (1.0f + __expf(-gt)) * up : 0.f);
       }
-    } else if constexpr (EPI == kEpiSwiGLU) {
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt) {
-        const int i = slice * 32 + 16 * nt + nq;
-        bf16x4 hi, lo;
-        for (int r = 0; r < 4; ++r) {
-          const float gt = acc[nt][j][r], up = acc[nt + 2][j][r];
-          const float m = t < g.T ? gt / (1.0f + __expf(-gt)) * up : 0.f;
-          hi[r] = (__bf16)m;
-          lo[r] = (__bf16)(m - (float)hi[r]);
-        }
-        *(bf16x4 *)(g.m_hi + (int64_t)t * g.I + i) = hi;
-        *(bf16x4 *)(g.m_lo + (int64_t)t * g.I + i) = lo;
-      }
+      *(f16x4 *)((_Float16 *)g.m_out + (int64_t)t * g.I + tile * 16 + 8 * i + 4 * half) = mv;
     }
   }
 }
@@ -222,61 +252,19 @@ __device__ __forceinline__ f32x4 sum_splits(const float *part, int64_t split_str
   return s;
 }
 
-// QKV: y = sum of splits; q -> q_out, k/v -> cache rows dest[t] (bf16).
-__global__ __launch_bounds__(256) void qkv_epilogue_kernel(GemmArgs g) {
-  const int64_t i4 = (int64_t)blockIdx.x * 256 + threadIdx.x;   // one group of 4 columns
-  const int N = g.N;
-  if (i4 * 4 >= (int64_t)g.T * N) return;
-  const int t = (int)(i4 * 4 / N), n = (int)(i4 * 4 % N);
-  const f32x4 y = sum_splits(g.part + (int64_t)t * N + n, (int64_t)g.Tpad * N, g.ksplit);
-  bf16x4 v;
-  for (int r = 0; r < 4; ++r) v[r] = (__bf16)y[r];
-  if (n < g.n_q) *(bf16x4 *)(g.q_out + (int64_t)t * g.n_q + n) = v;
-  else if (n < g.n_q + g.n_kv) *(bf16x4 *)(g.k_cache + (int64_t)g.dest[t] * g.n_kv + (n - g.n_q)) = v;
-  else *(bf16x4 *)(g.v_cache + (int64_t)g.dest[t] * g.n_kv + (n - g.n_q - g.n_kv)) = v;
-}
-
-// gate/up: m = silu(sum gate) * (sum up), written as hi + lo bf16 terms
-// [Tpad][I] (zero rows t >= T).  Virtual column of gate i: 64 (i / 32) + i % 32,
-// of up i: that + 32.
-__global__ __launch_bounds__(256) void swiglu_epilogue_kernel(GemmArgs g) {
-  const int64_t i4 = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int I = g.I;
-  if (i4 * 4 >= (int64_t)g.Tpad * I) return;
-  const int t = (int)(i4 * 4 / I), i = (int)(i4 * 4 % I);
-  bf16x4 hi, lo;
-  if (t < g.T) {
-    const int vg = 64 * (i / 32) + i % 32;
-    const f32x4 gs = sum_splits(g.part + (int64_t)t * g.N + vg, (int64_t)g.Tpad * g.N, g.ksplit);
-    const f32x4 us = sum_splits(g.part + (int64_t)t * g.N + vg + 32, (int64_t)g.Tpad * g.N, g.ksplit);
-    for (int r = 0; r < 4; ++r) {
-      const float m = gs[r] / (1.0f + __expf(-gs[r])) * us[r];
-      hi[r] = (__bf16)m;
-      lo[r] = (__bf16)(m - (float)hi[r]);
-    }
-  } else {
-    for (int r = 0; r < 4; ++r) { hi[r] = (__bf16)0.f; lo[r] = (__bf16)0.f; }
-  }
-  *(bf16x4 *)(g.m_hi + (int64_t)t * I + i) = hi;
-  *(bf16x4 *)(g.m_lo + (int64_t)t * I + i) = lo;
-}
-
 // Residual + RMSNorm: h[t] += sum of the splits of `part` (if any), then
-// x = RMSNorm(h[t]) * gamma -> x_hi (+ x_lo) unless x_hi is NULL.  One
+// x = RMSNorm(h[t]) * gamma -> x_hi as bf16 (or fp16) unless x_hi is NULL.  One
 // workgroup per row t < Tpad; rows t >= T are written as zeros (also the
 // padding rows `zero_rows`).  H is a multiple of 4.
 __global__ __launch_bounds__(256) void residual_norm_kernel(float *h, const float *part, int ksplit, int Tpad,
                                                             int H, int T, const __bf16 *gamma, float eps,
-                                                            __bf16 *x_hi, __bf16 *x_lo, __bf16 *zero_rows,
+                                                            __bf16 *x_hi, int out_f16, __bf16 *zero_rows,
                                                             int zero_cols) {
   const int t = blockIdx.x;
   const int tid = threadIdx.x;
   if (t >= T) {
     if (x_hi)
-      for (int c = tid; c < H; c += 256) {
-        x_hi[(int64_t)t * H + c] = (__bf16)0.f;
-        if (x_lo) x_lo[(int64_t)t * H + c] = (__bf16)0.f;
-      }
+      for (int c = tid; c < H; c += 256) x_hi[(int64_t)t * H + c] = (__bf16)0.f;   // 0 in bf16 and fp16
     if (zero_rows)
       for (int c = tid; c < zero_cols; c += 256) zero_rows[(int64_t)t * zero_cols + c] = (__bf16)0.f;
     return;
@@ -300,67 +288,88 @@ __global__ __launch_bounds__(256) void residual_norm_kernel(float *h, const floa
   const float inv = 1.0f / sqrtf(tot / (float)H + eps);
   for (int c = 4 * tid; c < H; c += 1024) {
     const f32x4 v = *(const f32x4 *)(row + c);
-    bf16x4 hi, lo;
-    for (int r = 0; r < 4; ++r) {
-      float x = v[r] * inv;
-      if (gamma) x *= (float)gamma[c + r];
-      hi[r] = (__bf16)x;
-      lo[r] = (__bf16)(x - (float)hi[r]);
+    f32x4 x;
+    for (int r = 0; r < 4; ++r) x[r] = v[r] * inv * (gamma ? (float)gamma[c + r] : 1.f);
+    if (out_f16) {
+      f16x4 o;
+      for (int r = 0; r < 4; ++r) o[r] = (_Float16)x[r];
+      *(f16x4 *)((_Float16 *)x_hi + (int64_t)t * H + c) = o;
+    } else {
+      bf16x4 o;
+      for (int r = 0; r < 4; ++r) o[r] = (__bf16)x[r];
+      *(bf16x4 *)(x_hi + (int64_t)t * H + c) = o;
     }
-    *(bf16x4 *)(x_hi + (int64_t)t * H + c) = hi;
-    if (x_lo) *(bf16x4 *)(x_lo + (int64_t)t * H + c) = lo;
   }
 }
 
 }  // namespace
 
 hipError_t launch_residual_norm(float *h, const float *part, int ksplit, int Tpad, int H, int T,
-                                const __bf16 *gamma, float eps, __bf16 *x_hi, __bf16 *x_lo,
+                                const __bf16 *gamma, float eps, void *x_out, bool out_f16,
                                 __bf16 *zero_rows, int zero_cols, hipStream_t stream) {
   timed_begin(KK_NORM, stream);
   hipLaunchKernelGGL(residual_norm_kernel, dim3(Tpad), dim3(256), 0, stream, h, part, ksplit, Tpad, H, T, gamma,
-                     eps, x_hi, x_lo, zero_rows, zero_cols);
+                     eps, (__bf16 *)x_out, out_f16 ? 1 : 0, zero_rows, zero_cols);
   timed_end(stream);
   return hipGetLastError();
 }
 
-// Tpad is a multiple of 16; when it exceeds one token group it must be a
-// multiple of kGemmTokenGroup (every group then has the same tile count).
-hipError_t launch_gemm(const GemmArgs &g, bool split, int epi, int kind, hipStream_t stream) {
-  const int ntt = std::min(kGemmMaxTokenTiles, g.Tpad / 16);
-  if (g.Tpad % 16 != 0 || (g.n_tgroups > 1 && g.Tpad % kGemmTokenGroup != 0) ||
-      (g.n_tgroups - 1) * kGemmMaxTokenTiles + ntt != g.Tpad / 16 || g.k_per_wg % 32 != 0)
+namespace {
+
+template <bool F16, int EPI>
+void launch_epi(const GemmArgs &g, dim3 grid, hipStream_t stream) {
+  if (g.rg == 4) hipLaunchKernelGGL((gemm_kernel<4, F16, EPI>), grid, dim3(256), 0, stream, g);
+  else if (g.rg == 2) hipLaunchKernelGGL((gemm_kernel<2, F16, EPI>), grid, dim3(256), 0, stream, g);
+  else hipLaunchKernelGGL((gemm_kernel<1, F16, EPI>), grid, dim3(256), 0, stream, g);
+}
+
+}  // namespace
+
+hipError_t launch_gemm(const GemmArgs &g, bool f16, int epi, int kind, hipStream_t stream) {
+  const int kg = g.rg == 4 ? 1 : g.rg == 2 ? 2 : g.rg == 1 ? 4 : 0;
+  if (kg == 0 || g.K <= 0 || g.ksplit < 1 || (int64_t)g.ksplit * g.k_per_wg != g.K ||
+      g.k_per_wg % (kGemmKStep * kg) != 0 || g.Tpad % kGemmTile != 0 || g.n_ttiles * kGemmTile != g.Tpad ||
+      g.T > g.Tpad || g.N != g.n_slices * kGemmTile * g.rg || (epi != kEpiResidual && g.ksplit != 1) ||
+      (epi == kEpiSwiGLU && (g.N != 2 * g.I || !f16)) || (epi == kEpiQKV && f16))
     return hipErrorInvalidValue;
-  const int nwg = g.n_tgroups * g.n_slices * g.ksplit;
-  const int tpw = std::min(kMaxTPW, ntt);
-  const int waves = (ntt + tpw - 1) / tpw;
-  const dim3 grid((nwg + 7) / 8 * 8), block(64 * waves);
+  const int nwg = g.n_slices * g.n_ttiles * g.ksplit;
+  if (nwg == 0) return hipSuccess;
+  const dim3 grid((nwg + 7) / 8 * 8);
   timed_begin(kind, stream);
-#define HPD_GEMM_LAUNCH(TPW)                                                                                   \
-  if (epi == kEpiSwiGLU) hipLaunchKernelGGL((gemm_kernel<TPW, true, kEpiSwiGLU>), grid, block, 0, stream, g);    \
-  else if (epi == kEpiQKV) hipLaunchKernelGGL((gemm_kernel<TPW, false, kEpiQKV>), grid, block, 0, stream, g);    \
-  else if (split) hipLaunchKernelGGL((gemm_kernel<TPW, true, kEpiResidual>), grid, block, 0, stream, g);        \
-  else hipLaunchKernelGGL((gemm_kernel<TPW, false, kEpiResidual>), grid, block, 0, stream, g);
-  if (tpw == 3) { HPD_GEMM_LAUNCH(3) }
-  else if (tpw == 2) { HPD_GEMM_LAUNCH(2) }
-  else { HPD_GEMM_LAUNCH(1) }
-#undef HPD_GEMM_LAUNCH
+  if (epi == kEpiSwiGLU) launch_epi<true, kEpiSwiGLU>(g, grid, stream);
+  else if (epi == kEpiQKV) launch_epi<false, kEpiQKV>(g, grid, stream);
+  else if (f16) launch_epi<true, kEpiResidual>(g, grid, stream);
+  else launch_epi<false, kEpiResidual>(g, grid, stream);
   timed_end(stream);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  if (g.ksplit == 1) return hipSuccess;   // QKV / SwiGLU epilogues ran inside the GEMM
-  if (epi == kEpiQKV) {
-    timed_begin(KK_EPILOGUE, stream);
-    const int64_t n4 = (int64_t)g.T * g.N / 4;
-    hipLaunchKernelGGL(qkv_epilogue_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, stream, g);
-    timed_end(stream);
-  } else if (epi == kEpiSwiGLU) {
-    timed_begin(KK_EPILOGUE, stream);
-    const int64_t n4 = (int64_t)g.Tpad * g.I / 4;
-    hipLaunchKernelGGL(swiglu_epilogue_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, stream, g);
-    timed_end(stream);
-  }
   return hipGetLastError();
+}
+
+// Bytes one CU streams for a tile choice: per workgroup (32 rg + 32) rows of
+// k_per_wg K values (2 bytes each) plus its partial tile, times the
+// workgroups per CU (256 CUs); split-K adds the partials the residual kernel
+// reads back.  The cheapest shape wins (fewer workgroups on ties).
+GemmShape choose_gemm_shape(int N, int K, int Tpad, int epi) {
+  GemmShape best{0, 0};
+  double best_cost = 0;
+  const int tiles = Tpad / kGemmTile;
+  for (int rg : {1, 2, 4}) {
+    const int kg = 4 / rg;
+    if (N % (kGemmTile * rg) != 0) continue;
+    for (int ks = 1; ks <= 32; ++ks) {
+      if (ks > 1 && epi != kEpiResidual) break;
+      if (K % ks != 0 || (K / ks) % (kGemmKStep * kg) != 0) continue;
+      const double nwg = (double)(N / (kGemmTile * rg)) * tiles * ks;
+      double per_wg = (double)(kGemmTile * rg + kGemmTile) * (K / ks) * 2;
+      if (epi == kEpiResidual) per_wg += (double)kGemmTile * rg * kGemmTile * 4;
+      double cost = per_wg * std::max(1.0, nwg / 256.0);
+      if (ks > 1) cost += (double)ks * Tpad * N * 4 / 256.0;
+      if (best.rg == 0 || cost < best_cost * 0.999) {
+        best = GemmShape{rg, ks};
+        best_cost = cost;
+      }
+    }
+  }
+  return best;
 }
 
 }  // namespace hpd

@@ -23,7 +23,7 @@ PlanDev plan_dev(const Plan &P, void *workspace);
 
 // Kernel kinds of the optional benchmark timing (hpd_kernel_timing).
 enum KernelKind { KK_SHARED = 0, KK_PRIVATE, KK_MERGE, KK_GEMM_QKV, KK_GEMM_O, KK_GEMM_GATE_UP,
-                  KK_GEMM_DOWN, KK_NORM, KK_EPILOGUE };
+                  KK_GEMM_DOWN, KK_NORM };
 void timed_begin(int kind, hipStream_t stream);
 void timed_end(hipStream_t stream);
 

@@ -93,6 +93,34 @@ __global__ void chase_kernel(const unsigned *next, int steps, unsigned *out) {
   out[0] = p;
 }
 
+// Each workgroup writes its 4 KB tile; with `fence`, it then publishes it with
+// an agent-scope release + arrival counter and the last arriving workgroup
+// reads a tile back after an acquire -- the synchronisation cost of an
+// in-kernel cross-workgroup reduction.  The counter is reset by the last
+// arrival.
+__global__ __launch_bounds__(256) void arrive_kernel(float *tiles, int *counter, float *sink, int fence) {
+  float *my = tiles + (size_t)blockIdx.x * 1024;
+  for (int i = threadIdx.x; i < 1024; i += 256) my[i] = (float)(blockIdx.x + i);
+  if (!fence) return;
+  __threadfence();
+  __shared__ int last;
+  if (threadIdx.x == 0) {
+    const int old = __hip_atomic_fetch_add(counter, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    last = old == (int)gridDim.x - 1;
+  }
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  float s = 0.f;
+  for (int i = threadIdx.x; i < 1024; i += 256) s += tiles[i];   // one tile back
+  if (s == 123.456f) sink[0] = s;
+  if (threadIdx.x == 0) __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__global__ void empty_kernel(float *sink) {
+  if (threadIdx.x == 1023) sink[0] = 0.f;
+}
+
 template <typename F> float time_ms(F launch, int reps) {
   hipEvent_t a, b;
   CHECK(hipEventCreate(&a));
@@ -152,12 +180,33 @@ int main(int argc, char **argv) {
   const int steps = 20000;
   const float chase_ms = time_ms([&] { hipLaunchKernelGGL(chase_kernel, dim3(1), dim3(1), 0, 0, d_next, steps, d_out); }, 3);
 
+  // dispatch floor: back-to-back empty launches (256 workgroups) on a stream and in a graph
+  const float empty_ms = time_ms([&] { hipLaunchKernelGGL(empty_kernel, dim3(256), dim3(256), 0, 0, sink); }, 200);
+  hipStream_t gs;
+  CHECK(hipStreamCreate(&gs));
+  hipGraph_t graph;
+  hipGraphExec_t exec;
+  CHECK(hipStreamBeginCapture(gs, hipStreamCaptureModeGlobal));
+  for (int i = 0; i < 100; ++i) hipLaunchKernelGGL(empty_kernel, dim3(256), dim3(256), 0, gs, sink);
+  CHECK(hipStreamEndCapture(gs, &graph));
+  CHECK(hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0));
+  const float graph_ms = time_ms([&] { hipGraphLaunch(exec, 0); }, 10) / 100.f;
+
+  float *tiles;
+  int *counter;
+  CHECK(hipMalloc(&tiles, (size_t)512 * 1024 * 4));
+  CHECK(hipMalloc(&counter, 64));
+  CHECK(hipMemset(counter, 0, 64));
+  const float nofence_ms = time_ms([&] { hipLaunchKernelGGL(arrive_kernel, dim3(512), dim3(256), 0, 0, tiles, counter, sink, 0); }, 50);
+  const float fence_ms = time_ms([&] { hipLaunchKernelGGL(arrive_kernel, dim3(512), dim3(256), 0, 0, tiles, counter, sink, 1); }, 50);
+
   std::printf("{\"device\": \"%s\", \"cus\": %d, \"clock_mhz\": %d, \"copy_mib\": %zu, "
               "\"copy_gbs\": %.1f, \"read_gbs\": %.1f, \"mfma_bf16_tflops\": %.1f, "
               "\"mfma32_bf16_tflops\": %.1f, \"exp2_gops\": %.1f, \"exp2_per_cu_per_clk\": %.2f, \"load_latency_ns\": %.0f, "
-              "\"copy_us\": %.2f}\n",
+              "\"copy_us\": %.2f, \"empty_kernel_stream_us\": %.2f, \"empty_kernel_graph_us\": %.2f, \"arrive512_nofence_us\": %.2f, \"arrive512_fence_us\": %.2f}\n",
               prop.gcnArchName, cus, prop.clockRate / 1000, mib, 2.0 * bytes / copy_ms / 1e6,
               bytes / read_ms / 1e6, mfma_flop / mfma_ms / 1e9, mfma32_flop / mfma32_ms / 1e9, exps / exp_ms / 1e6,
-              exps / (exp_ms * 1e-3) / cus / (prop.clockRate * 1e3), chase_ms * 1e6 / steps, copy_ms * 1e3);
+              exps / (exp_ms * 1e-3) / cus / (prop.clockRate * 1e3), chase_ms * 1e6 / steps, copy_ms * 1e3,
+              empty_ms * 1e3, graph_ms * 1e3, nofence_ms * 1e3, fence_ms * 1e3);
   return 0;
 }
