@@ -178,18 +178,21 @@ def bench_attention(args, torch, _lib):
     peak_mfma = BF16_PEAK_TFLOPS if b.dtype == "bf16" else FP32_PEAK_TFLOPS
     sh = kern.get("shared_prefix", {}).get("avg_us")
     pr = kern.get("private", {}).get("avg_us")
+    # bf16: one launch runs the shared-prefix and the private work items
+    sh_flop = w["shared_flop"] + (0 if pr else w["private_flop"])
     if sh:
-        kern["shared_prefix"].update(flop=w["shared_flop"], tflops=w["shared_flop"] / sh / 1e6,
-                                     mfma_frac=w["shared_flop"] / sh / 1e6 / peak_mfma)
+        kern["shared_prefix"].update(flop=sh_flop, tflops=sh_flop / sh / 1e6,
+                                     mfma_frac=sh_flop / sh / 1e6 / peak_mfma,
+                                     includes_private=not pr)
     if pr:
         kern["private"].update(bytes=w["private_bytes"], gbs=w["private_bytes"] / pr / 1e3,
                                hbm_frac=w["private_bytes"] / pr / 1e3 / HBM_PEAK_GBS)
     roof = None
     if sh:
-        ach = w["shared_flop"] / sh / 1e6
-        roof = {"bound": "mfma", "kernel": "shared_prefix_kernel", "achieved": ach, "peak": peak_mfma,
+        ach = sh_flop / sh / 1e6
+        roof = {"bound": "mfma", "kernel": "shared_prefix", "achieved": ach, "peak": peak_mfma,
                 "unit": "TFLOP/s", "frac": ach / peak_mfma, "traffic": None,
-                "algorithmic_per_launch": w["shared_flop"]}
+                "algorithmic_per_launch": sh_flop}
     res = {
         "metric": "branch-tokens/s per decode step", "value": w["T"] / (ms / 1e3), "unit": "branch-tokens/s",
         "n_gpus": 1, "steps": timed, "warmup": args.warmup, "ms_per_step": ms,
@@ -266,9 +269,10 @@ def bench_decode(args, torch, _lib):
     gw = gemm_work(T, Hq, Hkv, D, H, I)
     for name, k in kern.items():
         us = k["avg_us"]
-        if name == "shared_prefix":
-            k.update(bound="mfma", flop=aw["shared_flop"], tflops=aw["shared_flop"] / us / 1e6,
-                     frac=aw["shared_flop"] / us / 1e6 / BF16_PEAK_TFLOPS)
+        if name == "shared_prefix":   # bf16: also runs the private work items
+            fl = aw["shared_flop"] + (0 if "private" in kern else aw["private_flop"])
+            k.update(bound="mfma", flop=fl, tflops=fl / us / 1e6, frac=fl / us / 1e6 / BF16_PEAK_TFLOPS,
+                     includes_private="private" not in kern)
         elif name == "private":
             k.update(bound="hbm", bytes=aw["private_bytes"], gbs=aw["private_bytes"] / us / 1e3,
                      frac=aw["private_bytes"] / us / 1e3 / HBM_PEAK_GBS)

@@ -172,14 +172,82 @@ template <typename T, int NT> struct TileLoader {
   }
 };
 
+// ------------------------------------------------------------ bf16 LDS ring
+//
+// The bf16 shared-prefix kernel streams K and V tiles (64 keys x 128 bytes
+// each) through an LDS ring filled by direct global -> LDS copies, several
+// tiles ahead of the MFMAs.  K keeps the swizzle of Tile<bf16>.  V is stored
+// untransposed, [key][dims], with 16-byte chunk q of key row r at chunk
+// q ^ (2 ((r >> 1) & 3)), and the V^T operand of the PV product is read with
+// ds_read_b64_tr_b16: in each group of 16 lanes, lane i receives element
+// i % 4 of the 4 elements addressed by lane 4 j + i / 4, for j = 0..3.
+// Lane s of a group addresses V[K0 + s / 4][D0 + 4 (s % 4) .. + 3], so lane i
+// gets dims D0 + i of keys K0 .. K0 + 3: one half of an MFMA operand.  The 16
+// lanes then touch 4 key rows x 32 bytes, which the swizzle spreads over
+// distinct banks.
+
+
+__device__ __forceinline__ int vchunk(int key, int q) { return q ^ (2 * ((key >> 1) & 3)); }
+
+// The transpose read is issued as inline assembly: the compiler's own
+// ds_read_tr builtin makes it wait for every in-flight global -> LDS copy
+// (vmcnt(0)) before the read, which would drain the ring.  The caller waits
+// for the results with lds_wait_tr (lgkmcnt(0), tied to the result registers).
+typedef unsigned int u32x2t __attribute__((ext_vector_type(2)));
+template <int OFF>
+__device__ __forceinline__ u32x2t ds_read_tr16(const unsigned char *p) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset field");
+  u32x2t v;
+  const unsigned addr = (unsigned)(uintptr_t)(const __attribute__((address_space(3))) unsigned char *)p;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(OFF) : "memory");
+  return v;
+}
+
+// The 16 transpose reads of one V tile for a lane, [b][st][hh], from the
+// lane's two block bases (vt + voff[b]).
+template <int I>
+__device__ __forceinline__ void ds_read_tr16_tile(u32x2t (&vr)[16], const unsigned char *vb0, const unsigned char *vb1) {
+  if constexpr (I < 16) {
+    constexpr int b = I / 8, st = (I / 2) % 4, hh = I % 2;
+    constexpr int off = 128 * (32 * (st >> 1) + 16 * (st & 1) + 8 * hh);
+    vr[I] = ds_read_tr16<off>(b == 0 ? vb0 : vb1);
+    ds_read_tr16_tile<I + 1>(vr, vb0, vb1);
+  }
+}
+__device__ __forceinline__ void lds_wait_tr(u32x2t (&v)[16]) {
+  asm volatile("s_waitcnt lgkmcnt(0)"
+               : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]),
+                 "+v"(v[7]), "+v"(v[8]), "+v"(v[9]), "+v"(v[10]), "+v"(v[11]), "+v"(v[12]), "+v"(v[13]),
+                 "+v"(v[14]), "+v"(v[15])
+               :
+               : "memory");
+}
+
+// 16 bytes per lane, global -> LDS: lane i writes lds_base + 16 i (the LDS
+// address must be wave-uniform).
+__device__ __forceinline__ void dma16(const void *src, void *lds_base) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)lds_base, 16, 0, 0);
+}
+
+// s_waitcnt vmcnt(n) with expcnt and lgkmcnt left free.
+template <int N> __device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier of an LDS ring: completes this wave's LDS reads but not
+// its in-flight global -> LDS copies (those are waited for by count).
+__device__ __forceinline__ void ring_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // ------------------------------------------------------------ wave state
 
 // One wave: 32 query rows (lane % 32) against the keys of successive tiles.
 template <typename T> struct WaveAttn {
   Frag<T> qf[4];      // Q^T operand for the 4 contraction steps of D = 64
   f32x16 o[2];        // O^T accumulators: dims 0..31 and 32..63
+  f32x16 lsum;        // tile_ring: row sums of P on the matrix core (every register = l)
   float m;            // running max of the scaled log2 scores of this query
-  float l;            // this lane's share of the running sum
+  float l;            // this lane's share of the running sum (tile())
   int half;           // lane / 32
 
   __device__ __forceinline__ void init(const T *qrow, bool valid, int lane) {
@@ -189,7 +257,7 @@ template <typename T> struct WaveAttn {
       if (valid) ld16(qf[s], qrow + 32 * half + 8 * s);
       else zero(qf[s]);
     }
-    for (int r = 0; r < 16; ++r) { o[0][r] = 0.f; o[1][r] = 0.f; }
+    for (int r = 0; r < 16; ++r) { o[0][r] = 0.f; o[1][r] = 0.f; lsum[r] = 0.f; }
     m = -INFINITY;
     l = 0.f;
   }
@@ -263,6 +331,153 @@ template <typename T> struct WaveAttn {
         ld16(a, (const T *)(vrow + (16 * st + 8 * half) * (int)sizeof(T)));
         mma(o[b], a, pf[st]);
       }
+    }
+  }
+
+  // bf16 tile from the LDS ring: K tile kt (Tile<bf16> swizzle), V tile vt
+  // ([key][dims], vchunk swizzle).  voff: this lane's transpose-read offsets
+  // for dims blocks 0 and 1 (see vt_offsets).  Same arithmetic as tile(),
+  // except that the running max is only raised when a score exceeds it by
+  // more than 2^8 (log2 units): the probabilities then stay <= 256, and the
+  // O / l rescale is skipped for the (common) tiles that do not raise it.
+  __device__ __forceinline__ void tile_ring(const unsigned char *kt, const unsigned char *vt, const int (&voff)[2],
+                                            int key0, int limit, bool masked, float c, int lane) {
+    static_assert(sizeof(T) == 2, "bf16 only");
+    using Tl = Tile<T>;
+    const int kr = lane & 31;
+    f32x16 s[2];
+    for (int r = 0; r < 16; ++r) { s[0][r] = 0.f; s[1][r] = 0.f; }
+    Frag<T> a[2][4];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const int key = 32 * kb + kr;
+#pragma unroll
+      for (int st = 0; st < 4; ++st)
+        ld16(a[kb][st], (const T *)(kt + key * Tl::kRowBytes + 16 * Tl::kchunk(key, 4 * half + st)));
+    }
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int st = 0; st < 4; ++st) mma(s[kb], a[kb][st], qf[st]);
+    if (masked) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = key0 + 32 * kb + (r >> 2) * 8 + 4 * half + (r & 3);
+          if (key >= limit) s[kb][r] = -INFINITY;
+        }
+    }
+    float mx = s[0][0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32)) * c;
+    if (__ballot(mx > m + 8.f)) {   // wave-uniform: some query's max grew by > 2^8
+      const float m_new = fmaxf(m, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m - (m_new == -INFINITY ? 0.f : m_new));
+      m = m_new;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) { o[0][r] *= alpha; o[1][r] *= alpha; lsum[r] *= alpha; }
+    }
+    const float m_use = m == -INFINITY ? 0.f : m;
+    float p[32];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      p[r] = __builtin_amdgcn_exp2f(fmaf(s[0][r], c, -m_use));
+      p[16 + r] = __builtin_amdgcn_exp2f(fmaf(s[1][r], c, -m_use));
+    }
+    Frag<T> pf[4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) from_f32(pf[st], p + 8 * st);
+    // row sums of the (bf16) probabilities on the matrix core: an all-ones
+    // A operand makes every output row of lsum the sum over the tile's keys
+    Frag<T> ones;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ones.v[e] = (__bf16)1.f;
+#pragma unroll
+    for (int st = 0; st < 4; ++st) mma(lsum, ones, pf[st]);
+    // PV step st, lane half h, element e contracts key
+    // 32 (st / 2) + 16 (st % 2) + 8 (e / 4) + 4 h + e % 4 (the S^T register
+    // order of p); dims block b: lane group g = lane / 16 covers dims
+    // 32 b + 16 (g % 2) + (lane % 16).
+    u32x2t vr[16];   // [b][st][hh]
+    ds_read_tr16_tile<0>(vr, vt + voff[0], vt + voff[1]);
+    lds_wait_tr(vr);
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int st = 0; st < 4; ++st) {
+        Frag<T> va;
+        va.v = __builtin_bit_cast(bf16x8, u32x4{vr[(b * 4 + st) * 2][0], vr[(b * 4 + st) * 2][1],
+                                                vr[(b * 4 + st) * 2 + 1][0], vr[(b * 4 + st) * 2 + 1][1]});
+        mma(o[b], va, pf[st]);
+      }
+  }
+
+  // Transpose-read offsets (bytes, within a V tile) of this lane for dims
+  // blocks 0 and 1 at key offset 0: the lane addresses key 4 h + (lane % 16) / 4
+  // and dims 32 b + 16 ((lane / 16) % 2) + 4 (lane % 4).  Adding 8, 16 or 32
+  // keys leaves the vchunk swizzle unchanged, so the 8 reads of a block are
+  // constant offsets from these.
+  __device__ static __forceinline__ void vt_offsets(int lane, int (&voff)[2]) {
+    const int grp = lane >> 4, s16 = lane & 15, key = 4 * (lane >> 5) + (s16 >> 2);
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int dim = 32 * b + 16 * (grp & 1) + 4 * (s16 & 3);
+      voff[b] = key * 128 + 16 * vchunk(key, dim >> 3) + 2 * (dim & 7);
+    }
+  }
+
+  // Folds the state of another wave that saw other keys of the same rows
+  // (same lane order) into this one.
+  __device__ __forceinline__ void combine(float m2, float l2, const f32x16 (&o2)[2]) {
+    const float m_new = fmaxf(m, m2);
+    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    const float a1 = __builtin_amdgcn_exp2f(m - m_use), a2 = __builtin_amdgcn_exp2f(m2 - m_use);
+    m = m_new;
+    l = l * a1 + l2 * a2;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      o[0][r] = o[0][r] * a1 + o2[0][r] * a2;
+      o[1][r] = o[1][r] * a1 + o2[1][r] * a2;
+    }
+  }
+
+  // Normalises the wave's 32 partial rows and writes them as fp16 (bf16
+  // path): the O^T registers go to this wave's 4 KB of LDS as [32 rows][64
+  // dims] (16-byte chunk q of row r at q ^ (r & 7)), and are stored back 8
+  // whole 128-byte rows per instruction.  prow_of(r) gives the partial row of
+  // the wave's row r (lane % 32 order), or -1 for a row without a query.
+  // l_total: l already holds the query's whole sum (tile_ring), rather than
+  // this lane's share of it (tile()).
+  template <typename RowFn>
+  __device__ __forceinline__ void write_f16(unsigned char *scratch, _Float16 *part_o, float *part_lse,
+                                            RowFn prow_of, int lane, bool l_total) {
+    typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+    const float l_other = __shfl_xor(l, 32);
+    const float l_tot = l_total ? l : l + l_other;
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const int qr = lane & 31;
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        f16x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = (_Float16)(o[b][4 * j + e] * inv);
+        *(f16x4 *)(scratch + qr * 128 + 16 * ((4 * b + j) ^ (qr & 7)) + 8 * half) = v;
+      }
+    const int64_t pr_self = prow_of(qr);   // every lane calls prow_of (it may use cross-lane reads)
+    if (half == 0 && pr_self >= 0) part_lse[pr_self] = l_tot > 0.f ? m + __builtin_amdgcn_logf(l_tot) : -INFINITY;
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wave's LDS writes precede its reads
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int row = 8 * k + (lane >> 3), c = lane & 7;
+      const u32x4 v = *(const u32x4 *)(scratch + row * 128 + 16 * (c ^ (row & 7)));
+      const int64_t pr = prow_of(row);
+      if (pr >= 0) *(u32x4 *)(part_o + pr * D + 8 * c) = v;
     }
   }
 
@@ -355,21 +570,152 @@ __global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
   if (wave_active) w.write(a.dev.part_o, a.dev.part_lse, prow, valid);
 }
 
+// bf16 shared-prefix kernel: same items and arithmetic as shared_prefix_kernel,
+// on 8 waves: waves w and w + 4 own the same 32 rows and take the even and
+// odd key tiles of the item, so two waves share each SIMD (one's MFMAs
+// overlap the other's softmax); their states are combined through LDS at the
+// end.  K and V stream through an LDS ring of kPairRing tile pairs filled by
+// direct global -> LDS copies, two pairs ahead.  Each tile is 16 copy
+// instructions of 8 key rows x 128 bytes (4 per wave and pair).  Key rows past
+// the item's range are clamped to its last key (their scores are masked; a
+// pair's missing odd tile is loaded clamped and not used), which keeps every
+// wave's copy count the same.
+constexpr int kPairRing = 3;
+
+template <typename T, bool WAVE_LOCAL>
+__device__ __forceinline__ void private_item(const AttnArgs &a, int item, int lane, unsigned char *lds);
+
+constexpr int kPrivPerWG = 8;   // private items per workgroup of the bf16 attention kernel
+
+__global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
+  using T = __bf16;
+  using Tl = Tile<T>;
+  constexpr int S = kPairRing, kTileBytes = 64 * 128, kTile = 2 * kTileBytes, kPair = 2 * kTile;
+  constexpr int kRingBytes = S * kPair, kPrivBytes = kPrivPerWG * Tl::kBytes;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[kRingBytes > kPrivBytes ? kRingBytes : kPrivBytes];
+
+  const int per_xcd = gridDim.x / 8;
+  const int item = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (item >= a.n_shared) {
+    // workgroups past the shared items run the private items, one per wave
+    const int wave = threadIdx.x >> 6, pi = (item - a.n_shared) * kPrivPerWG + wave;
+    if (pi < a.n_private) private_item<T, true>(a, pi, threadIdx.x & 63, lds + wave * Tl::kBytes);
+    return;
+  }
+  const int32_t *it = a.dev.shared_items + (int64_t)item * SI_NFIELDS;
+  const int g = it[SI_KVH], row0 = it[SI_ROW0], nrows = it[SI_NROWS];
+  const int key0 = it[SI_KEY0], key1 = it[SI_KEY1], slot = it[SI_SLOT], flags = it[SI_FLAGS];
+  const int prefix_row = it[SI_PREFIX_ROW], page_q_row = it[SI_PAGE_Q_ROW];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int rw = wave & 3, par = wave >> 2;             // row group, key-tile parity
+  const int rloc = rw * 32 + (lane & 31);
+  const bool valid = rloc < nrows;
+  const int R = row0 + rloc;                           // stacked row of (page, g)
+  const int t = page_q_row + (valid ? R / a.G : 0);
+  const int hq = g * a.G + (valid ? R % a.G : 0);
+  int limit = key1;
+  if ((flags & SI_FLAG_FORK) && valid) limit = min(limit, a.dev.token_fork[t]);
+  const bool wave_active = rw * 32 < nrows;
+  const int wmin = wave_min(valid ? limit : key1);
+
+  const int64_t stride = (int64_t)a.Hkv * D;
+  const T *kbase = (const T *)a.shared_k + ((int64_t)prefix_row * a.Hkv + g) * D;
+  const T *vbase = (const T *)a.shared_v + ((int64_t)prefix_row * a.Hkv + g) * D;
+  int voff[2];
+  WaveAttn<T>::vt_offsets(lane, voff);
+
+  // copy instructions of this wave for a pair: its parity's tile, K and V
+  // rows 16 rw + lane / 8 and 16 rw + 8 + lane / 8, physical chunk lane % 8
+  const int crow = 16 * rw + (lane >> 3), pch = lane & 7;
+  const int kq0 = Tl::kchunk(crow, pch), kq1 = Tl::kchunk(crow + 8, pch);
+  const int vq0 = vchunk(crow, pch), vq1 = vchunk(crow + 8, pch);
+  const int ntiles = (key1 - key0 + 63) / 64, npairs = (ntiles + 1) / 2;
+  auto issue = [&](int j) {
+    unsigned char *st = lds + (j % S) * kPair + par * kTile;
+    const int k0 = key0 + 64 * (2 * j + par);
+    const int64_t r0 = min(k0 + crow, key1 - 1), r1 = min(k0 + crow + 8, key1 - 1);
+    dma16(kbase + r0 * stride + 8 * kq0, st + 1024 * (2 * rw));
+    dma16(kbase + r1 * stride + 8 * kq1, st + 1024 * (2 * rw + 1));
+    dma16(vbase + r0 * stride + 8 * vq0, st + kTileBytes + 1024 * (2 * rw));
+    dma16(vbase + r1 * stride + 8 * vq1, st + kTileBytes + 1024 * (2 * rw + 1));
+  };
+  static_assert(kPairRing == 3, "the waits below assume two pairs in flight");
+  // Pair 0, then this lane's Q fragments and partial-row index, then pair 1.
+  // Pair 0 and the loads behind it are retired here (pair 1 stays in
+  // flight), so the loop never waits for the Q loads.
+  if (npairs > 0) issue(0);
+  WaveAttn<T> w;
+  w.init((const T *)a.q + ((int64_t)t * a.Hq + hq) * D, valid, lane);
+  const int my_slots = valid ? a.dev.token_slots[2 * t] : 0;
+  if (npairs > 1) {
+    issue(1);
+    wait_vm<4>();
+  } else {
+    wait_vm<0>();
+  }
+  const int my_prow = valid ? (my_slots + slot) * a.Hq + hq : -1;
+  for (int j = 0; j < npairs; ++j) {
+    if (j > 0) {
+      if (j + 1 < npairs) wait_vm<4>();
+      else wait_vm<0>();
+    }
+    ring_barrier();   // pair j visible to every wave; the slot of pair j - 1 is free
+    if (j + 2 < npairs) issue(j + 2);
+    const int ti = 2 * j + par;
+    if (wave_active && ti < ntiles) {
+      const int k0 = key0 + 64 * ti;
+      const unsigned char *st = lds + (j % S) * kPair + par * kTile;
+      w.tile_ring(st, st + kTileBytes, voff, k0, limit, k0 + 64 > wmin, a.c, lane);
+    }
+  }
+  ring_barrier();   // every wave is done with the ring; its LDS becomes scratch
+  w.l = w.lsum[0];  // the query's whole sum (see tile_ring)
+  // odd-tile waves hand (m, l, O) to their even-tile partners
+  float *xch = (float *)lds + rw * (34 * 64);
+  if (par == 1 && wave_active) {
+    xch[lane] = w.m;
+    xch[64 + lane] = w.l;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      xch[(2 + r) * 64 + lane] = w.o[0][r];
+      xch[(18 + r) * 64 + lane] = w.o[1][r];
+    }
+  }
+  __syncthreads();
+  if (par == 1 || !wave_active) return;
+  {
+    f32x16 o2[2];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      o2[0][r] = xch[(2 + r) * 64 + lane];
+      o2[1][r] = xch[(18 + r) * 64 + lane];
+    }
+    w.combine(xch[lane], xch[64 + lane], o2);
+  }
+  auto prow_of = [&](int r) -> int64_t { return __shfl(my_prow, r); };
+  w.write_f16(lds + 4 * 34 * 64 * 4 + rw * 4096, (_Float16 *)a.dev.part_o, a.dev.part_lse, prow_of, lane, true);
+}
+
 // ------------------------------------------------------------ private kernel
 
-template <typename T>
-__global__ __launch_bounds__(64) void private_kernel(AttnArgs a) {
+// One private work item on one wave: the wave's own LDS tile `lds`
+// (Tile<T>::kBytes).  WAVE_LOCAL: the workgroup's other waves run other items,
+// so the tile hand-overs only need this wave's LDS operations to have
+// completed (they execute in order); otherwise the workgroup is this one wave
+// and a workgroup barrier is used.
+template <typename T, bool WAVE_LOCAL>
+__device__ __forceinline__ void private_item(const AttnArgs &a, int item, int lane, unsigned char *lds) {
   constexpr int NT = 64;
-  using Tl = Tile<T>;
-  __shared__ __attribute__((aligned(16))) unsigned char lds[Tl::kBytes];
-  const int item = blockIdx.x;
-  if (item >= a.n_private) return;
+  auto sync = [] {
+    if constexpr (WAVE_LOCAL) asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    else __syncthreads();
+  };
   const int32_t *it = a.dev.private_items + (int64_t)item * PI_NFIELDS;
   const int g = it[PI_KVH], row0 = it[PI_ROW0], nrows = it[PI_NROWS];
   const int key0 = it[PI_KEY0], key1 = it[PI_KEY1], slot = it[PI_SLOT], past = it[PI_PAST];
   const int priv_row = it[PI_PRIV_ROW], q_row = it[PI_Q_ROW];
 
-  const int lane = threadIdx.x;
   const int rloc = lane & 31;
   const bool valid = rloc < nrows;
   const int R = row0 + rloc;                            // stacked row of (branch, g)
@@ -389,20 +735,37 @@ __global__ __launch_bounds__(64) void private_kernel(AttnArgs a) {
   for (int k0 = key0; k0 < key1; k0 += 64) {
     ld.load(kbase + (int64_t)k0 * stride, stride, key1 - k0, lane);
     ld.load_v(vbase + (int64_t)k0 * stride, stride, key1 - k0, lane);
-    __syncthreads();   // previous tile fully consumed
+    sync();   // previous tile fully consumed
     ld.store(lds, lane);
-    __syncthreads();
+    sync();
     w.tile(lds, k0, limit, k0 + 64 > wmin, a.c, lane);
   }
-  const int64_t prow = valid ? ((int64_t)a.dev.token_slots[2 * t] + slot) * a.Hq + hq : 0;
-  w.write(a.dev.part_o, a.dev.part_lse, prow, valid);
+  if constexpr (sizeof(T) == 2) {
+    sync();   // the tile is consumed; its LDS becomes write scratch
+    auto prow_of = [&](int r) -> int64_t {
+      if (r >= nrows) return -1;
+      const int Rr = row0 + r, tr = q_row + Rr / a.G;
+      return ((int64_t)a.dev.token_slots[2 * tr] + slot) * a.Hq + g * a.G + Rr % a.G;
+    };
+    w.write_f16(lds, (_Float16 *)a.dev.part_o, a.dev.part_lse, prow_of, lane, false);
+  } else {
+    const int64_t prow = valid ? ((int64_t)a.dev.token_slots[2 * t] + slot) * a.Hq + hq : 0;
+    w.write(a.dev.part_o, a.dev.part_lse, prow, valid);
+  }
+}
+
+// fp32 private kernel: one wave per item.
+__global__ __launch_bounds__(64) void private_kernel_f32(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) unsigned char lds[Tile<float>::kBytes];
+  if ((int)blockIdx.x >= a.n_private) return;
+  private_item<float, false>(a, blockIdx.x, threadIdx.x, lds);
 }
 
 // ------------------------------------------------------------ merge kernel
 
 // 16 threads per (token, head) row, 4 dims each.  Partial lse values are in
 // log2 units; the exported lse is natural-log.
-template <typename TO>
+template <typename TO, typename TP>
 __global__ __launch_bounds__(256) void merge_kernel(PlanDev dev, TO *out, float *lse, int T, int Hq) {
   const int row = blockIdx.x * 16 + (threadIdx.x >> 4);
   if (row >= T * Hq) return;
@@ -410,7 +773,7 @@ __global__ __launch_bounds__(256) void merge_kernel(PlanDev dev, TO *out, float 
   const int t = row / Hq, h = row % Hq;
   const int first = dev.token_slots[2 * t], cnt = dev.token_slots[2 * t + 1];
   const float *lse_p = dev.part_lse + (int64_t)first * Hq + h;
-  const float *o_p = dev.part_o + ((int64_t)first * Hq + h) * D + 4 * sub;
+  const TP *o_p = (const TP *)dev.part_o + ((int64_t)first * Hq + h) * D + 4 * sub;
   // batches of 8 partials: every load of a batch is issued before it is used
   float mx = -INFINITY;
   for (int i0 = 0; i0 < cnt; i0 += 8) {
@@ -430,7 +793,13 @@ __global__ __launch_bounds__(256) void merge_kernel(PlanDev dev, TO *out, float 
     for (int i = 0; i < 8; ++i) {
       const int64_t j = min(i0 + i, cnt - 1);
       l8[i] = lse_p[j * Hq];
-      o8[i] = *(const f32x4 *)(o_p + j * Hq * D);
+      if constexpr (sizeof(TP) == 2) {
+        typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+        const f16x4 h4 = *(const f16x4 *)(o_p + j * Hq * D);
+        o8[i] = f32x4{(float)h4[0], (float)h4[1], (float)h4[2], (float)h4[3]};
+      } else {
+        o8[i] = *(const f32x4 *)(o_p + j * Hq * D);
+      }
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -483,28 +852,45 @@ hipError_t launch_branch_attention(const Plan &P, const void *q, const void *sha
   a.G = P.G;
   a.c = P.scale * kLog2e;
   const bool bf16 = P.attn.dtype == HPD_BF16;
-  if (a.n_shared > 0) {
-    const int grid = (a.n_shared + 7) / 8 * 8;
-    timed_begin(KK_SHARED, stream);
-    if (bf16) hipLaunchKernelGGL(shared_prefix_kernel<__bf16>, dim3(grid), dim3(256), 0, stream, a);
-    else hipLaunchKernelGGL(shared_prefix_kernel<float>, dim3(grid), dim3(256), 0, stream, a);
-    timed_end(stream);
-  }
-  if (a.n_private > 0) {
-    timed_begin(KK_PRIVATE, stream);
-    if (bf16) hipLaunchKernelGGL(private_kernel<__bf16>, dim3(a.n_private), dim3(64), 0, stream, a);
-    else hipLaunchKernelGGL(private_kernel<float>, dim3(a.n_private), dim3(64), 0, stream, a);
-    timed_end(stream);
+  if (bf16) {
+    // one launch: shared-prefix items, then the private items 8 per workgroup
+    const int nwg = a.n_shared + (a.n_private + kPrivPerWG - 1) / kPrivPerWG;
+    if (nwg > 0) {
+      timed_begin(KK_SHARED, stream);
+      hipLaunchKernelGGL(shared_prefix_ring_kernel, dim3((nwg + 7) / 8 * 8), dim3(512), 0, stream, a);
+      timed_end(stream);
+    }
+  } else {
+    if (a.n_shared > 0) {
+      timed_begin(KK_SHARED, stream);
+      hipLaunchKernelGGL(shared_prefix_kernel<float>, dim3((a.n_shared + 7) / 8 * 8), dim3(256), 0, stream, a);
+      timed_end(stream);
+    }
+    if (a.n_private > 0) {
+      timed_begin(KK_PRIVATE, stream);
+      hipLaunchKernelGGL(private_kernel_f32, dim3(a.n_private), dim3(64), 0, stream, a);
+      timed_end(stream);
+    }
   }
   const int rows = P.T * P.attn.num_q_heads;
   const int mgrid = (rows + 15) / 16;
   timed_begin(KK_MERGE, stream);
-  if (P.attn.out_dtype == HPD_BF16)
-    hipLaunchKernelGGL(merge_kernel<__bf16>, dim3(mgrid), dim3(256), 0, stream, a.dev, (__bf16 *)out, lse,
-                       P.T, P.attn.num_q_heads);
-  else
-    hipLaunchKernelGGL(merge_kernel<float>, dim3(mgrid), dim3(256), 0, stream, a.dev, (float *)out, lse,
-                       P.T, P.attn.num_q_heads);
+  // bf16 inputs: fp16 partials; fp32 inputs: fp32 partials
+  if (P.attn.out_dtype == HPD_BF16) {
+    if (bf16)
+      hipLaunchKernelGGL((merge_kernel<__bf16, _Float16>), dim3(mgrid), dim3(256), 0, stream, a.dev, (__bf16 *)out,
+                         lse, P.T, P.attn.num_q_heads);
+    else
+      hipLaunchKernelGGL((merge_kernel<__bf16, float>), dim3(mgrid), dim3(256), 0, stream, a.dev, (__bf16 *)out,
+                         lse, P.T, P.attn.num_q_heads);
+  } else {
+    if (bf16)
+      hipLaunchKernelGGL((merge_kernel<float, _Float16>), dim3(mgrid), dim3(256), 0, stream, a.dev, (float *)out,
+                         lse, P.T, P.attn.num_q_heads);
+    else
+      hipLaunchKernelGGL((merge_kernel<float, float>), dim3(mgrid), dim3(256), 0, stream, a.dev, (float *)out, lse,
+                         P.T, P.attn.num_q_heads);
+  }
   timed_end(stream);
   return hipGetLastError();
 }

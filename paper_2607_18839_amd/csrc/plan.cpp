@@ -144,9 +144,24 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
     }
 
   // ---- partial slots per token
+  // Prefix keys per shared work item: a multiple of kSharedSplitUnit, sized so
+  // that the shared-prefix work is about one workgroup per CU
+  // (kSharedTargetItems); longer items amortise each workgroup's fixed
+  // start-up and write-out, and fewer splits mean fewer partials to merge.
+  auto shared_items_for = [&](int64_t split) {
+    int64_t n = 0;
+    for (int p = 0; p < np; ++p)
+      n += (int64_t)Hkv * ceil_div((int64_t)P.page_T[p] * G, (int64_t)kSharedWaves * kTileRows) *
+           ceil_div(P.prefix_len[p], split);
+    return n;
+  };
+  int64_t units = shared_items_for(kSharedSplitUnit);
+  int64_t mult = std::max<int64_t>(1, ceil_div(units, kSharedTargetItems));
+  while (shared_items_for(kSharedSplitUnit * mult) > kSharedTargetItems) ++mult;   // ceilings per page
+  P.split_keys = (int32_t)std::min<int64_t>(kSharedSplitUnit * mult, INT32_MAX / 2);
   std::vector<int32_t> page_splits(np);
   for (int p = 0; p < np; ++p)
-    page_splits[p] = (int32_t)ceil_div(P.prefix_len[p], kSharedSplitKeys);
+    page_splits[p] = (int32_t)ceil_div(P.prefix_len[p], P.split_keys);
   P.token_slots.resize(2 * (size_t)P.T);
   int64_t slot = 0;
   for (int i = 0; i < nb; ++i) {
@@ -173,7 +188,7 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
       for (int s = 0; s < page_splits[p]; ++s)
         for (int r0 = 0; r0 < R; r0 += group_rows) {
           const int nr = std::min(group_rows, R - r0);
-          const int k0 = s * kSharedSplitKeys, k1 = std::min(Pp, k0 + kSharedSplitKeys);
+          const int k0 = s * P.split_keys, k1 = std::min(Pp, k0 + P.split_keys);
           int flags = 0;
           if (P.has_fork)
             for (int r = r0; r < r0 + nr; ++r)

@@ -32,7 +32,8 @@ enum PrivateItemField {
 constexpr int kSharedWaves = 4;      // waves per shared-prefix workgroup
 constexpr int kTileRows = 32;        // stacked query rows per wave (MFMA 32x32)
 constexpr int kKeyTile = 64;         // keys per LDS tile
-constexpr int kSharedSplitKeys = 256;   // prefix keys per shared work item
+constexpr int kSharedSplitUnit = 128;   // shared work items cover multiples of this many prefix keys
+constexpr int kSharedTargetItems = 256; // aim: about one shared-prefix workgroup per CU
 constexpr int kPrivateChunkKeys = 128;  // private keys per private work item
 constexpr int SI_FLAG_FORK = 1;      // rows have their own fork limits
 constexpr int kNumCounters = 8192;   // self-resetting arrival counters (split-K / merges)
@@ -54,6 +55,7 @@ struct Plan {
   std::vector<int32_t> token_fork;                    // [T] visible prefix per token
   std::vector<int32_t> token_dest;                    // [T] private row of token t: priv_row + L + j
   int64_t num_slots = 0;                              // partial rows = num_slots * Hq
+  int32_t split_keys = 0;                             // prefix keys per shared work item
 
   // device workspace layout (byte offsets, 256-aligned)
   size_t off_shared_items = 0, off_private_items = 0, off_token_slots = 0,
