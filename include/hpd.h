@@ -179,8 +179,8 @@ typedef struct {
 } hpd_model_desc;
 
 /* Bytes of device workspace hpd_decode_step needs on top of
- * hpd_plan_workspace_bytes (activations of the T tokens and split-K
- * partials of the projections). */
+ * hpd_plan_workspace_bytes (activations of the T tokens and per-token
+ * sums of squares for the folded RMSNorm). */
 size_t hpd_decode_workspace_bytes(const hpd_model_desc *model, const hpd_plan *plan);
 
 /* One full decode step of the decoder stack for every new token of every
@@ -228,7 +228,9 @@ typedef struct {
 hpd_status hpd_kernel_timing(int enable, int max_launches);
 hpd_status hpd_kernel_times_read(hpd_kernel_times *out, int keep_pairs);
 /* Kind k: 0 shared_prefix, 1 private, 2 merge, 3 gemm_qkv, 4 gemm_o,
- * 5 gemm_gate_up, 6 gemm_down, 7 residual_norm. */
+ * 5 gemm_gate_up, 6 gemm_down, 7 norm_input.  With bf16 inputs kind 0 is
+ * one launch that runs the shared-prefix and the private work items (kind 1
+ * is then never launched). */
 const char *hpd_kernel_kind_name(int kind);
 
 const char *hpd_status_string(hpd_status status);

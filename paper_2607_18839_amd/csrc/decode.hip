@@ -1,22 +1,26 @@
 // One branch-parallel decode step of the decoder stack (C ABI entry points).
 //
 // The step runs every new token of every branch through all layers at once
-// (Algorithm 1, the parallel draft over the active pool).  Per layer, with
-// the residual stream h [T][hidden] kept in fp32 in hidden_out:
-//   1 [h += previous down projection] RMSNorm(h) -> x (bf16)
-//   2 QKV GEMM -> q (bf16) and the new K/V rows (bf16), written into the
+// (Algorithm 1, the parallel draft over the active pool).  The residual
+// stream h [T][hidden] stays in fp32 in hidden_out.  RMSNorm is folded into
+// the projections (see gemm.h): a norm's input x = h * gamma is written by
+// whatever last updated h, with per-token sums of squares, and the next
+// projection scales its outputs by the per-token factor.  Per step:
+//   0 h = hidden_in; x = h * gamma_attn[0] (bf16), sums of squares
+// and per layer:
+//   1 QKV GEMM -> q (bf16) and the new K/V rows (bf16), written into the
 //     layer's private cache at row priv_row + L + j
-//   3 branch attention (shared-prefix, private, merge kernels) -> a (bf16)
-//   4 O GEMM (split-K partials)
-//   5 h += a W_o^T, RMSNorm(h) -> x (fp16) (one kernel)
-//   6 gate/up GEMM (fp16), SwiGLU -> m (fp16)
-//   7 down GEMM (fp16, partials), added to h by the next layer's step 1 (or
-//     by a final residual kernel after the last layer)
+//   2 branch attention (one launch for the shared-prefix and private work
+//     items, then the merge) -> a (bf16)
+//   3 O GEMM: h += a W_o^T; x = h * gamma_mlp (fp16), sums of squares
+//   4 gate/up GEMM (fp16), SwiGLU -> m (fp16)
+//   5 down GEMM (fp16): h += m W_down^T; x = h * gamma_attn[l + 1] (bf16),
+//     sums of squares (not after the last layer)
 // (section "Overview", paragraph "LLM Decoder": GQA, RMSNorm, SwiGLU).
-// Split-K partials are summed by the consuming kernel in split order, so the
-// result does not depend on scheduling and needs no cross-workgroup sync.
-// Buffers: x, q, attn, m and the partials live in the workspace after the
-// attention plan's tables; rows T..Tpad-1 of x, attn and m are kept zero.
+// Every output element is written by one workgroup, so the result does not
+// depend on scheduling.  Buffers x, q, attn, m and the sums of squares live
+// in the workspace after the attention plan's tables; rows T..Tpad-1 of x,
+// attn and m are kept zero.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -37,8 +41,8 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct DecodeLayout {
   int T, Tpad, H, I, nq, nkv;
-  GemmShape qkv, o, gu, down;
-  size_t off_x, off_q, off_attn, off_m, off_part, bytes;
+  int rg_qkv, rg_o, rg_gu, rg_down;
+  size_t off_x, off_q, off_attn, off_m, off_ss, bytes;
 };
 
 DecodeLayout decode_layout(const hpd_model_desc &m, const Plan &P) {
@@ -49,10 +53,10 @@ DecodeLayout decode_layout(const hpd_model_desc &m, const Plan &P) {
   L.I = m.intermediate;
   L.nq = P.attn.num_q_heads * HPD_HEAD_DIM;
   L.nkv = P.attn.num_kv_heads * HPD_HEAD_DIM;
-  L.qkv = choose_gemm_shape(L.nq + 2 * L.nkv, L.H, L.Tpad, kEpiQKV);
-  L.o = choose_gemm_shape(L.H, L.nq, L.Tpad, kEpiResidual);
-  L.gu = choose_gemm_shape(2 * L.I, L.H, L.Tpad, kEpiSwiGLU);
-  L.down = choose_gemm_shape(L.H, L.I, L.Tpad, kEpiResidual);
+  L.rg_qkv = choose_gemm_rg(L.nq + 2 * L.nkv, L.H, L.Tpad);
+  L.rg_o = choose_gemm_rg(L.H, L.nq, L.Tpad);
+  L.rg_gu = choose_gemm_rg(2 * L.I, L.H, L.Tpad);
+  L.rg_down = choose_gemm_rg(L.H, L.I, L.Tpad);
   size_t off = align256(P.workspace_bytes);
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -63,9 +67,7 @@ DecodeLayout decode_layout(const hpd_model_desc &m, const Plan &P) {
   L.off_q = take((size_t)L.T * L.nq * 2);
   L.off_attn = take((size_t)L.Tpad * L.nq * 2);
   L.off_m = take((size_t)L.Tpad * L.I * 2);
-  // partials of the residual projections (O, down); N = hidden for both
-  const size_t part = (size_t)std::max(L.o.ksplit, L.down.ksplit) * L.Tpad * L.H * sizeof(float);
-  L.off_part = take(part);
+  L.off_ss = take((size_t)L.Tpad * (L.H / kGemmTile) * sizeof(float));
   L.bytes = off;
   return L;
 }
@@ -144,42 +146,35 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
   }
   hipStream_t stream = (hipStream_t)stream_;
   unsigned char *ws = (unsigned char *)workspace;
-  __bf16 *x = (__bf16 *)(ws + L.off_x);   // bf16 (attention input) or fp16 (MLP input)
+  __bf16 *x = (__bf16 *)(ws + L.off_x);   // x = h * gamma: bf16 (attention input) or fp16 (MLP input)
   __bf16 *q = (__bf16 *)(ws + L.off_q), *attn = (__bf16 *)(ws + L.off_attn);
   __bf16 *mlp = (__bf16 *)(ws + L.off_m);   // SwiGLU product, fp16 bits
-  float *part = (float *)(ws + L.off_part);
+  float *ss = (float *)(ws + L.off_ss);     // sums of squares of h per 32 columns
   const hpd::PlanDev dev = hpd::plan_dev(P, workspace);
-
-  hipError_t e = hipSuccess;
-  if (hidden_out != hidden_in)
-    e = hipMemcpyAsync(hidden_out, hidden_in, (size_t)L.T * L.H * sizeof(float), hipMemcpyDeviceToDevice,
-                       stream);
   float *h = hidden_out;
-  auto base = [&](const hpd::GemmShape &s, const __bf16 *xh, int N, int K) {
+  auto gamma = [&](const void *const *arr, int l) { return arr ? (const __bf16 *)arr[l] : nullptr; };
+  auto base = [&](int rg, const __bf16 *xin, int N, int K) {
     hpd::GemmArgs g{};
     g.K = K;
     g.N = N;
-    g.rg = s.rg;
-    g.n_slices = N / (hpd::kGemmTile * s.rg);
-    g.ksplit = s.ksplit;
-    g.k_per_wg = K / s.ksplit;
+    g.rg = rg;
+    g.n_slices = N / (hpd::kGemmTile * rg);
     g.n_ttiles = L.Tpad / hpd::kGemmTile;
-    g.x = xh;
+    g.x = xin;
     g.T = L.T;
     g.Tpad = L.Tpad;
-    g.part = part;
+    g.ss_in = ss;
+    g.n_ss = L.H / hpd::kGemmTile;
+    g.inv_H = 1.0f / (float)L.H;
+    g.eps = m.rms_eps;
     return g;
   };
-  int pending_ksplit = 0;   // down-projection partials not yet added to h
+
+  hipError_t e = hpd::launch_norm_input(hidden_in, h, L.T, L.Tpad, L.H, gamma(m.g_attn_norm, 0), x, ss, attn,
+                                         L.nq, stream);
   for (int l = 0; l < m.num_layers && e == hipSuccess; ++l) {
-    const __bf16 *g1 = m.g_attn_norm ? (const __bf16 *)m.g_attn_norm[l] : nullptr;
-    const __bf16 *g2 = m.g_mlp_norm ? (const __bf16 *)m.g_mlp_norm[l] : nullptr;
-    // 1: previous layer's down projection into h, attention-input norm (bf16)
-    e = hpd::launch_residual_norm(h, pending_ksplit ? part : nullptr, pending_ksplit, L.Tpad, L.H, L.T, g1,
-                                  m.rms_eps, x, false, attn, L.nq, stream);
-    if (e != hipSuccess) break;
-    // 2: QKV projection; the epilogue appends the new K/V rows to the cache
-    hpd::GemmArgs g = base(L.qkv, x, L.nq + 2 * L.nkv, L.H);
+    // 1: QKV projection; the epilogue appends the new K/V rows to the cache
+    hpd::GemmArgs g = base(L.rg_qkv, x, L.nq + 2 * L.nkv, L.H);
     g.w0 = (const __bf16 *)m.w_qkv[l];
     g.q_out = q;
     g.n_q = L.nq;
@@ -189,35 +184,40 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
     g.dest = dev.token_dest;
     e = hpd::launch_gemm(g, false, hpd::kEpiQKV, hpd::KK_GEMM_QKV, stream);
     if (e != hipSuccess) break;
-    // 3: attention over the shared prefix and the private rows
+    // 2: attention over the shared prefix and the private rows
     e = hpd::launch_branch_attention(P, q, shared_k ? shared_k[l] : nullptr, shared_v ? shared_v[l] : nullptr,
                                      priv_k[l], priv_v[l], attn, nullptr, workspace, stream);
     if (e != hipSuccess) break;
-    // 4 + 5: O projection, residual add and MLP-input norm (fp16)
-    g = base(L.o, attn, L.H, L.nq);
+    // 3: O projection into h; MLP norm input (fp16)
+    g = base(L.rg_o, attn, L.H, L.nq);
     g.w0 = (const __bf16 *)m.w_o[l];
+    g.h = h;
+    g.x_out = x;
+    g.x_out_f16 = true;
+    g.gamma = gamma(m.g_mlp_norm, l);
+    g.ss_out = ss;
     e = hpd::launch_gemm(g, false, hpd::kEpiResidual, hpd::KK_GEMM_O, stream);
     if (e != hipSuccess) break;
-    e = hpd::launch_residual_norm(h, part, L.o.ksplit, L.Tpad, L.H, L.T, g2, m.rms_eps, x, true, nullptr, 0,
-                                  stream);
-    if (e != hipSuccess) break;
-    // 6: gate/up projection, SwiGLU (fp16)
-    g = base(L.gu, x, 2 * L.I, L.H);
+    // 4: gate/up projection, SwiGLU (fp16)
+    g = base(L.rg_gu, x, 2 * L.I, L.H);
     g.w0 = (const __bf16 *)m.w_gate[l];
     g.w1 = (const __bf16 *)m.w_up[l];
     g.m_out = mlp;
     g.I = L.I;
     e = hpd::launch_gemm(g, true, hpd::kEpiSwiGLU, hpd::KK_GEMM_GATE_UP, stream);
     if (e != hipSuccess) break;
-    // 7: down projection (fp16; added to h by the next layer's first kernel)
-    g = base(L.down, mlp, L.H, L.I);
+    // 5: down projection into h (fp16); next layer's attention norm input
+    g = base(L.rg_down, mlp, L.H, L.I);
     g.w0 = (const __bf16 *)m.w_down[l];
+    g.h = h;
+    if (l + 1 < m.num_layers) {
+      g.x_out = x;
+      g.x_out_f16 = false;
+      g.gamma = gamma(m.g_attn_norm, l + 1);
+      g.ss_out = ss;
+    }
     e = hpd::launch_gemm(g, true, hpd::kEpiResidual, hpd::KK_GEMM_DOWN, stream);
-    pending_ksplit = L.down.ksplit;
   }
-  if (e == hipSuccess)
-    e = hpd::launch_residual_norm(h, part, pending_ksplit, L.Tpad, L.H, L.T, nullptr, m.rms_eps, nullptr, false,
-                                  nullptr, 0, stream);
   if (e != hipSuccess) {
     hpd::set_last_error(std::string("hpd_decode_step: ") + hipGetErrorString(e));
     return HPD_ERR_HIP;

@@ -13,43 +13,52 @@ constexpr int kGemmTile = 32;             // weight rows and tokens of one wave'
 constexpr int kGemmKStep = 64;            // K per pipeline step (4 MFMAs of 16)
 constexpr int kEpiQKV = 0, kEpiResidual = 1, kEpiSwiGLU = 2;
 
-// One projection Y[t][n] = sum_k X[t][k] W[n][k].  A workgroup of 4 waves
-// owns the output tile of 32 rg weight rows x 32 tokens over K range
-// [ks * k_per_wg, (ks + 1) * k_per_wg): wave w takes rows 32 (w % rg) .. and
-// the K quarter/half w / rg of that range (rg * kg = 4).
+// One projection Y[t][n] = sum_k X[t][k] W[n][k] over the full K range.  A
+// workgroup of 4 waves owns the output tile of 32 rg weight rows x 32
+// tokens: wave w takes rows 32 (w % rg) .. and the K quarter / half w / rg
+// (rg * kg = 4; the K groups are added through LDS).
+//
+// RMSNorm is folded into the projections.  The residual projections (O,
+// down) add their result into the fp32 residual stream h, and write the next
+// norm's input unnormalised, x = h * gamma (bf16 or fp16), together with the
+// sums of squares of h over each 32-column tile, ss[t][tile].  The projections
+// that consume x (QKV, gate/up) scale their outputs by 1 / sqrt(sum ss / H +
+// eps) per token: RMSNorm's per-token factor commutes with the product.
 struct GemmArgs {
   const __bf16 *w0;         // W[N][K] (SwiGLU: gate rows [I][K])
   const __bf16 *w1;         // SwiGLU: up rows [I][K]; otherwise unused
   int K;
   int N;                    // output columns (SwiGLU: 2 I, gate and up)
-  int rg;                   // row groups per workgroup: 1, 2 or 4
+  int rg;                   // row groups per workgroup: 1, 2 or 4 (K % (64 * 4 / rg) == 0)
   int n_slices;             // N / (32 rg)
-  int ksplit, k_per_wg;     // K = ksplit * k_per_wg; k_per_wg % (64 * 4 / rg) == 0
   int n_ttiles;             // Tpad / 32
   const __bf16 *x;          // [Tpad][K] activations (bf16, or fp16 for the MLP), rows >= T finite
   int T, Tpad;
-  float *part;              // residual epilogue: [ksplit][Tpad][N] fp32 (rows < T written)
-  // epilogues
-  __bf16 *q_out; int n_q;                   // QKV: q[t][0..n_q)
-  __bf16 *k_cache, *v_cache; int n_kv;      // QKV: cache rows dest[t]
+  // QKV / SwiGLU: per-token norm factor from ss_in [Tpad][n_ss] (sum / H + eps)
+  const float *ss_in; int n_ss; float inv_H, eps;
+  // QKV epilogue
+  __bf16 *q_out; int n_q;                   // q[t][0..n_q)
+  __bf16 *k_cache, *v_cache; int n_kv;      // cache rows dest[t]
   const int32_t *dest;
-  __bf16 *m_out; int I;                     // SwiGLU output [Tpad][I], fp16 bits (rows >= T zero)
+  // SwiGLU epilogue
+  __bf16 *m_out; int I;                     // [Tpad][I], fp16 bits (rows >= T zero)
+  // residual epilogue (N = H): h += Y; then, if x_out: x_out = h * gamma, ss_out
+  float *h;                                 // [T][N] fp32
+  __bf16 *x_out; bool x_out_f16;            // [Tpad][N]; rows < T written
+  const __bf16 *gamma;                      // [N] bf16, NULL = ones
+  float *ss_out;                            // [Tpad][N / 32]
 };
 
-// h[t] += sum over splits of part[ks][t][:] (part may be NULL), then
-// x = RMSNorm(h) -> x_out (bf16, or fp16 if out_f16) unless x_out is NULL.
-hipError_t launch_residual_norm(float *h, const float *part, int ksplit, int Tpad, int H, int T,
-                                const __bf16 *gamma, float eps, void *x_out, bool out_f16,
-                                __bf16 *zero_rows, int zero_cols, hipStream_t stream);
+// Start of a step: h = h_in (if different), x = h * gamma, ss, and zero rows
+// T..Tpad-1 of x and of `zero_rows` ([Tpad][zero_cols]).
+hipError_t launch_norm_input(const float *h_in, float *h, int T, int Tpad, int H, const __bf16 *gamma,
+                             __bf16 *x, float *ss, __bf16 *zero_rows, int zero_cols, hipStream_t stream);
 // f16: fp16 GEMM (bf16 weights converted to fp16 in registers, fp16
-// activations); epi: kEpi*.  The QKV and SwiGLU epilogues need ksplit == 1.
+// activations); epi: kEpi*.
 hipError_t launch_gemm(const GemmArgs &g, bool f16, int epi, int kind, hipStream_t stream);
 
-// Tile choice for an N x K projection over Tpad tokens: rg, ksplit and the
-// register ring depth, from a model of the bytes each CU has to stream.
-struct GemmShape {
-  int rg, ksplit;
-};
-GemmShape choose_gemm_shape(int N, int K, int Tpad, int epi);
+// Row groups per workgroup for an N x K projection over Tpad tokens, from a
+// model of the bytes each CU has to stream.
+int choose_gemm_rg(int N, int K, int Tpad);
 
 }  // namespace hpd

@@ -15,10 +15,10 @@
 // K quarters, added through LDS at the end, in wave order), or both (rg = 2).
 // Operands stream through a 4-step LDS ring filled by direct global -> LDS
 // copies (8 rows x 128 bytes per instruction), 3 steps ahead of the MFMAs.
-// Residual projections may also split K over workgroups ("split-K"); those
-// partial tiles are added, in split order, by the residual + RMSNorm kernel,
-// so there is no cross-workgroup synchronisation and the result does not
-// depend on scheduling.  The QKV and SwiGLU epilogues run in the GEMM.
+// Every output element is produced by one workgroup over the whole of K, so
+// the epilogues can finish it: the QKV and SwiGLU epilogues apply the folded
+// RMSNorm factor and write q / the new K/V rows / m; the residual epilogue
+// adds into h and writes the next norm's input (see gemm.h).
 //
 // Precision: the QKV and O projections take bf16 activations (rounding them
 // costs ~5e-4 of absolute error on the residual stream after 18 layers).  The
@@ -105,20 +105,36 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   constexpr int kInstr = (RG + 1) * 4 / RG;   // copy instructions per wave per step
   __shared__ __attribute__((aligned(16))) unsigned char lds[S * kStageBytes];
 
-  const int nwg = g.n_slices * g.n_ttiles * g.ksplit;
+  const int nwg = g.n_slices * g.n_ttiles;
   const int per_xcd = gridDim.x / 8;
   // XCD-aware order: consecutive logical tiles share an XCD (and its L2); the
   // token tiles of one weight slice are consecutive, so the slice is fetched
   // from HBM once per XCD.
   const int logical = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
   if (logical >= nwg) return;
-  const int ks = logical % g.ksplit, rest = logical / g.ksplit;
-  const int tt = rest % g.n_ttiles, slice = rest / g.n_ttiles;
+  const int tt = logical % g.n_ttiles, slice = logical / g.n_ttiles;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int rg = wave % RG, kgi = wave / RG;
-  const int kw = g.k_per_wg / KG;   // K per wave
+  const int kw = g.K / KG;   // K per wave
   const int nsteps = kw / kGemmKStep;
-  const int64_t kbase = (int64_t)ks * g.k_per_wg + (int64_t)kgi * kw;
+  const int64_t kbase = (int64_t)kgi * kw;
+  const int frow = lane & 31, half = lane >> 5;
+  const int t = tt * kGemmTile + frow;   // this lane's token in the epilogue
+  const int tile = slice * RG + rg;      // 32-row tile of the output columns
+
+  // Epilogue operands, loaded before the main loop (no later step needs them
+  // sooner, and the loop's waits retire them): the per-token sums of squares
+  // (QKV, SwiGLU; up to 32 partials) or the residual row slice (residual).
+  f32x4 pre[8];
+  if constexpr (EPI == kEpiResidual) {
+    const float *hr = g.h + (int64_t)min(t, g.T - 1) * g.N + tile * kGemmTile + 4 * half;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pre[i] = *(const f32x4 *)(hr + 8 * i);
+  } else {
+    const float *sr = g.ss_in + (int64_t)t * g.n_ss;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) pre[i] = *(const f32x4 *)(sr + 4 * min(i, g.n_ss / 4 - 1));
+  }
 
   // copy sources: instruction q of the K group covers tile q / 4 (row group
   // q / 4 < RG, else the token tile), rows 8 (q % 4) + lane / 8
@@ -155,7 +171,6 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   f32x16 acc;
 #pragma unroll
   for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-  const int frow = lane & 31, half = lane >> 5;
   const int a_off = kgi * kGroupBytes + rg * kTileBytes + frow * 128;
   const int b_off = kgi * kGroupBytes + RG * kTileBytes + frow * 128;
 #pragma unroll
@@ -183,7 +198,6 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
                                                       __builtin_bit_cast(bf16x8, bv[j]), acc, 0, 0, 0);
     }
   }
-  const int tile = slice * RG + rg;   // 32-row tile of the output columns
 
   if constexpr (KG > 1) {
     // K groups 1.. hand their tiles to K group 0, which adds them in order
@@ -202,114 +216,123 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
       for (int r = 0; r < 16; ++r) acc[r] += red[((k * RG + rg) * 16 + r) * 64 + lane];
   }
 
-  const int t = tt * kGemmTile + frow;
   if constexpr (EPI == kEpiResidual) {
+    // h += Y; x_out = h * gamma (the next norm's input, unnormalised) and the
+    // sum of squares of h over this 32-column tile
     if (t >= g.T) return;
-    float *dst = g.part + ((int64_t)ks * g.Tpad + t) * g.N + tile * kGemmTile + 4 * half;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      *(f32x4 *)(dst + 8 * i) = f32x4{acc[4 * i], acc[4 * i + 1], acc[4 * i + 2], acc[4 * i + 3]};
-  } else if constexpr (EPI == kEpiQKV) {
-    if (t >= g.T) return;
+    float *hr = g.h + (int64_t)t * g.N + tile * kGemmTile + 4 * half;
+    float ss = 0.f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int n = tile * kGemmTile + 8 * i + 4 * half;   // 4-runs never straddle q / k / v
-      bf16x4 v;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = (__bf16)acc[4 * i + r];
-      if (n < g.n_q) *(bf16x4 *)(g.q_out + (int64_t)t * g.n_q + n) = v;
-      else if (n < g.n_q + g.n_kv) *(bf16x4 *)(g.k_cache + (int64_t)g.dest[t] * g.n_kv + (n - g.n_q)) = v;
-      else *(bf16x4 *)(g.v_cache + (int64_t)g.dest[t] * g.n_kv + (n - g.n_q - g.n_kv)) = v;
-    }
-  } else {   // SwiGLU: m = silu(gate) * up, fp16; rows t >= T are written as zeros
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      f16x4 mv;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float gt = acc[4 * i + r], up = acc[4 * i + 8 + r];
-        mv[r] = (_Float16)(t < g.T ? gt / (1.0f + __expf(-gt)) * up : 0.f);
+        pre[i][r] += acc[4 * i + r];
+        ss = fmaf(pre[i][r], pre[i][r], ss);
       }
-      *(f16x4 *)((_Float16 *)g.m_out + (int64_t)t * g.I + tile * 16 + 8 * i + 4 * half) = mv;
+      *(f32x4 *)(hr + 8 * i) = pre[i];
+    }
+    if (!g.x_out) return;
+    ss += __shfl_xor(ss, 32);
+    if (half == 0) g.ss_out[(int64_t)t * (g.N / kGemmTile) + tile] = ss;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int n = tile * kGemmTile + 8 * i + 4 * half;
+      f32x4 v = pre[i];
+      if (g.gamma)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] *= (float)g.gamma[n + r];
+      if (g.x_out_f16) {
+        f16x4 o;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[r] = (_Float16)v[r];
+        *(f16x4 *)((_Float16 *)g.x_out + (int64_t)t * g.N + n) = o;
+      } else {
+        bf16x4 o;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[r] = (__bf16)v[r];
+        *(bf16x4 *)(g.x_out + (int64_t)t * g.N + n) = o;
+      }
+    }
+    return;
+  } else {
+    // per-token RMSNorm factor from the partial sums of squares
+    float sum = 0.f;
+    if (g.n_ss <= 32) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if (4 * i < g.n_ss) sum += (pre[i][0] + pre[i][1]) + (pre[i][2] + pre[i][3]);
+    } else {
+      const float *sr = g.ss_in + (int64_t)t * g.n_ss;
+      for (int i = 0; i < g.n_ss; i += 4) {
+        const f32x4 v = *(const f32x4 *)(sr + i);
+        sum += (v[0] + v[1]) + (v[2] + v[3]);
+      }
+    }
+    const float inv_rms = 1.0f / sqrtf(sum * g.inv_H + g.eps);
+    if constexpr (EPI == kEpiQKV) {
+      if (t >= g.T) return;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int n = tile * kGemmTile + 8 * i + 4 * half;   // 4-runs never straddle q / k / v
+        bf16x4 v;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = (__bf16)(acc[4 * i + r] * inv_rms);
+        if (n < g.n_q) *(bf16x4 *)(g.q_out + (int64_t)t * g.n_q + n) = v;
+        else if (n < g.n_q + g.n_kv) *(bf16x4 *)(g.k_cache + (int64_t)g.dest[t] * g.n_kv + (n - g.n_q)) = v;
+        else *(bf16x4 *)(g.v_cache + (int64_t)g.dest[t] * g.n_kv + (n - g.n_q - g.n_kv)) = v;
+      }
+    } else {   // SwiGLU: m = silu(gate) * up, fp16; rows t >= T are written as zeros
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        f16x4 mv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float gt = acc[4 * i + r] * inv_rms, up = acc[4 * i + 8 + r] * inv_rms;
+          mv[r] = (_Float16)(t < g.T ? gt / (1.0f + __expf(-gt)) * up : 0.f);
+        }
+        *(f16x4 *)((_Float16 *)g.m_out + (int64_t)t * g.I + tile * 16 + 8 * i + 4 * half) = mv;
+      }
     }
   }
 }
 
-// ------------------------------------------------------------ consumers of the partials
-
-// Sum over the splits of 4 consecutive partial columns; the loads of a batch
-// of 8 splits are all issued before the first add (split order kept).
-__device__ __forceinline__ f32x4 sum_splits(const float *part, int64_t split_stride, int ksplit) {
-  f32x4 s = {0.f, 0.f, 0.f, 0.f};
-  for (int k0 = 0; k0 < ksplit; k0 += 8) {
-    f32x4 v[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) v[i] = *(const f32x4 *)(part + (int64_t)min(k0 + i, ksplit - 1) * split_stride);
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      if (k0 + i < ksplit) s += v[i];
-  }
-  return s;
-}
-
-// Residual + RMSNorm: h[t] += sum of the splits of `part` (if any), then
-// x = RMSNorm(h[t]) * gamma -> x_hi as bf16 (or fp16) unless x_hi is NULL.  One
-// workgroup per row t < Tpad; rows t >= T are written as zeros (also the
-// padding rows `zero_rows`).  H is a multiple of 4.
-__global__ __launch_bounds__(256) void residual_norm_kernel(float *h, const float *part, int ksplit, int Tpad,
-                                                            int H, int T, const __bf16 *gamma, float eps,
-                                                            __bf16 *x_hi, int out_f16, __bf16 *zero_rows,
-                                                            int zero_cols) {
-  const int t = blockIdx.x;
-  const int tid = threadIdx.x;
+// Start of a step: h = h_in, x = h * gamma (bf16), sums of squares of h over
+// 32-column tiles; rows T..Tpad-1 of x and zero_rows are zeroed.  One
+// workgroup per row; H is a multiple of 128.
+__global__ __launch_bounds__(256) void norm_input_kernel(const float *h_in, float *h, int T, int H,
+                                                         const __bf16 *gamma, __bf16 *x, float *ss,
+                                                         __bf16 *zero_rows, int zero_cols) {
+  const int t = blockIdx.x, tid = threadIdx.x;
   if (t >= T) {
-    if (x_hi)
-      for (int c = tid; c < H; c += 256) x_hi[(int64_t)t * H + c] = (__bf16)0.f;   // 0 in bf16 and fp16
+    for (int c = tid; c < H; c += 256) x[(int64_t)t * H + c] = (__bf16)0.f;
     if (zero_rows)
       for (int c = tid; c < zero_cols; c += 256) zero_rows[(int64_t)t * zero_cols + c] = (__bf16)0.f;
     return;
   }
-  float *row = h + (int64_t)t * H;
-  float ss = 0.f;
   for (int c = 4 * tid; c < H; c += 1024) {
-    f32x4 v = *(const f32x4 *)(row + c);
-    if (part) {
-      v += sum_splits(part + (int64_t)t * H + c, (int64_t)Tpad * H, ksplit);
-      *(f32x4 *)(row + c) = v;
-    }
-    ss = fmaf(v[0], v[0], fmaf(v[1], v[1], fmaf(v[2], v[2], fmaf(v[3], v[3], ss))));
-  }
-  if (!x_hi) return;
-  for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
-  __shared__ float wsum[4];
-  if ((tid & 63) == 0) wsum[tid >> 6] = ss;
-  __syncthreads();
-  const float tot = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
-  const float inv = 1.0f / sqrtf(tot / (float)H + eps);
-  for (int c = 4 * tid; c < H; c += 1024) {
-    const f32x4 v = *(const f32x4 *)(row + c);
-    f32x4 x;
-    for (int r = 0; r < 4; ++r) x[r] = v[r] * inv * (gamma ? (float)gamma[c + r] : 1.f);
-    if (out_f16) {
-      f16x4 o;
-      for (int r = 0; r < 4; ++r) o[r] = (_Float16)x[r];
-      *(f16x4 *)((_Float16 *)x_hi + (int64_t)t * H + c) = o;
-    } else {
-      bf16x4 o;
-      for (int r = 0; r < 4; ++r) o[r] = (__bf16)x[r];
-      *(bf16x4 *)(x_hi + (int64_t)t * H + c) = o;
-    }
+    const f32x4 v = *(const f32x4 *)(h_in + (int64_t)t * H + c);
+    if (h != h_in) *(f32x4 *)(h + (int64_t)t * H + c) = v;
+    float sq = fmaf(v[0], v[0], fmaf(v[1], v[1], fmaf(v[2], v[2], v[3] * v[3])));
+    // 8 consecutive threads cover one 32-column tile
+    sq += __shfl_xor(sq, 1);
+    sq += __shfl_xor(sq, 2);
+    sq += __shfl_xor(sq, 4);
+    if ((tid & 7) == 0) ss[(int64_t)t * (H / kGemmTile) + c / kGemmTile] = sq;
+    bf16x4 o;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) o[r] = (__bf16)(v[r] * (gamma ? (float)gamma[c + r] : 1.f));
+    *(bf16x4 *)(x + (int64_t)t * H + c) = o;
   }
 }
 
 }  // namespace
 
-hipError_t launch_residual_norm(float *h, const float *part, int ksplit, int Tpad, int H, int T,
-                                const __bf16 *gamma, float eps, void *x_out, bool out_f16,
-                                __bf16 *zero_rows, int zero_cols, hipStream_t stream) {
+hipError_t launch_norm_input(const float *h_in, float *h, int T, int Tpad, int H, const __bf16 *gamma,
+                             __bf16 *x, float *ss, __bf16 *zero_rows, int zero_cols, hipStream_t stream) {
+  if (H % 128 != 0 || T < 1 || Tpad < T) return hipErrorInvalidValue;
   timed_begin(KK_NORM, stream);
-  hipLaunchKernelGGL(residual_norm_kernel, dim3(Tpad), dim3(256), 0, stream, h, part, ksplit, Tpad, H, T, gamma,
-                     eps, (__bf16 *)x_out, out_f16 ? 1 : 0, zero_rows, zero_cols);
+  hipLaunchKernelGGL(norm_input_kernel, dim3(Tpad), dim3(256), 0, stream, h_in, h, T, H, gamma, x, ss, zero_rows,
+                     zero_cols);
   timed_end(stream);
   return hipGetLastError();
 }
@@ -327,13 +350,13 @@ void launch_epi(const GemmArgs &g, dim3 grid, hipStream_t stream) {
 
 hipError_t launch_gemm(const GemmArgs &g, bool f16, int epi, int kind, hipStream_t stream) {
   const int kg = g.rg == 4 ? 1 : g.rg == 2 ? 2 : g.rg == 1 ? 4 : 0;
-  if (kg == 0 || g.K <= 0 || g.ksplit < 1 || (int64_t)g.ksplit * g.k_per_wg != g.K ||
-      g.k_per_wg % (kGemmKStep * kg) != 0 || g.Tpad % kGemmTile != 0 || g.n_ttiles * kGemmTile != g.Tpad ||
-      g.T > g.Tpad || g.N != g.n_slices * kGemmTile * g.rg || (epi != kEpiResidual && g.ksplit != 1) ||
+  if (kg == 0 || g.K <= 0 || g.K % (kGemmKStep * kg) != 0 || g.Tpad % kGemmTile != 0 ||
+      g.n_ttiles * kGemmTile != g.Tpad || g.T < 1 || g.T > g.Tpad || g.N != g.n_slices * kGemmTile * g.rg ||
       (epi == kEpiSwiGLU && (g.N != 2 * g.I || !f16)) || (epi == kEpiQKV && f16))
     return hipErrorInvalidValue;
-  const int nwg = g.n_slices * g.n_ttiles * g.ksplit;
-  if (nwg == 0) return hipSuccess;
+  if (epi == kEpiResidual ? (!g.h || (g.x_out && !g.ss_out)) : (!g.ss_in || g.n_ss < 4 || g.n_ss % 4 != 0))
+    return hipErrorInvalidValue;
+  const int nwg = g.n_slices * g.n_ttiles;
   const dim3 grid((nwg + 7) / 8 * 8);
   timed_begin(kind, stream);
   if (epi == kEpiSwiGLU) launch_epi<true, kEpiSwiGLU>(g, grid, stream);
@@ -344,29 +367,21 @@ hipError_t launch_gemm(const GemmArgs &g, bool f16, int epi, int kind, hipStream
   return hipGetLastError();
 }
 
-// Bytes one CU streams for a tile choice: per workgroup (32 rg + 32) rows of
-// k_per_wg K values (2 bytes each) plus its partial tile, times the
-// workgroups per CU (256 CUs); split-K adds the partials the residual kernel
-// reads back.  The cheapest shape wins (fewer workgroups on ties).
-GemmShape choose_gemm_shape(int N, int K, int Tpad, int epi) {
-  GemmShape best{0, 0};
+// Bytes one CU streams for a choice of rg: per workgroup (32 rg + 32) rows of
+// K values (2 bytes each), times the workgroups per CU (256 CUs).  The
+// cheapest shape wins (fewer workgroups on ties).
+int choose_gemm_rg(int N, int K, int Tpad) {
+  int best = 0;
   double best_cost = 0;
   const int tiles = Tpad / kGemmTile;
   for (int rg : {1, 2, 4}) {
     const int kg = 4 / rg;
-    if (N % (kGemmTile * rg) != 0) continue;
-    for (int ks = 1; ks <= 32; ++ks) {
-      if (ks > 1 && epi != kEpiResidual) break;
-      if (K % ks != 0 || (K / ks) % (kGemmKStep * kg) != 0) continue;
-      const double nwg = (double)(N / (kGemmTile * rg)) * tiles * ks;
-      double per_wg = (double)(kGemmTile * rg + kGemmTile) * (K / ks) * 2;
-      if (epi == kEpiResidual) per_wg += (double)kGemmTile * rg * kGemmTile * 4;
-      double cost = per_wg * std::max(1.0, nwg / 256.0);
-      if (ks > 1) cost += (double)ks * Tpad * N * 4 / 256.0;
-      if (best.rg == 0 || cost < best_cost * 0.999) {
-        best = GemmShape{rg, ks};
-        best_cost = cost;
-      }
+    if (N % (kGemmTile * rg) != 0 || K % (kGemmKStep * kg) != 0) continue;
+    const double nwg = (double)(N / (kGemmTile * rg)) * tiles;
+    const double cost = (double)(kGemmTile * rg + kGemmTile) * K * 2 * std::max(1.0, nwg / 256.0);
+    if (best == 0 || cost < best_cost * 0.999) {
+      best = rg;
+      best_cost = cost;
     }
   }
   return best;

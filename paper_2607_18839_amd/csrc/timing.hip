@@ -30,7 +30,7 @@ thread_local int t_open = -1;   // pool index of the pair opened by this thread
 
 const char *kKindNames[HPD_NUM_KERNEL_KINDS] = {
     "shared_prefix", "private", "merge", "gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down",
-    "residual_norm"};
+    "norm_input"};
 
 }  // namespace
 
