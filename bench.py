@@ -36,8 +36,8 @@ FP32_PEAK_TFLOPS = 157.3
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="c4")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--layers", type=int, default=None, help="c4 only: fewer layers (not for reporting)")
@@ -89,40 +89,43 @@ def main():
     print(json.dumps(res))
 
 
-def _graph_time(torch, step, n_in_graph, K, W):
-    """Captures n_in_graph consecutive steps in one HIP graph (torch's
-    CUDAGraph on ROCm), replays it W times untimed, then times replays
-    covering at least K steps.  Returns (ms per step, steps timed)."""
+def _graph_time(torch, step, n_graphs, K, W):
+    """Captures n_graphs HIP graphs (torch's CUDAGraph on ROCm), graph i
+    running step(i) once, replays them round-robin W times untimed, then
+    times exactly K replays, with an event after each.  Returns (mean ms per
+    step, K, {p10, p50, p90} of the per-step times in ms)."""
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):           # eager warm-up outside capture
-        for i in range(n_in_graph):
+        for i in range(n_graphs):
             step(i)
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
-        for i in range(n_in_graph):
+    graphs = []
+    for i in range(n_graphs):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
             step(i)
-    for _ in range(max(1, W)):
-        g.replay()
+        graphs.append(g)
+    for w in range(max(1, W)):
+        graphs[w % n_graphs].replay()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     torch.cuda.synchronize()
-    reps = max(1, -(-K // n_in_graph))
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        g.replay()
-    e1.record()
+    ev[0].record()
+    for i in range(K):
+        graphs[i % n_graphs].replay()
+        ev[i + 1].record()
     torch.cuda.synchronize()
-    return e0.elapsed_time(e1) / (reps * n_in_graph), reps * n_in_graph
+    per = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(K)])
+    pct = {f"p{q}": float(np.percentile(per, q)) for q in (10, 50, 90)}
+    return ev[0].elapsed_time(ev[K]) / K, K, pct
 
 
 def _kernel_pass(torch, _lib, step, K, W, queue_cycles=20_000_000):
-    """Per-kernel durations from HIP events the library records around each
-    launch.  Every step is first queued behind a bounded spin kernel
-    (torch.cuda._sleep), so its launches run back to back on the GPU and the
-    event intervals do not include host launch latency."""
+    """Per-kernel durations from the HIP events the library binds to each of
+    its launches (start and end of the kernel's execution).  Every step is
+    first queued behind a bounded spin kernel (torch.cuda._sleep), so its
+    launches run back to back on the GPU as in the timed region."""
     _lib.hpd_kernel_timing(1, 200000)
     _lib.hpd_kernel_times_read()
     tot = {}
@@ -137,6 +140,25 @@ def _kernel_pass(torch, _lib, step, K, W, queue_cycles=20_000_000):
     _lib.hpd_kernel_timing(0)
     return {k: dict(launches=c, avg_us=(1000.0 * ms / c if c else None)) for k, (c, ms) in tot.items()
             if not k.startswith("_") and c}
+
+
+def _traffic(kind):
+    """HBM bytes per launch of kernel kind from profiles/traffic_c4.md (rocprofv3
+    FETCH_SIZE / WRITE_SIZE runs scaled by a plain copy kernel's readings), or
+    None when the kernel's source has changed since the counters were taken."""
+    import hashlib
+    import re
+    root = os.path.dirname(os.path.abspath(__file__))
+    try:
+        text = open(os.path.join(root, "profiles", "traffic_c4.md")).read()
+        block = json.loads(re.search(r"```json\n(.*?)```", text, re.S).group(1))
+        k = block["kernels"][kind]
+        src = os.path.join(root, "paper_2607_18839_amd", "csrc", k["source"])
+        if hashlib.sha256(open(src, "rb").read()).hexdigest() != block["source_sha256"][k["source"]]:
+            return None
+        return k["traffic_bytes"]
+    except (OSError, KeyError, AttributeError, ValueError):
+        return None
 
 
 def _cpu_info():
@@ -171,7 +193,7 @@ def bench_attention(args, torch, _lib):
         q, sk, sv, pk, pv = replicas[i % reps]
         layer(q, sk, sv, pk, pv, out=out)
 
-    ms, timed = _graph_time(torch, step, min(args.steps, reps), args.steps, args.warmup)
+    ms, timed, pct = _graph_time(torch, step, reps, args.steps, args.warmup)
     kern = _kernel_pass(torch, _lib, step, min(args.steps, 20), args.warmup, queue_cycles=2_000_000)
     w = attn_work(b.prefix_len, b.branch_page, b.num_new, b.past_len, b.num_q_heads, b.num_kv_heads, 64,
                   s_in, s_in)
@@ -195,9 +217,9 @@ def bench_attention(args, torch, _lib):
                 "algorithmic_per_launch": sh_flop}
     res = {
         "metric": "branch-tokens/s per decode step", "value": w["T"] / (ms / 1e3), "unit": "branch-tokens/s",
-        "n_gpus": 1, "steps": timed, "warmup": args.warmup, "ms_per_step": ms,
+        "n_gpus": 1, "steps": timed, "warmup": args.warmup, "ms_per_step": ms, "latency_ms": pct,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": b.dtype, "data": "synthetic", "timing": "HIP graph replay",
+        "dtype": b.dtype, "data": "synthetic", "timing": "HIP graph replay (one step per graph, one graph per input replica)",
         "config": {"workload": f"{args.workload}: single attention layer", "pages": b.num_pages,
                    "branches": b.num_branches, "branch_tokens": w["T"],
                    "prefix_len_total": int(b.prefix_len.sum()),
@@ -262,7 +284,7 @@ def bench_decode(args, torch, _lib):
     def step(i):
         step_obj(h_in, sk, sv, pk, pv, hidden_out=h_out)
 
-    ms, timed = _graph_time(torch, step, 1, args.steps, args.warmup)
+    ms, timed, pct = _graph_time(torch, step, 1, args.steps, args.warmup)
     kern = _kernel_pass(torch, _lib, step, min(args.steps, 10), args.warmup)
     T, Hq, Hkv, D, H, I = step_obj.T, inp.num_q_heads, inp.num_kv_heads, 64, inp.hidden, inp.intermediate
     aw = attn_work(inp.prefix_len, inp.branch_page, inp.num_new, inp.past_len, Hq, Hkv, D, 2, 2)
@@ -283,13 +305,13 @@ def bench_decode(args, torch, _lib):
     d = kern[dom]
     if d.get("bound") == "mfma":
         roof = {"bound": "mfma", "kernel": dom, "achieved": d["tflops"], "peak": BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": d["frac"], "traffic": None, "algorithmic_per_launch": d["flop"]}
+                "unit": "TFLOP/s", "frac": d["frac"], "traffic": _traffic(dom), "algorithmic_per_launch": d["flop"]}
     else:
         roof = {"bound": "hbm", "kernel": dom, "achieved": d.get("gbs"), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": d.get("frac"), "traffic": None, "algorithmic_per_launch": d.get("bytes")}
+                "frac": d.get("frac"), "traffic": _traffic(dom), "algorithmic_per_launch": d.get("bytes")}
     res = {
         "metric": "branch-tokens/s per decode step", "value": T / (ms / 1e3), "unit": "branch-tokens/s",
-        "n_gpus": 1, "steps": timed, "warmup": args.warmup, "ms_per_step": ms,
+        "n_gpus": 1, "steps": timed, "warmup": args.warmup, "ms_per_step": ms, "latency_ms": pct,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "timing": "HIP graph replay (one step per graph)",
         "data": "synthetic (seeded N(0,1) KV and hidden, N(0,0.02) bf16 weights)",

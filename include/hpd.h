@@ -210,15 +210,16 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan,
                            void *workspace, size_t workspace_bytes, void *stream);
 
 /* ---- Benchmark support: per-kernel timing with HIP events.
- * When enabled, every kernel a step enqueues is bracketed by a pair of HIP
- * events recorded on that kernel's own stream; hpd_kernel_times_read waits
- * for them and returns, per kernel kind, the number of launches and the sum
- * of their elapsed times since the previous read.  The event pool
+ * When enabled, every kernel a step enqueues is launched with a pair of HIP
+ * events bound to its own dispatch (hipExtLaunchKernel), so each pair spans
+ * the kernel's execution, as a kernel trace reports it.  hpd_kernel_times_read
+ * waits for the pairs and returns, per kernel kind, the number of launches and
+ * the sum of their durations since the previous read.  The event pool
  * (max_launches pairs) is created by hpd_kernel_timing(1, n), outside any
- * timed region; launches beyond it are counted in `dropped`.  Timing adds
- * two event records per launch.  Under stream capture the event records
- * become graph nodes: read with keep_pairs = 1 after each replay (the pairs
- * stay assigned to the captured launches); keep_pairs = 0 releases them. */
+ * timed region; launches beyond it are counted in `dropped`.  Timing is for
+ * eager launches: do not enable it while capturing a graph.  keep_pairs = 1
+ * keeps the pairs assigned after the read (re-read after re-running the same
+ * launches); keep_pairs = 0 releases them. */
 #define HPD_NUM_KERNEL_KINDS 8
 typedef struct {
   int64_t count[HPD_NUM_KERNEL_KINDS];

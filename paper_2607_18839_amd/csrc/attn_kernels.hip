@@ -855,43 +855,23 @@ hipError_t launch_branch_attention(const Plan &P, const void *q, const void *sha
   if (bf16) {
     // one launch: shared-prefix items, then the private items 8 per workgroup
     const int nwg = a.n_shared + (a.n_private + kPrivPerWG - 1) / kPrivPerWG;
-    if (nwg > 0) {
-      timed_begin(KK_SHARED, stream);
-      hipLaunchKernelGGL(shared_prefix_ring_kernel, dim3((nwg + 7) / 8 * 8), dim3(512), 0, stream, a);
-      timed_end(stream);
-    }
+    if (nwg > 0) launch(KK_SHARED, shared_prefix_ring_kernel, dim3((nwg + 7) / 8 * 8), dim3(512), stream, a);
   } else {
-    if (a.n_shared > 0) {
-      timed_begin(KK_SHARED, stream);
-      hipLaunchKernelGGL(shared_prefix_kernel<float>, dim3((a.n_shared + 7) / 8 * 8), dim3(256), 0, stream, a);
-      timed_end(stream);
-    }
-    if (a.n_private > 0) {
-      timed_begin(KK_PRIVATE, stream);
-      hipLaunchKernelGGL(private_kernel_f32, dim3(a.n_private), dim3(64), 0, stream, a);
-      timed_end(stream);
-    }
+    if (a.n_shared > 0)
+      launch(KK_SHARED, shared_prefix_kernel<float>, dim3((a.n_shared + 7) / 8 * 8), dim3(256), stream, a);
+    if (a.n_private > 0) launch(KK_PRIVATE, private_kernel_f32, dim3(a.n_private), dim3(64), stream, a);
   }
   const int rows = P.T * P.attn.num_q_heads;
-  const int mgrid = (rows + 15) / 16;
-  timed_begin(KK_MERGE, stream);
+  const dim3 mgrid((rows + 15) / 16), mblock(256);
+  const int T = P.T, Hq = P.attn.num_q_heads;
   // bf16 inputs: fp16 partials; fp32 inputs: fp32 partials
   if (P.attn.out_dtype == HPD_BF16) {
-    if (bf16)
-      hipLaunchKernelGGL((merge_kernel<__bf16, _Float16>), dim3(mgrid), dim3(256), 0, stream, a.dev, (__bf16 *)out,
-                         lse, P.T, P.attn.num_q_heads);
-    else
-      hipLaunchKernelGGL((merge_kernel<__bf16, float>), dim3(mgrid), dim3(256), 0, stream, a.dev, (__bf16 *)out,
-                         lse, P.T, P.attn.num_q_heads);
+    if (bf16) launch(KK_MERGE, merge_kernel<__bf16, _Float16>, mgrid, mblock, stream, a.dev, (__bf16 *)out, lse, T, Hq);
+    else launch(KK_MERGE, merge_kernel<__bf16, float>, mgrid, mblock, stream, a.dev, (__bf16 *)out, lse, T, Hq);
   } else {
-    if (bf16)
-      hipLaunchKernelGGL((merge_kernel<float, _Float16>), dim3(mgrid), dim3(256), 0, stream, a.dev, (float *)out,
-                         lse, P.T, P.attn.num_q_heads);
-    else
-      hipLaunchKernelGGL((merge_kernel<float, float>), dim3(mgrid), dim3(256), 0, stream, a.dev, (float *)out, lse,
-                         P.T, P.attn.num_q_heads);
+    if (bf16) launch(KK_MERGE, merge_kernel<float, _Float16>, mgrid, mblock, stream, a.dev, (float *)out, lse, T, Hq);
+    else launch(KK_MERGE, merge_kernel<float, float>, mgrid, mblock, stream, a.dev, (float *)out, lse, T, Hq);
   }
-  timed_end(stream);
   return hipGetLastError();
 }
 

@@ -330,20 +330,17 @@ __global__ __launch_bounds__(256) void norm_input_kernel(const float *h_in, floa
 hipError_t launch_norm_input(const float *h_in, float *h, int T, int Tpad, int H, const __bf16 *gamma,
                              __bf16 *x, float *ss, __bf16 *zero_rows, int zero_cols, hipStream_t stream) {
   if (H % 128 != 0 || T < 1 || Tpad < T) return hipErrorInvalidValue;
-  timed_begin(KK_NORM, stream);
-  hipLaunchKernelGGL(norm_input_kernel, dim3(Tpad), dim3(256), 0, stream, h_in, h, T, H, gamma, x, ss, zero_rows,
-                     zero_cols);
-  timed_end(stream);
+  launch(KK_NORM, norm_input_kernel, dim3(Tpad), dim3(256), stream, h_in, h, T, H, gamma, x, ss, zero_rows, zero_cols);
   return hipGetLastError();
 }
 
 namespace {
 
 template <bool F16, int EPI>
-void launch_epi(const GemmArgs &g, dim3 grid, hipStream_t stream) {
-  if (g.rg == 4) hipLaunchKernelGGL((gemm_kernel<4, F16, EPI>), grid, dim3(256), 0, stream, g);
-  else if (g.rg == 2) hipLaunchKernelGGL((gemm_kernel<2, F16, EPI>), grid, dim3(256), 0, stream, g);
-  else hipLaunchKernelGGL((gemm_kernel<1, F16, EPI>), grid, dim3(256), 0, stream, g);
+void launch_epi(const GemmArgs &g, int kind, dim3 grid, hipStream_t stream) {
+  if (g.rg == 4) launch(kind, gemm_kernel<4, F16, EPI>, grid, dim3(256), stream, g);
+  else if (g.rg == 2) launch(kind, gemm_kernel<2, F16, EPI>, grid, dim3(256), stream, g);
+  else launch(kind, gemm_kernel<1, F16, EPI>, grid, dim3(256), stream, g);
 }
 
 }  // namespace
@@ -358,12 +355,10 @@ hipError_t launch_gemm(const GemmArgs &g, bool f16, int epi, int kind, hipStream
     return hipErrorInvalidValue;
   const int nwg = g.n_slices * g.n_ttiles;
   const dim3 grid((nwg + 7) / 8 * 8);
-  timed_begin(kind, stream);
-  if (epi == kEpiSwiGLU) launch_epi<true, kEpiSwiGLU>(g, grid, stream);
-  else if (epi == kEpiQKV) launch_epi<false, kEpiQKV>(g, grid, stream);
-  else if (f16) launch_epi<true, kEpiResidual>(g, grid, stream);
-  else launch_epi<false, kEpiResidual>(g, grid, stream);
-  timed_end(stream);
+  if (epi == kEpiSwiGLU) launch_epi<true, kEpiSwiGLU>(g, kind, grid, stream);
+  else if (epi == kEpiQKV) launch_epi<false, kEpiQKV>(g, kind, grid, stream);
+  else if (f16) launch_epi<true, kEpiResidual>(g, kind, grid, stream);
+  else launch_epi<false, kEpiResidual>(g, kind, grid, stream);
   return hipGetLastError();
 }
 

@@ -1,6 +1,7 @@
 // Internal launchers of the gfx950 kernels (not part of the public ABI).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "plan.h"
@@ -24,8 +25,21 @@ PlanDev plan_dev(const Plan &P, void *workspace);
 // Kernel kinds of the optional benchmark timing (hpd_kernel_timing).
 enum KernelKind { KK_SHARED = 0, KK_PRIVATE, KK_MERGE, KK_GEMM_QKV, KK_GEMM_O, KK_GEMM_GATE_UP,
                   KK_GEMM_DOWN, KK_NORM };
-void timed_begin(int kind, hipStream_t stream);
-void timed_end(hipStream_t stream);
+// Per-kernel timing (benchmark support).  When timing is on, timed_events
+// hands out a pool pair for a launch of `kind` (else two nulls); launch()
+// then binds the pair to the kernel's own dispatch (start and end of its
+// execution, not markers around it).
+struct TimedEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+TimedEvents timed_events(int kind);
+
+template <typename... KArgs, typename... Args>
+void launch(int kind, void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t stream, Args... args) {
+  const TimedEvents ev = timed_events(kind);
+  if (ev.start) hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, ev.start, ev.stop, 0, args...);
+  else hipLaunchKernelGGL(kernel, grid, block, 0, stream, args...);
+}
 
 // One attention layer: shared-prefix kernel, private kernel, merge kernel.
 // q/k/v in P.attn.dtype; out in P.attn.out_dtype; lse may be NULL.

@@ -9,6 +9,7 @@
 
 #include <cstdio>
 #include <cstdlib>
+#include <string>
 #include <vector>
 
 #define CHECK(x)                                                                      \
@@ -137,7 +138,11 @@ template <typename F> float time_ms(F launch, int reps) {
 }
 
 int main(int argc, char **argv) {
-  const size_t mib = argc > 1 ? std::strtoul(argv[1], nullptr, 10) : 1024;
+  // "peaks copy N": only N MiB copies (3 launches), the reference for
+  // scaling memory-traffic counters; otherwise "peaks [N]" runs everything.
+  const bool copy_only = argc > 1 && std::string(argv[1]) == "copy";
+  const int size_arg = copy_only ? 2 : 1;
+  const size_t mib = argc > size_arg ? std::strtoul(argv[size_arg], nullptr, 10) : 1024;
   const size_t bytes = mib << 20, n4 = bytes / 16;
   hipDeviceProp_t prop;
   CHECK(hipGetDeviceProperties(&prop, 0));
@@ -149,6 +154,12 @@ int main(int argc, char **argv) {
   CHECK(hipMemset(src, 0, bytes));
   const int cus = prop.multiProcessorCount;
   const int grid = cus * 8;
+  if (copy_only) {
+    for (int i = 0; i < 3; ++i) hipLaunchKernelGGL(copy_kernel, dim3(grid), dim3(256), 0, 0, src, dst, n4);
+    CHECK(hipDeviceSynchronize());
+    std::printf("{\"copy_mib\": %zu, \"launches\": 3}\n", mib);
+    return 0;
+  }
 
   const float copy_ms = time_ms([&] { hipLaunchKernelGGL(copy_kernel, dim3(grid), dim3(256), 0, 0, src, dst, n4); }, 10);
   const float read_ms = time_ms([&] { hipLaunchKernelGGL(read_kernel, dim3(grid), dim3(256), 0, 0, src, n4, sink); }, 10);

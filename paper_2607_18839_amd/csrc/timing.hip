@@ -1,8 +1,9 @@
 // Optional per-kernel timing with HIP events, for benchmarks.
 //
-// When enabled, every launcher brackets each kernel it enqueues with a pair
-// of events recorded on the kernel's own stream.  Events come from a pool
-// created when timing is switched on, so the timed region creates nothing.
+// When enabled, every launch gets a pair of events bound to its dispatch
+// (hipExtLaunchKernel: the kernel's own start and end).  Events come from a
+// pool created when timing is switched on, so the timed region creates
+// nothing.
 #include <hip/hip_runtime.h>
 
 #include <mutex>
@@ -26,7 +27,6 @@ size_t g_used = 0;
 double g_total_ms[HPD_NUM_KERNEL_KINDS] = {};
 int64_t g_count[HPD_NUM_KERNEL_KINDS] = {};
 int64_t g_dropped = 0;
-thread_local int t_open = -1;   // pool index of the pair opened by this thread
 
 const char *kKindNames[HPD_NUM_KERNEL_KINDS] = {
     "shared_prefix", "private", "merge", "gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down",
@@ -34,23 +34,19 @@ const char *kKindNames[HPD_NUM_KERNEL_KINDS] = {
 
 }  // namespace
 
-void timed_begin(int kind, hipStream_t stream) {
-  if (!g_enabled) return;
+TimedEvents timed_events(int kind) {
+  TimedEvents ev;
+  if (!g_enabled) return ev;
   std::lock_guard<std::mutex> lk(g_mu);
   if (g_used >= g_pool.size()) {
     ++g_dropped;
-    t_open = -1;
-    return;
+    return ev;
   }
-  t_open = (int)g_used++;
-  g_pool[t_open].kind = kind;
-  hipEventRecord(g_pool[t_open].start, stream);
-}
-
-void timed_end(hipStream_t stream) {
-  if (!g_enabled || t_open < 0) return;
-  hipEventRecord(g_pool[t_open].stop, stream);
-  t_open = -1;
+  Pair &p = g_pool[g_used++];
+  p.kind = kind;
+  ev.start = p.start;
+  ev.stop = p.stop;
+  return ev;
 }
 
 }  // namespace hpd
