@@ -334,18 +334,12 @@ template <typename T> struct WaveAttn {
     }
   }
 
-  // bf16 tile from the LDS ring: K tile kt (Tile<bf16> swizzle), V tile vt
-  // ([key][dims], vchunk swizzle).  voff: this lane's transpose-read offsets
-  // for dims blocks 0 and 1 (see vt_offsets).  Same arithmetic as tile(),
-  // except that the running max is only raised when a score exceeds it by
-  // more than 2^8 (log2 units): the probabilities then stay <= 256, and the
-  // O / l rescale is skipped for the (common) tiles that do not raise it.
-  __device__ __forceinline__ void tile_ring(const unsigned char *kt, const unsigned char *vt, const int (&voff)[2],
-                                            int key0, int limit, bool masked, float c, int lane) {
+  // Raw scores S^T of a K tile in the ring (Tile<bf16> swizzle): the two
+  // 32-key blocks' MFMA chains are interleaved.
+  __device__ __forceinline__ void qk_ring(const unsigned char *kt, f32x16 (&s)[2], int lane) {
     static_assert(sizeof(T) == 2, "bf16 only");
     using Tl = Tile<T>;
     const int kr = lane & 31;
-    f32x16 s[2];
     for (int r = 0; r < 16; ++r) { s[0][r] = 0.f; s[1][r] = 0.f; }
     Frag<T> a[2][4];
 #pragma unroll
@@ -356,9 +350,110 @@ template <typename T> struct WaveAttn {
         ld16(a[kb][st], (const T *)(kt + key * Tl::kRowBytes + 16 * Tl::kchunk(key, 4 * half + st)));
     }
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int st = 0; st < 4; ++st)
 #pragma unroll
-      for (int st = 0; st < 4; ++st) mma(s[kb], a[kb][st], qf[st]);
+      for (int kb = 0; kb < 2; ++kb) mma(s[kb], a[kb][st], qf[st]);
+  }
+
+  // One software-pipelined step of the ring kernel: the LDS reads of the
+  // next tile's K (kt_next, or none) and of this tile's V^T are issued first,
+  // the softmax of this tile's raw scores s_cur runs while they are in flight,
+  // then the next tile's QK^T MFMAs (into s_next) and this tile's PV and
+  // row-sum MFMAs are issued together.
+  __device__ __forceinline__ void step_ring(const unsigned char *kt_next, const unsigned char *vt, const int (&voff)[2],
+                                            f32x16 (&s_cur)[2], f32x16 (&s_next)[2], int key0, int limit,
+                                            bool masked, float c, int lane) {
+    static_assert(sizeof(T) == 2, "bf16 only");
+    using Tl = Tile<T>;
+    const int kr = lane & 31;
+    Frag<T> ka[2][4];
+    if (kt_next) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const int key = 32 * kb + kr;
+#pragma unroll
+        for (int st = 0; st < 4; ++st)
+          ld16(ka[kb][st], (const T *)(kt_next + key * Tl::kRowBytes + 16 * Tl::kchunk(key, 4 * half + st)));
+      }
+    }
+    u32x2t vr[16];   // [b][st][hh]
+    ds_read_tr16_tile<0>(vr, vt + voff[0], vt + voff[1]);
+    // softmax of this tile (VALU)
+    if (masked) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = key0 + 32 * kb + (r >> 2) * 8 + 4 * half + (r & 3);
+          if (key >= limit) s_cur[kb][r] = -INFINITY;
+        }
+    }
+    float mx = s_cur[0][0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s_cur[0][r]);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s_cur[1][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32)) * c;
+    if (__ballot(mx > m + 8.f)) {   // wave-uniform: some query's max grew by > 2^8
+      const float m_new = fmaxf(m, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m - (m_new == -INFINITY ? 0.f : m_new));
+      m = m_new;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) { o[0][r] *= alpha; o[1][r] *= alpha; lsum[r] *= alpha; }
+    }
+    const float m_use = m == -INFINITY ? 0.f : m;
+    float p[32];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      p[r] = __builtin_amdgcn_exp2f(fmaf(s_cur[0][r], c, -m_use));
+      p[16 + r] = __builtin_amdgcn_exp2f(fmaf(s_cur[1][r], c, -m_use));
+    }
+    Frag<T> pf[4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) from_f32(pf[st], p + 8 * st);
+    lds_wait_tr(vr);   // also completes the K reads (lgkmcnt(0))
+    // matrix core: next tile's scores, this tile's PV and row sums
+    if (kt_next) {
+      for (int r = 0; r < 16; ++r) { s_next[0][r] = 0.f; s_next[1][r] = 0.f; }
+#pragma unroll
+      for (int st = 0; st < 4; ++st)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) mma(s_next[kb], ka[kb][st], qf[st]);
+    }
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int st = 0; st < 4; ++st) {
+        Frag<T> va;
+        va.v = __builtin_bit_cast(bf16x8, u32x4{vr[(b * 4 + st) * 2][0], vr[(b * 4 + st) * 2][1],
+                                                vr[(b * 4 + st) * 2 + 1][0], vr[(b * 4 + st) * 2 + 1][1]});
+        mma(o[b], va, pf[st]);
+      }
+    Frag<T> ones;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ones.v[e] = (__bf16)1.f;
+#pragma unroll
+    for (int st = 0; st < 4; ++st) mma(lsum, ones, pf[st]);
+  }
+
+  // bf16 tile from the LDS ring: K tile kt (Tile<bf16> swizzle), V tile vt.
+  // Same arithmetic as tile() apart from the lazily raised max (see
+  // softmax_pv_ring).
+  __device__ __forceinline__ void tile_ring(const unsigned char *kt, const unsigned char *vt, const int (&voff)[2],
+                                            int key0, int limit, bool masked, float c, int lane) {
+    f32x16 s[2];
+    qk_ring(kt, s, lane);
+    softmax_pv_ring(s, vt, voff, key0, limit, masked, c, lane);
+  }
+
+  // Softmax of raw scores s (tile with first key key0) and O^T += V^T P^T
+  // from the V tile vt ([key][dims], vchunk swizzle).  voff: this lane's
+  // transpose-read offsets for dims blocks 0 and 1 (see vt_offsets).  The
+  // running max is only raised when a score exceeds it by more than 2^8
+  // (log2 units): the probabilities then stay <= 256, and the O / l rescale
+  // is skipped for the (common) tiles that do not raise it.
+  __device__ __forceinline__ void softmax_pv_ring(f32x16 (&s)[2], const unsigned char *vt, const int (&voff)[2],
+                                                  int key0, int limit, bool masked, float c, int lane) {
     if (masked) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
@@ -572,15 +667,17 @@ __global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
 
 // bf16 shared-prefix kernel: same items and arithmetic as shared_prefix_kernel,
 // on 8 waves: waves w and w + 4 own the same 32 rows and take the even and
-// odd key tiles of the item, so two waves share each SIMD (one's MFMAs
-// overlap the other's softmax); their states are combined through LDS at the
-// end.  K and V stream through an LDS ring of kPairRing tile pairs filled by
-// direct global -> LDS copies, two pairs ahead.  Each tile is 16 copy
-// instructions of 8 key rows x 128 bytes (4 per wave and pair).  Key rows past
-// the item's range are clamped to its last key (their scores are masked; a
-// pair's missing odd tile is loaded clamped and not used), which keeps every
-// wave's copy count the same.
-constexpr int kPairRing = 3;
+// odd key tiles of the item, so two waves share each SIMD; their states are
+// combined through LDS at the end.  K and V stream through an LDS ring of
+// kPairRing tile pairs filled by direct global -> LDS copies, up to three pairs
+// ahead.  Each wave is software-pipelined by one tile: the QK^T MFMAs of its
+// next tile are issued before the softmax of the current one, so they run on
+// the matrix core while the VALU works.  Each tile is 16 copy instructions of
+// 8 key rows x 128 bytes (4 per wave and pair).  Key rows past the item's
+// range are clamped to its last key (their scores are masked; a pair's
+// missing odd tile is loaded clamped and not used), which keeps every wave's
+// copy count the same.
+constexpr int kPairRing = 4;
 
 template <typename T, bool WAVE_LOCAL>
 __device__ __forceinline__ void private_item(const AttnArgs &a, int item, int lane, unsigned char *lds);
@@ -640,33 +737,43 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
     dma16(vbase + r0 * stride + 8 * vq0, st + kTileBytes + 1024 * (2 * rw));
     dma16(vbase + r1 * stride + 8 * vq1, st + kTileBytes + 1024 * (2 * rw + 1));
   };
-  static_assert(kPairRing == 3, "the waits below assume two pairs in flight");
-  // Pair 0, then this lane's Q fragments and partial-row index, then pair 1.
-  // Pair 0 and the loads behind it are retired here (pair 1 stays in
-  // flight), so the loop never waits for the Q loads.
+  // wait until pair j's copies (this wave's 4) have landed, with `ahead`
+  // later pairs still in flight
+  auto wait_pair = [&](int ahead) {
+    if (ahead >= 2) wait_vm<8>();
+    else if (ahead == 1) wait_vm<4>();
+    else wait_vm<0>();
+  };
+  static_assert(kPairRing == 4, "the ring holds pairs j - 1 .. j + 2 at iteration j");
+  // Pair 0, then this lane's Q fragments and partial-row index, then pairs 1
+  // and 2.  Pair 0 and the loads behind it are retired here, so the loop
+  // never waits for the Q loads.
   if (npairs > 0) issue(0);
   WaveAttn<T> w;
   w.init((const T *)a.q + ((int64_t)t * a.Hq + hq) * D, valid, lane);
   const int my_slots = valid ? a.dev.token_slots[2 * t] : 0;
-  if (npairs > 1) {
-    issue(1);
-    wait_vm<4>();
-  } else {
-    wait_vm<0>();
-  }
+  if (npairs > 1) issue(1);
+  if (npairs > 2) issue(2);
+  wait_pair(min(npairs - 1, 2));
   const int my_prow = valid ? (my_slots + slot) * a.Hq + hq : -1;
+  ring_barrier();   // pair 0 visible to every wave
+  f32x16 s_cur[2], s_next[2];
+  if (wave_active && par < ntiles) w.qk_ring(lds + par * kTile, s_cur, lane);
   for (int j = 0; j < npairs; ++j) {
-    if (j > 0) {
-      if (j + 1 < npairs) wait_vm<4>();
-      else wait_vm<0>();
+    // pair j + 1 visible; the slot of pair j - 1 (read in iteration j - 1) is free
+    if (j + 1 < npairs) {
+      wait_pair(min(npairs - 1, j + 2) - (j + 1));
+      ring_barrier();
+      if (j + 3 < npairs) issue(j + 3);
     }
-    ring_barrier();   // pair j visible to every wave; the slot of pair j - 1 is free
-    if (j + 2 < npairs) issue(j + 2);
     const int ti = 2 * j + par;
     if (wave_active && ti < ntiles) {
+      const unsigned char *kt_next = ti + 2 < ntiles ? lds + ((j + 1) % S) * kPair + par * kTile : nullptr;
       const int k0 = key0 + 64 * ti;
-      const unsigned char *st = lds + (j % S) * kPair + par * kTile;
-      w.tile_ring(st, st + kTileBytes, voff, k0, limit, k0 + 64 > wmin, a.c, lane);
+      w.step_ring(kt_next, lds + (j % S) * kPair + par * kTile + kTileBytes, voff, s_cur, s_next, k0, limit,
+                  k0 + 64 > wmin, a.c, lane);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) { s_cur[0][r] = s_next[0][r]; s_cur[1][r] = s_next[1][r]; }
     }
   }
   ring_barrier();   // every wave is done with the ring; its LDS becomes scratch

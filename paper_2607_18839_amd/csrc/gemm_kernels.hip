@@ -79,7 +79,9 @@ template <int N> __device__ __forceinline__ void wait_vm() {
 // its in-flight global -> LDS copies (those are waited for by count).
 __device__ __forceinline__ void ring_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-constexpr int kRing = 4;   // LDS ring depth in pipeline steps
+// LDS ring depth in pipeline steps (measured: 2 to 7 steps stream equally
+// fast or slower; the per-step cost, not the bytes in flight, sets the pace).
+constexpr int kRing = 4;
 
 // Each step (64 K) of a K group lands in LDS as RG weight tiles and one token
 // tile of [32 rows][128 bytes].  The copies are spread over the group's waves
@@ -161,11 +163,17 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     for (int j = 0; j < kInstr; ++j) dma16(src[j] + c * kGemmKStep, st + dst[j]);
   };
   // wait until this wave's copies of the current step have landed, with
-  // `ahead` later steps still in flight
+  // `ahead` (<= S - 2) later steps still in flight
   auto wait_step = [&](int ahead) {
-    if (ahead >= 2) wait_vm<2 * kInstr>();
-    else if (ahead == 1) wait_vm<kInstr>();
-    else wait_vm<0>();
+    static_assert(S <= 7 && (S - 2) * kInstr < 64, "vmcnt range");
+    switch (ahead) {
+      case 0: wait_vm<0>(); break;
+      case 1: wait_vm<kInstr>(); break;
+      case 2: wait_vm<2 * kInstr>(); break;
+      case 3: wait_vm<3 * kInstr>(); break;
+      case 4: wait_vm<4 * kInstr>(); break;
+      default: wait_vm<5 * kInstr>(); break;
+    }
   };
 
   f32x16 acc;
@@ -178,7 +186,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     if (c < nsteps) issue(c);
   for (int c = 0; c < nsteps; ++c) {
     wait_step(min(nsteps - 1 - c, S - 2));
-    ring_barrier();   // step c visible to every wave; the slot of step c - 1 is free
+    // step c visible to every wave, the slot of step c - 1 free: with rg = 1
+    // each wave reads only the tiles it copied itself, so its own waits and
+    // LDS-completion suffice; otherwise the waves share the token tile
+    if constexpr (RG > 1) ring_barrier();
+    else asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     if (c + S - 1 < nsteps) issue(c + S - 1);
     const unsigned char *st = lds + (c % S) * kStageBytes;
     u32x4 av[4], bv[4];   // all fragments of the step are read before the first MFMA
