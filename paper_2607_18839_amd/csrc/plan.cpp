@@ -159,9 +159,15 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   int64_t mult = std::max<int64_t>(1, ceil_div(units, kSharedTargetItems));
   while (shared_items_for(kSharedSplitUnit * mult) > kSharedTargetItems) ++mult;   // ceilings per page
   P.split_keys = (int32_t)std::min<int64_t>(kSharedSplitUnit * mult, INT32_MAX / 2);
-  std::vector<int32_t> page_splits(np);
-  for (int p = 0; p < np; ++p)
+  // each page's prefix is cut into page_splits[p] ranges of equal length
+  // (rounded up to kSharedSplitUnit), so one page's items are balanced
+  std::vector<int32_t> page_splits(np), page_split_keys(np);
+  for (int p = 0; p < np; ++p) {
     page_splits[p] = (int32_t)ceil_div(P.prefix_len[p], P.split_keys);
+    page_split_keys[p] = page_splits[p] > 0 ? (int32_t)(kSharedSplitUnit *
+        ceil_div(ceil_div(P.prefix_len[p], page_splits[p]), kSharedSplitUnit)) : 0;
+    if (page_split_keys[p] > 0) page_splits[p] = (int32_t)ceil_div(P.prefix_len[p], page_split_keys[p]);
+  }
   P.token_slots.resize(2 * (size_t)P.T);
   int64_t slot = 0;
   for (int i = 0; i < nb; ++i) {
@@ -188,7 +194,7 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
       for (int s = 0; s < page_splits[p]; ++s)
         for (int r0 = 0; r0 < R; r0 += group_rows) {
           const int nr = std::min(group_rows, R - r0);
-          const int k0 = s * P.split_keys, k1 = std::min(Pp, k0 + P.split_keys);
+          const int k0 = s * page_split_keys[p], k1 = std::min(Pp, k0 + page_split_keys[p]);
           int flags = 0;
           if (P.has_fork)
             for (int r = r0; r < r0 + nr; ++r)
