@@ -871,9 +871,13 @@ __global__ __launch_bounds__(64) void private_kernel_f32(AttnArgs a) {
 // ------------------------------------------------------------ merge kernel
 
 // 16 threads per (token, head) row, 4 dims each.  Partial lse values are in
-// log2 units; the exported lse is natural-log.
+// log2 units; the exported lse is natural-log.  One pass over the partials in
+// batches of 16 (every load of a batch issued before its first use), with a
+// running max: sum_i 2^(lse_i - m) O_i / sum_i 2^(lse_i - m), partials in
+// slot order.
 template <typename TO, typename TP>
 __global__ __launch_bounds__(256) void merge_kernel(PlanDev dev, TO *out, float *lse, int T, int Hq) {
+  constexpr int B = 16;
   const int row = blockIdx.x * 16 + (threadIdx.x >> 4);
   if (row >= T * Hq) return;
   const int sub = threadIdx.x & 15;
@@ -881,41 +885,40 @@ __global__ __launch_bounds__(256) void merge_kernel(PlanDev dev, TO *out, float 
   const int first = dev.token_slots[2 * t], cnt = dev.token_slots[2 * t + 1];
   const float *lse_p = dev.part_lse + (int64_t)first * Hq + h;
   const TP *o_p = (const TP *)dev.part_o + ((int64_t)first * Hq + h) * D + 4 * sub;
-  // batches of 8 partials: every load of a batch is issued before it is used
-  float mx = -INFINITY;
-  for (int i0 = 0; i0 < cnt; i0 += 8) {
-    float l8[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) l8[i] = lse_p[(int64_t)min(i0 + i, cnt - 1) * Hq];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) mx = fmaxf(mx, l8[i]);
-  }
-  const float m_use = mx == -INFINITY ? 0.f : mx;
+  float m = -INFINITY, wsum = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  float wsum = 0.f;
-  for (int i0 = 0; i0 < cnt; i0 += 8) {
-    float l8[8];
-    f32x4 o8[8];
+  for (int i0 = 0; i0 < cnt; i0 += B) {
+    float lb[B];
+    f32x4 ob[B];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < B; ++i) {
       const int64_t j = min(i0 + i, cnt - 1);
-      l8[i] = lse_p[j * Hq];
+      lb[i] = lse_p[j * Hq];
       if constexpr (sizeof(TP) == 2) {
         typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
         const f16x4 h4 = *(const f16x4 *)(o_p + j * Hq * D);
-        o8[i] = f32x4{(float)h4[0], (float)h4[1], (float)h4[2], (float)h4[3]};
+        ob[i] = f32x4{(float)h4[0], (float)h4[1], (float)h4[2], (float)h4[3]};
       } else {
-        o8[i] = *(const f32x4 *)(o_p + j * Hq * D);
+        ob[i] = *(const f32x4 *)(o_p + j * Hq * D);
       }
     }
+    float mb = m;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < B; ++i)
+      if (i0 + i < cnt) mb = fmaxf(mb, lb[i]);
+    const float mu = mb == -INFINITY ? 0.f : mb;
+    const float alpha = __builtin_amdgcn_exp2f(m - mu);   // 0 on the first batch (m = -inf)
+    wsum *= alpha;
+    acc *= alpha;
+#pragma unroll
+    for (int i = 0; i < B; ++i) {
       if (i0 + i < cnt) {
-        const float wgt = __builtin_amdgcn_exp2f(l8[i] - m_use);
+        const float wgt = __builtin_amdgcn_exp2f(lb[i] - mu);
         wsum += wgt;
-        acc += wgt * o8[i];
+        acc += wgt * ob[i];
       }
     }
+    m = mb;
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
   TO *dst = out + (int64_t)row * D + 4 * sub;
@@ -927,7 +930,7 @@ __global__ __launch_bounds__(256) void merge_kernel(PlanDev dev, TO *out, float 
   } else {
     *(f32x4 *)dst = acc * inv;
   }
-  if (lse && sub == 0) lse[row] = wsum > 0.f ? (mx + __builtin_amdgcn_logf(wsum)) * kLn2 : -INFINITY;
+  if (lse && sub == 0) lse[row] = wsum > 0.f ? (m + __builtin_amdgcn_logf(wsum)) * kLn2 : -INFINITY;
 }
 
 }  // namespace
