@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--layers", type=int, default=None, help="c4 only: fewer layers (not for reporting)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--warm", action="store_true", help="attention workloads: reuse one input replica")
+    ap.add_argument("--weights", choices=("packed", "torch"), default="packed",
+                    help="c4: projection weights packed once at load (HPD_WEIGHTS_PACKED) or in torch layout")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     return ap.parse_args()
 
@@ -276,7 +278,9 @@ def bench_decode(args, torch, _lib):
     pk = [dev(a) for a in inp.priv_k]
     pv = [dev(a) for a in inp.priv_v]
     step_obj = DecodeStep(inp.num_q_heads, inp.num_kv_heads, inp.prefix_len, inp.branch_page, inp.num_new,
-                          inp.past_len, w, inp.hidden, inp.intermediate, inp.rms_eps)
+                          inp.past_len, w, inp.hidden, inp.intermediate, inp.rms_eps,
+                          packed=args.weights == "packed")
+    del w   # the packed copies are held by step_obj; the torch-layout tensors are not read again
     h_in = torch.from_numpy(inp.hidden_in).cuda()
     h_out = torch.empty_like(h_in)
     stream = torch.cuda.current_stream()
@@ -319,7 +323,8 @@ def bench_decode(args, torch, _lib):
                                "1 layout (k=1) + 32 content (k=4) branches, 4096-token shared prefix",
                    "layers": inp.num_layers, "hidden": H, "intermediate": I, "heads": [Hq, Hkv, D],
                    "branch_tokens": T, "branches": int(len(inp.num_new)), "prefix_len": int(inp.prefix_len[0]),
-                   "private_rows": int((inp.past_len + inp.num_new).sum())},
+                   "private_rows": int((inp.past_len + inp.num_new).sum()),
+                   "weights": args.weights + (" (packed once before timing)" if args.weights == "packed" else "")},
         "roofline": roof, "kernels": kern,
     }
     if not args.no_cpu_baseline:

@@ -176,7 +176,37 @@ typedef struct {
   const void *const *w_down;    /* [L] -> [hidden][intermediate]               */
   const void *const *g_attn_norm; /* [L] -> [hidden] bf16 RMSNorm gain; NULL = ones */
   const void *const *g_mlp_norm;  /* [L] -> [hidden] bf16 RMSNorm gain; NULL = ones */
+  int32_t weight_format;        /* hpd_weight_format; 0 = HPD_WEIGHTS_TORCH      */
 } hpd_model_desc;
+
+/* Layout of the projection weights of an hpd_model_desc.
+ * HPD_WEIGHTS_TORCH: the layouts above (torch Linear, W[out][in], bf16).
+ * HPD_WEIGHTS_PACKED: every projection packed once with hpd_pack_weight
+ *   (w_qkv, w_o, w_down) or hpd_pack_gate_up (w_gate points to the packed
+ *   gate/up pair; w_up is ignored and may be NULL).  The decode step then
+ *   reads each weight tile with whole contiguous 1 KB loads per wave. */
+typedef enum { HPD_WEIGHTS_TORCH = 0, HPD_WEIGHTS_PACKED = 1 } hpd_weight_format;
+
+/* Packed layout of a bf16 matrix W[rows][cols] (rows % 32 == 0, cols % 64
+ * == 0): tiles of 32 rows x 64 columns, 4096 bytes each, ordered by row tile
+ * then column tile; inside a tile, 16-byte piece (j, l) for j = 0..3 and
+ * l = 0..63 sits at byte 1024 j + 16 l and holds row 32 r + l % 32, columns
+ * 64 c + 32 (l / 32) + 8 j .. + 7 of tile (r, c).  The packed matrix has the
+ * same size as W: hpd_packed_weight_bytes(rows, cols) = rows * cols * 2.
+ * w: device [rows][cols] bf16; out: device buffer of that size (not
+ * overlapping w), 16-byte aligned.  Stream-ordered; HPD_ERR_INVALID_ARGUMENT
+ * for NULL pointers or bad sizes, HPD_ERR_HIP if the launch fails. */
+size_t hpd_packed_weight_bytes(int32_t rows, int32_t cols);
+hpd_status hpd_pack_weight(const void *w, int32_t rows, int32_t cols, void *out, void *stream);
+
+/* Packed gate/up pair of a SwiGLU MLP: w_gate, w_up are device
+ * [intermediate][hidden] bf16 (intermediate % 16 == 0, hidden % 64 == 0);
+ * out (hpd_packed_weight_bytes(2 intermediate, hidden) bytes) holds the
+ * packed [2 intermediate][hidden] matrix whose row tile r is gate rows
+ * 16 r .. 16 r + 15 followed by up rows 16 r .. 16 r + 15 (so a row tile
+ * computes 16 gate and their 16 up outputs together). */
+hpd_status hpd_pack_gate_up(const void *w_gate, const void *w_up, int32_t intermediate, int32_t hidden,
+                            void *out, void *stream);
 
 /* Bytes of device workspace hpd_decode_step needs on top of
  * hpd_plan_workspace_bytes (activations of the T tokens and per-token

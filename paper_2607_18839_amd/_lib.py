@@ -67,7 +67,10 @@ class hpd_model_desc(ctypes.Structure):
     _fields_ = [("num_layers", ctypes.c_int32), ("hidden", ctypes.c_int32),
                 ("intermediate", ctypes.c_int32), ("rms_eps", ctypes.c_float),
                 ("w_qkv", PP), ("w_o", PP), ("w_gate", PP), ("w_up", PP), ("w_down", PP),
-                ("g_attn_norm", PP), ("g_mlp_norm", PP)]
+                ("g_attn_norm", PP), ("g_mlp_norm", PP), ("weight_format", ctypes.c_int32)]
+
+
+HPD_WEIGHTS_TORCH, HPD_WEIGHTS_PACKED = 0, 1
 
 
 # Every symbol include/hpd.h declares, with its ctypes signature.
@@ -84,6 +87,11 @@ SIGNATURES = {
     "hpd_decode_step": (ctypes.c_int, [ctypes.POINTER(hpd_model_desc), ctypes.c_void_p, ctypes.c_void_p,
                                        ctypes.c_void_p, PP, PP, PP, PP, ctypes.c_void_p, ctypes.c_size_t,
                                        ctypes.c_void_p]),
+    "hpd_packed_weight_bytes": (ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int32]),
+    "hpd_pack_weight": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                       ctypes.c_void_p]),
+    "hpd_pack_gate_up": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                        ctypes.c_void_p, ctypes.c_void_p]),
     "hpd_kernel_timing": (ctypes.c_int, [ctypes.c_int, ctypes.c_int]),
     "hpd_kernel_times_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int]),
     "hpd_kernel_kind_name": (ctypes.c_char_p, [ctypes.c_int]),
@@ -202,13 +210,25 @@ def _ptr_array(ptrs):
 
 
 def model_desc(num_layers, hidden, intermediate, rms_eps, w_qkv, w_o, w_gate, w_up, w_down,
-               g_attn_norm=None, g_mlp_norm=None):
+               g_attn_norm=None, g_mlp_norm=None, weight_format=HPD_WEIGHTS_TORCH):
     """hpd_model_desc from lists of device pointers; keeps the arrays alive."""
     keep = [_ptr_array(x) for x in (w_qkv, w_o, w_gate, w_up, w_down, g_attn_norm, g_mlp_norm)]
     cast = [None if k is None else ctypes.cast(k, PP) for k in keep]
-    d = hpd_model_desc(num_layers, hidden, intermediate, rms_eps, *cast)
+    d = hpd_model_desc(num_layers, hidden, intermediate, rms_eps, *cast, weight_format)
     d._keep = keep
     return d
+
+
+def hpd_packed_weight_bytes(rows, cols):
+    return int(load().hpd_packed_weight_bytes(rows, cols))
+
+
+def hpd_pack_weight(w, rows, cols, out, stream=None):
+    _check(load().hpd_pack_weight(w, rows, cols, out, stream), "hpd_pack_weight")
+
+
+def hpd_pack_gate_up(w_gate, w_up, intermediate, hidden, out, stream=None):
+    _check(load().hpd_pack_gate_up(w_gate, w_up, intermediate, hidden, out, stream), "hpd_pack_gate_up")
 
 
 def hpd_decode_workspace_bytes(model, plan):

@@ -7,6 +7,7 @@
 #include <new>
 #include <string>
 
+#include "gemm.h"
 #include "hpd.h"
 #include "kernels.h"
 #include "plan.h"
@@ -130,6 +131,37 @@ hpd_status hpd_branch_attn_step(const hpd_plan *plan, const void *q, const void 
   hipError_t e = hpd::launch_branch_attention(P, q, shared_k, shared_v, priv_k, priv_v, out, lse,
                                               workspace, (hipStream_t)stream);
   if (e != hipSuccess) return hip_err(e, "hpd_branch_attn_step");
+  return HPD_OK;
+}
+
+size_t hpd_packed_weight_bytes(int32_t rows, int32_t cols) {
+  if (rows <= 0 || cols <= 0) return 0;
+  return (size_t)rows * (size_t)cols * 2;
+}
+
+hpd_status hpd_pack_weight(const void *w, int32_t rows, int32_t cols, void *out, void *stream) {
+  if (!w || !out) return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_pack_weight: NULL pointer");
+  if (rows <= 0 || cols <= 0 || rows % 32 != 0 || cols % 64 != 0)
+    return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_pack_weight: rows must be a positive multiple of 32, cols of 64");
+  if (!aligned(w, 16) || !aligned(out, 16))
+    return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_pack_weight: pointers must be 16-byte aligned");
+  hipError_t e = hpd::launch_pack_weight((const __bf16 *)w, nullptr, rows, cols, false, (__bf16 *)out,
+                                         (hipStream_t)stream);
+  if (e != hipSuccess) return hip_err(e, "hpd_pack_weight");
+  return HPD_OK;
+}
+
+hpd_status hpd_pack_gate_up(const void *w_gate, const void *w_up, int32_t intermediate, int32_t hidden, void *out,
+                            void *stream) {
+  if (!w_gate || !w_up || !out) return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_pack_gate_up: NULL pointer");
+  if (intermediate <= 0 || hidden <= 0 || intermediate % 16 != 0 || hidden % 64 != 0)
+    return set_err(HPD_ERR_INVALID_ARGUMENT,
+                   "hpd_pack_gate_up: intermediate must be a positive multiple of 16, hidden of 64");
+  if (!aligned(w_gate, 16) || !aligned(w_up, 16) || !aligned(out, 16))
+    return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_pack_gate_up: pointers must be 16-byte aligned");
+  hipError_t e = hpd::launch_pack_weight((const __bf16 *)w_gate, (const __bf16 *)w_up, 2 * intermediate, hidden,
+                                         true, (__bf16 *)out, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_err(e, "hpd_pack_gate_up");
   return HPD_OK;
 }
 

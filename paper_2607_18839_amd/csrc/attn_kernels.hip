@@ -876,7 +876,8 @@ __global__ __launch_bounds__(64) void private_kernel_f32(AttnArgs a) {
 // running max: sum_i 2^(lse_i - m) O_i / sum_i 2^(lse_i - m), partials in
 // slot order.
 template <typename TO, typename TP>
-__global__ __launch_bounds__(256) void merge_kernel(PlanDev dev, TO *out, float *lse, int T, int Hq) {
+__global__ __launch_bounds__(256) void merge_kernel(PlanDev dev, TO *out, float *lse, int T, int Hq,
+                                                    int out_packed) {
   constexpr int B = 16;
   const int row = blockIdx.x * 16 + (threadIdx.x >> 4);
   if (row >= T * Hq) return;
@@ -921,7 +922,8 @@ __global__ __launch_bounds__(256) void merge_kernel(PlanDev dev, TO *out, float 
     m = mb;
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-  TO *dst = out + (int64_t)row * D + 4 * sub;
+  // out is [T][Hq * D], row-major or (16-bit outputs only) packed
+  TO *dst = out + (out_packed ? packed_offset(t, h * D + 4 * sub, Hq * D) : (int64_t)row * D + 4 * sub);
   if constexpr (sizeof(TO) == 2) {
     typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
     bf16x4 r;
@@ -951,7 +953,7 @@ PlanDev plan_dev(const Plan &P, void *workspace) {
 
 hipError_t launch_branch_attention(const Plan &P, const void *q, const void *shared_k,
                                    const void *shared_v, const void *priv_k, const void *priv_v,
-                                   void *out, float *lse, void *workspace, hipStream_t stream) {
+                                   void *out, float *lse, void *workspace, hipStream_t stream, bool out_packed) {
   AttnArgs a;
   a.q = q; a.shared_k = shared_k; a.shared_v = shared_v; a.priv_k = priv_k; a.priv_v = priv_v;
   a.dev = plan_dev(P, workspace);
@@ -976,11 +978,11 @@ hipError_t launch_branch_attention(const Plan &P, const void *q, const void *sha
   const int T = P.T, Hq = P.attn.num_q_heads;
   // bf16 inputs: fp16 partials; fp32 inputs: fp32 partials
   if (P.attn.out_dtype == HPD_BF16) {
-    if (bf16) launch(KK_MERGE, merge_kernel<__bf16, _Float16>, mgrid, mblock, stream, a.dev, (__bf16 *)out, lse, T, Hq);
-    else launch(KK_MERGE, merge_kernel<__bf16, float>, mgrid, mblock, stream, a.dev, (__bf16 *)out, lse, T, Hq);
+    if (bf16) launch(KK_MERGE, merge_kernel<__bf16, _Float16>, mgrid, mblock, stream, a.dev, (__bf16 *)out, lse, T, Hq, out_packed ? 1 : 0);
+    else launch(KK_MERGE, merge_kernel<__bf16, float>, mgrid, mblock, stream, a.dev, (__bf16 *)out, lse, T, Hq, out_packed ? 1 : 0);
   } else {
-    if (bf16) launch(KK_MERGE, merge_kernel<float, _Float16>, mgrid, mblock, stream, a.dev, (float *)out, lse, T, Hq);
-    else launch(KK_MERGE, merge_kernel<float, float>, mgrid, mblock, stream, a.dev, (float *)out, lse, T, Hq);
+    if (bf16) launch(KK_MERGE, merge_kernel<float, _Float16>, mgrid, mblock, stream, a.dev, (float *)out, lse, T, Hq, 0);
+    else launch(KK_MERGE, merge_kernel<float, float>, mgrid, mblock, stream, a.dev, (float *)out, lse, T, Hq, 0);
   }
   return hipGetLastError();
 }

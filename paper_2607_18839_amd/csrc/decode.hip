@@ -18,7 +18,8 @@
 //     sums of squares (not after the last layer)
 // (section "Overview", paragraph "LLM Decoder": GQA, RMSNorm, SwiGLU).
 // Every output element is written by one workgroup, so the result does not
-// depend on scheduling.  Buffers x, q, attn, m and the sums of squares live
+// depend on scheduling.  With HPD_WEIGHTS_PACKED weights the activations x,
+// attn and m are kept in the same packed layout as the weights.  Buffers x, q, attn, m and the sums of squares live
 // in the workspace after the attention plan's tables; rows T..Tpad-1 of x,
 // attn and m are kept zero.
 #include <hip/hip_runtime.h>
@@ -86,12 +87,17 @@ hpd_status validate(const hpd_model_desc *m, const hpd_plan *plan, std::string *
     return HPD_ERR_UNSUPPORTED;
   }
   if (!(m->rms_eps >= 0.f) || m->rms_eps > 1.f) { *err = "rms_eps out of range"; return HPD_ERR_INVALID_ARGUMENT; }
-  if (!m->w_qkv || !m->w_o || !m->w_gate || !m->w_up || !m->w_down) {
+  if (m->weight_format != HPD_WEIGHTS_TORCH && m->weight_format != HPD_WEIGHTS_PACKED) {
+    *err = "unknown weight_format";
+    return HPD_ERR_INVALID_ARGUMENT;
+  }
+  const bool packed = m->weight_format == HPD_WEIGHTS_PACKED;   // w_up unused when packed
+  if (!m->w_qkv || !m->w_o || !m->w_gate || (!packed && !m->w_up) || !m->w_down) {
     *err = "NULL weight array";
     return HPD_ERR_INVALID_ARGUMENT;
   }
   for (int l = 0; l < m->num_layers; ++l) {
-    if (!m->w_qkv[l] || !m->w_o[l] || !m->w_gate[l] || !m->w_up[l] || !m->w_down[l]) {
+    if (!m->w_qkv[l] || !m->w_o[l] || !m->w_gate[l] || (!packed && !m->w_up[l]) || !m->w_down[l]) {
       *err = "NULL weight of layer " + std::to_string(l);
       return HPD_ERR_INVALID_ARGUMENT;
     }
@@ -152,6 +158,9 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
   float *ss = (float *)(ws + L.off_ss);     // sums of squares of h per 32 columns
   const hpd::PlanDev dev = hpd::plan_dev(P, workspace);
   float *h = hidden_out;
+  // packed weights: every activation buffer (x, attn, m) is kept in the packed
+  // layout too, and the projections stream both operands with whole 1 KB loads
+  const bool packed = m.weight_format == HPD_WEIGHTS_PACKED;
   auto gamma = [&](const void *const *arr, int l) { return arr ? (const __bf16 *)arr[l] : nullptr; };
   auto base = [&](int rg, const __bf16 *xin, int N, int K) {
     hpd::GemmArgs g{};
@@ -167,11 +176,13 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
     g.n_ss = L.H / hpd::kGemmTile;
     g.inv_H = 1.0f / (float)L.H;
     g.eps = m.rms_eps;
+    g.a_packed = packed;
+    g.act_packed = packed;
     return g;
   };
 
   hipError_t e = hpd::launch_norm_input(hidden_in, h, L.T, L.Tpad, L.H, gamma(m.g_attn_norm, 0), x, ss, attn,
-                                         L.nq, stream);
+                                         L.nq, packed, stream);
   for (int l = 0; l < m.num_layers && e == hipSuccess; ++l) {
     // 1: QKV projection; the epilogue appends the new K/V rows to the cache
     hpd::GemmArgs g = base(L.rg_qkv, x, L.nq + 2 * L.nkv, L.H);
@@ -186,7 +197,7 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
     if (e != hipSuccess) break;
     // 2: attention over the shared prefix and the private rows
     e = hpd::launch_branch_attention(P, q, shared_k ? shared_k[l] : nullptr, shared_v ? shared_v[l] : nullptr,
-                                     priv_k[l], priv_v[l], attn, nullptr, workspace, stream);
+                                     priv_k[l], priv_v[l], attn, nullptr, workspace, stream, packed);
     if (e != hipSuccess) break;
     // 3: O projection into h; MLP norm input (fp16)
     g = base(L.rg_o, attn, L.H, L.nq);
@@ -200,8 +211,8 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
     if (e != hipSuccess) break;
     // 4: gate/up projection, SwiGLU (fp16)
     g = base(L.rg_gu, x, 2 * L.I, L.H);
-    g.w0 = (const __bf16 *)m.w_gate[l];
-    g.w1 = (const __bf16 *)m.w_up[l];
+    g.w0 = (const __bf16 *)m.w_gate[l];   // packed: the interleaved gate/up pair
+    g.w1 = packed ? nullptr : (const __bf16 *)m.w_up[l];
     g.m_out = mlp;
     g.I = L.I;
     e = hpd::launch_gemm(g, true, hpd::kEpiSwiGLU, hpd::KK_GEMM_GATE_UP, stream);

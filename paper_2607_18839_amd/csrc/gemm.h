@@ -47,12 +47,22 @@ struct GemmArgs {
   __bf16 *x_out; bool x_out_f16;            // [Tpad][N]; rows < T written
   const __bf16 *gamma;                      // [N] bf16, NULL = ones
   float *ss_out;                            // [Tpad][N / 32]
+  // layouts: a_packed: w0 is packed (packed_offset; SwiGLU: the interleaved
+  // gate/up pair, w1 unused); act_packed: x, x_out and m_out are packed.
+  // a_packed requires act_packed; row-major weights require row-major
+  // activations.
+  bool a_packed, act_packed;
 };
 
 // Start of a step: h = h_in (if different), x = h * gamma, ss, and zero rows
 // T..Tpad-1 of x and of `zero_rows` ([Tpad][zero_cols]).
 hipError_t launch_norm_input(const float *h_in, float *h, int T, int Tpad, int H, const __bf16 *gamma,
-                             __bf16 *x, float *ss, __bf16 *zero_rows, int zero_cols, hipStream_t stream);
+                             __bf16 *x, float *ss, __bf16 *zero_rows, int zero_cols, bool packed,
+                             hipStream_t stream);
+// W[rows][cols] -> packed layout (gate_up: interleave w (gate) and w2 (up),
+// each [rows / 2][cols]).
+hipError_t launch_pack_weight(const __bf16 *w, const __bf16 *w2, int rows, int cols, bool gate_up, __bf16 *out,
+                              hipStream_t stream);
 // f16: fp16 GEMM (bf16 weights converted to fp16 in registers, fp16
 // activations); epi: kEpi*.
 hipError_t launch_gemm(const GemmArgs &g, bool f16, int epi, int kind, hipStream_t stream);

@@ -30,6 +30,7 @@
 
 #include <algorithm>
 #include <cstdint>
+#include <type_traits>
 
 #include "gemm.h"
 
@@ -56,6 +57,109 @@ __device__ __forceinline__ u32x4 bf16x8_to_f16x8(u32x4 v) {
     r[i] = (unsigned)__builtin_bit_cast(unsigned short, l16) | ((unsigned)__builtin_bit_cast(unsigned short, h16) << 16);
   }
   return r;
+}
+
+// Epilogue operands, loaded before a GEMM's main loop (no later step needs
+// them sooner, and the loop's waits retire them): the per-token sums of
+// squares (QKV, SwiGLU; up to 32 partials) or the residual row slice.
+template <int EPI>
+__device__ __forceinline__ void prefetch_epilogue(const GemmArgs &g, int t, int tile, int half, f32x4 (&pre)[8]) {
+  if constexpr (EPI == kEpiResidual) {
+    const float *hr = g.h + (int64_t)min(t, g.T - 1) * g.N + tile * kGemmTile + 4 * half;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pre[i] = *(const f32x4 *)(hr + 8 * i);
+  } else {
+    const float *sr = g.ss_in + (int64_t)t * g.n_ss;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) pre[i] = *(const f32x4 *)(sr + 4 * min(i, g.n_ss / 4 - 1));
+  }
+}
+
+// Writes the finished 32 x 32 tile `tile` for token t (this lane: rows
+// 8 (r / 4) + 4 half + r % 4 of the tile, see below) through epilogue EPI.
+template <int EPI>
+__device__ __forceinline__ void epilogue(const GemmArgs &g, const f32x16 &acc, f32x4 (&pre)[8], int t, int tile,
+                                         int half) {
+  if constexpr (EPI == kEpiResidual) {
+    // h += Y; x_out = h * gamma (the next norm's input, unnormalised) and the
+    // sum of squares of h over this 32-column tile
+    if (t >= g.T) return;
+    float *hr = g.h + (int64_t)t * g.N + tile * kGemmTile + 4 * half;
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        pre[i][r] += acc[4 * i + r];
+        ss = fmaf(pre[i][r], pre[i][r], ss);
+      }
+      *(f32x4 *)(hr + 8 * i) = pre[i];
+    }
+    if (!g.x_out) return;
+    ss += __shfl_xor(ss, 32);
+    if (half == 0) g.ss_out[(int64_t)t * (g.N / kGemmTile) + tile] = ss;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int n = tile * kGemmTile + 8 * i + 4 * half;
+      f32x4 v = pre[i];
+      if (g.gamma)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] *= (float)g.gamma[n + r];
+      const int64_t off = g.act_packed ? packed_offset(t, n, g.N) : (int64_t)t * g.N + n;
+      if (g.x_out_f16) {
+        f16x4 o;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[r] = (_Float16)v[r];
+        *(f16x4 *)((_Float16 *)g.x_out + off) = o;
+      } else {
+        bf16x4 o;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[r] = (__bf16)v[r];
+        *(bf16x4 *)(g.x_out + off) = o;
+      }
+    }
+  } else {
+    // per-token RMSNorm factor from the partial sums of squares
+    float sum = 0.f;
+    if (g.n_ss <= 32) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if (4 * i < g.n_ss) sum += (pre[i][0] + pre[i][1]) + (pre[i][2] + pre[i][3]);
+    } else {
+      const float *sr = g.ss_in + (int64_t)t * g.n_ss;
+      for (int i = 0; i < g.n_ss; i += 4) {
+        const f32x4 v = *(const f32x4 *)(sr + i);
+        sum += (v[0] + v[1]) + (v[2] + v[3]);
+      }
+    }
+    const float inv_rms = 1.0f / sqrtf(sum * g.inv_H + g.eps);
+    if constexpr (EPI == kEpiQKV) {
+      if (t >= g.T) return;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int n = tile * kGemmTile + 8 * i + 4 * half;   // 4-runs never straddle q / k / v
+        bf16x4 v;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = (__bf16)(acc[4 * i + r] * inv_rms);
+        if (n < g.n_q) *(bf16x4 *)(g.q_out + (int64_t)t * g.n_q + n) = v;
+        else if (n < g.n_q + g.n_kv) *(bf16x4 *)(g.k_cache + (int64_t)g.dest[t] * g.n_kv + (n - g.n_q)) = v;
+        else *(bf16x4 *)(g.v_cache + (int64_t)g.dest[t] * g.n_kv + (n - g.n_q - g.n_kv)) = v;
+      }
+    } else {   // SwiGLU: m = silu(gate) * up, fp16; rows t >= T are written as zeros
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        f16x4 mv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float gt = acc[4 * i + r] * inv_rms, up = acc[4 * i + 8 + r] * inv_rms;
+          mv[r] = (_Float16)(t < g.T ? gt / (1.0f + __expf(-gt)) * up : 0.f);
+        }
+        const int col = tile * 16 + 8 * i + 4 * half;
+        const int64_t off = g.act_packed ? packed_offset(t, col, g.I) : (int64_t)t * g.I + col;
+        *(f16x4 *)((_Float16 *)g.m_out + off) = mv;
+      }
+    }
+  }
 }
 
 // LDS rows are 128 bytes (64 K values); 16-byte piece q of row r is stored at
@@ -124,19 +228,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   const int t = tt * kGemmTile + frow;   // this lane's token in the epilogue
   const int tile = slice * RG + rg;      // 32-row tile of the output columns
 
-  // Epilogue operands, loaded before the main loop (no later step needs them
-  // sooner, and the loop's waits retire them): the per-token sums of squares
-  // (QKV, SwiGLU; up to 32 partials) or the residual row slice (residual).
   f32x4 pre[8];
-  if constexpr (EPI == kEpiResidual) {
-    const float *hr = g.h + (int64_t)min(t, g.T - 1) * g.N + tile * kGemmTile + 4 * half;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) pre[i] = *(const f32x4 *)(hr + 8 * i);
-  } else {
-    const float *sr = g.ss_in + (int64_t)t * g.n_ss;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) pre[i] = *(const f32x4 *)(sr + 4 * min(i, g.n_ss / 4 - 1));
-  }
+  prefetch_epilogue<EPI>(g, t, tile, half, pre);
 
   // copy sources: instruction q of the K group covers tile q / 4 (row group
   // q / 4 < RG, else the token tile), rows 8 (q % 4) + lane / 8
@@ -228,97 +321,169 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
       for (int r = 0; r < 16; ++r) acc[r] += red[((k * RG + rg) * 16 + r) * 64 + lane];
   }
 
-  if constexpr (EPI == kEpiResidual) {
-    // h += Y; x_out = h * gamma (the next norm's input, unnormalised) and the
-    // sum of squares of h over this 32-column tile
-    if (t >= g.T) return;
-    float *hr = g.h + (int64_t)t * g.N + tile * kGemmTile + 4 * half;
-    float ss = 0.f;
+  epilogue<EPI>(g, acc, pre, t, tile, half);
+}
+
+// The same projection with both operands in the packed layout (packed_offset:
+// weights packed once by hpd_pack_weight / hpd_pack_gate_up, activations
+// written packed by their producers).  A wave's fragments for one step are
+// then 4 whole contiguous 1 KB pieces per operand, loaded straight into a
+// register ring of kPackedRing steps (3 ahead of the MFMAs); no LDS is used
+// until the K groups are added.
+constexpr int kPackedRing = 4;
+
+template <int RG, bool F16, int EPI>
+__global__ __launch_bounds__(256) void gemm_packed_kernel(GemmArgs g) {
+  constexpr int KG = 4 / RG, S = kPackedRing;
+  const int nwg = g.n_slices * g.n_ttiles;
+  const int per_xcd = gridDim.x / 8;
+  const int logical = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;   // XCD-aware, as gemm_kernel
+  if (logical >= nwg) return;
+  const int tt = logical % g.n_ttiles, slice = logical / g.n_ttiles;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int rg = wave % RG, kgi = wave / RG;
+  const int frow = lane & 31, half = lane >> 5;
+  const int t = tt * kGemmTile + frow;
+  const int tile = slice * RG + rg;
+  const int ksteps = g.K / kGemmKStep, nsteps = ksteps / KG, ks0 = kgi * nsteps;
+
+  f32x4 pre[8];
+  prefetch_epilogue<EPI>(g, t, tile, half, pre);
+
+  const __bf16 *arow = g.w0 + ((int64_t)tile * ksteps + ks0) * 2048 + lane * 8;
+  const __bf16 *brow = g.x + ((int64_t)tt * ksteps + ks0) * 2048 + lane * 8;
+  u32x4 a[S][4], b[S][4];   // step c lives in slot c % S
+  // The scheduling barriers keep each step's loads where they are issued (the
+  // scheduler would otherwise sink them next to their MFMAs, emptying the ring).
+  auto load = [&](int step, int slot) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int j = 0; j < 4; ++j) a[slot][j] = *(const u32x4 *)(arow + (int64_t)step * 2048 + 512 * j);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        pre[i][r] += acc[4 * i + r];
-        ss = fmaf(pre[i][r], pre[i][r], ss);
-      }
-      *(f32x4 *)(hr + 8 * i) = pre[i];
+    for (int j = 0; j < 4; ++j) b[slot][j] = *(const u32x4 *)(brow + (int64_t)step * 2048 + 512 * j);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  f32x16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  auto compute = [&](int slot) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if constexpr (F16)
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, bf16x8_to_f16x8(a[slot][j])),
+                                                     __builtin_bit_cast(f16x8, b[slot][j]), acc, 0, 0, 0);
+      else
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[slot][j]),
+                                                      __builtin_bit_cast(bf16x8, b[slot][j]), acc, 0, 0, 0);
     }
-    if (!g.x_out) return;
-    ss += __shfl_xor(ss, 32);
-    if (half == 0) g.ss_out[(int64_t)t * (g.N / kGemmTile) + tile] = ss;
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // Steps 0..S-2 are loaded up front; step c + S - 1 goes into the slot freed
+  // by step c - 1 just before step c computes.  The main loop takes whole
+  // groups of S steps whose loads are all in range; the remaining REM steps
+  // (at most 2 S - 2; all of them when nsteps < 2 S - 1) run as a straight-
+  // line tail specialised on REM.  No load sits under a runtime condition, so
+  // the compiler waits for exactly the slot being consumed.
+  auto tail = [&](int base, auto rem) {
+    constexpr int REM = decltype(rem)::value;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int n = tile * kGemmTile + 8 * i + 4 * half;
-      f32x4 v = pre[i];
-      if (g.gamma)
+    for (int u = 0; u < REM; ++u) {
+      if (u + S - 1 < REM) load(base + u + S - 1, (u + S - 1) % S);
+      compute(u % S);
+    }
+  };
+  auto prologue = [&](auto n) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] *= (float)g.gamma[n + r];
-      if (g.x_out_f16) {
-        f16x4 o;
+    for (int u = 0; u < decltype(n)::value; ++u) load(u, u);
+  };
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  using I4 = std::integral_constant<int, 4>;
+  using I5 = std::integral_constant<int, 5>;
+  using I6 = std::integral_constant<int, 6>;
+  static_assert(S == 4, "the tail cases below cover REM = 1 .. 2 S - 2");
+  if (nsteps >= 2 * S - 1) {
+    prologue(I3{});
+    const int n_main = (nsteps - (2 * S - 1)) / S + 1;
+    for (int gi = 0; gi < n_main; ++gi) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) o[r] = (_Float16)v[r];
-        *(f16x4 *)((_Float16 *)g.x_out + (int64_t)t * g.N + n) = o;
-      } else {
-        bf16x4 o;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) o[r] = (__bf16)v[r];
-        *(bf16x4 *)(g.x_out + (int64_t)t * g.N + n) = o;
+      for (int u = 0; u < S; ++u) {
+        load(gi * S + u + S - 1, (u + S - 1) % S);
+        compute(u);
       }
     }
-    return;
+    const int base = n_main * S;
+    switch (nsteps - base) {   // S - 1 .. 2 S - 2
+      case 3: tail(base, I3{}); break;
+      case 4: tail(base, I4{}); break;
+      case 5: tail(base, I5{}); break;
+      default: tail(base, I6{}); break;
+    }
   } else {
-    // per-token RMSNorm factor from the partial sums of squares
-    float sum = 0.f;
-    if (g.n_ss <= 32) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        if (4 * i < g.n_ss) sum += (pre[i][0] + pre[i][1]) + (pre[i][2] + pre[i][3]);
-    } else {
-      const float *sr = g.ss_in + (int64_t)t * g.n_ss;
-      for (int i = 0; i < g.n_ss; i += 4) {
-        const f32x4 v = *(const f32x4 *)(sr + i);
-        sum += (v[0] + v[1]) + (v[2] + v[3]);
-      }
-    }
-    const float inv_rms = 1.0f / sqrtf(sum * g.inv_H + g.eps);
-    if constexpr (EPI == kEpiQKV) {
-      if (t >= g.T) return;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int n = tile * kGemmTile + 8 * i + 4 * half;   // 4-runs never straddle q / k / v
-        bf16x4 v;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = (__bf16)(acc[4 * i + r] * inv_rms);
-        if (n < g.n_q) *(bf16x4 *)(g.q_out + (int64_t)t * g.n_q + n) = v;
-        else if (n < g.n_q + g.n_kv) *(bf16x4 *)(g.k_cache + (int64_t)g.dest[t] * g.n_kv + (n - g.n_q)) = v;
-        else *(bf16x4 *)(g.v_cache + (int64_t)g.dest[t] * g.n_kv + (n - g.n_q - g.n_kv)) = v;
-      }
-    } else {   // SwiGLU: m = silu(gate) * up, fp16; rows t >= T are written as zeros
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        f16x4 mv;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float gt = acc[4 * i + r] * inv_rms, up = acc[4 * i + 8 + r] * inv_rms;
-          mv[r] = (_Float16)(t < g.T ? gt / (1.0f + __expf(-gt)) * up : 0.f);
-        }
-        *(f16x4 *)((_Float16 *)g.m_out + (int64_t)t * g.I + tile * 16 + 8 * i + 4 * half) = mv;
-      }
+    switch (nsteps) {   // 1 .. 2 S - 2
+      case 1: prologue(I1{}); tail(0, I1{}); break;
+      case 2: prologue(I2{}); tail(0, I2{}); break;
+      case 3: prologue(I3{}); tail(0, I3{}); break;
+      case 4: prologue(I3{}); tail(0, I4{}); break;
+      case 5: prologue(I3{}); tail(0, I5{}); break;
+      default: prologue(I3{}); tail(0, I6{}); break;
     }
   }
+
+  if constexpr (KG > 1) {
+    // K groups 1.. hand their tiles to K group 0, which adds them in order
+    __shared__ float red[(KG - 1) * RG * 16 * 64];
+    if (kgi > 0) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) red[(((kgi - 1) * RG + rg) * 16 + r) * 64 + lane] = acc[r];
+    }
+    __syncthreads();
+    if (kgi > 0) return;
+#pragma unroll
+    for (int k = 0; k < KG - 1; ++k)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[r] += red[((k * RG + rg) * 16 + r) * 64 + lane];
+  }
+  epilogue<EPI>(g, acc, pre, t, tile, half);
+}
+
+// Packs W[rows][cols] (bf16) into the packed layout: one thread per 16-byte
+// piece of the output.  gate_up: rows are the pair's interleaved rows (row tile
+// r = gate rows 16 r .. 16 r + 15, then up rows 16 r .. 16 r + 15) read from
+// w (gate) and w2 (up), each [rows / 2][cols].
+__global__ __launch_bounds__(256) void pack_weight_kernel(const __bf16 *w, const __bf16 *w2, int rows, int cols,
+                                                          int gate_up, __bf16 *out) {
+  const int64_t piece = (int64_t)blockIdx.x * 256 + threadIdx.x;   // 8 elements each
+  if (piece * 8 >= (int64_t)rows * cols) return;
+  const int64_t tile_id = piece / 256;
+  const int in_tile = (int)(piece % 256), j = in_tile / 64, l = in_tile % 64;
+  const int ctiles = cols / 64;
+  const int r = (int)(tile_id / ctiles) * 32 + (l & 31);
+  const int c = (int)(tile_id % ctiles) * 64 + 32 * (l >> 5) + 8 * j;
+  const __bf16 *src;
+  if (gate_up) {
+    const int src_row = (r >> 5) * 16 + (r & 15);
+    src = ((r & 31) < 16 ? w : w2) + (int64_t)src_row * cols + c;
+  } else {
+    src = w + (int64_t)r * cols + c;
+  }
+  *(u32x4 *)(out + piece * 8) = *(const u32x4 *)src;
 }
 
 // Start of a step: h = h_in, x = h * gamma (bf16), sums of squares of h over
-// 32-column tiles; rows T..Tpad-1 of x and zero_rows are zeroed.  One
-// workgroup per row; H is a multiple of 128.
+// 32-column tiles; rows T..Tpad-1 of x and zero_rows are zeroed.  x and
+// zero_rows are row-major or, if packed, in the packed layout.  One workgroup
+// per row; H and zero_cols are multiples of 128.
 __global__ __launch_bounds__(256) void norm_input_kernel(const float *h_in, float *h, int T, int H,
                                                          const __bf16 *gamma, __bf16 *x, float *ss,
-                                                         __bf16 *zero_rows, int zero_cols) {
+                                                         __bf16 *zero_rows, int zero_cols, int packed) {
   const int t = blockIdx.x, tid = threadIdx.x;
+  auto at = [&](int c, int cols) { return packed ? packed_offset(t, c, cols) : (int64_t)t * cols + c; };
   if (t >= T) {
-    for (int c = tid; c < H; c += 256) x[(int64_t)t * H + c] = (__bf16)0.f;
+    const bf16x4 z = {(__bf16)0.f, (__bf16)0.f, (__bf16)0.f, (__bf16)0.f};   // 0 in bf16 and fp16
+    for (int c = 4 * tid; c < H; c += 1024) *(bf16x4 *)(x + at(c, H)) = z;
     if (zero_rows)
-      for (int c = tid; c < zero_cols; c += 256) zero_rows[(int64_t)t * zero_cols + c] = (__bf16)0.f;
+      for (int c = 4 * tid; c < zero_cols; c += 1024) *(bf16x4 *)(zero_rows + at(c, zero_cols)) = z;
     return;
   }
   for (int c = 4 * tid; c < H; c += 1024) {
@@ -333,16 +498,18 @@ __global__ __launch_bounds__(256) void norm_input_kernel(const float *h_in, floa
     bf16x4 o;
 #pragma unroll
     for (int r = 0; r < 4; ++r) o[r] = (__bf16)(v[r] * (gamma ? (float)gamma[c + r] : 1.f));
-    *(bf16x4 *)(x + (int64_t)t * H + c) = o;
+    *(bf16x4 *)(x + at(c, H)) = o;
   }
 }
 
 }  // namespace
 
 hipError_t launch_norm_input(const float *h_in, float *h, int T, int Tpad, int H, const __bf16 *gamma,
-                             __bf16 *x, float *ss, __bf16 *zero_rows, int zero_cols, hipStream_t stream) {
-  if (H % 128 != 0 || T < 1 || Tpad < T) return hipErrorInvalidValue;
-  launch(KK_NORM, norm_input_kernel, dim3(Tpad), dim3(256), stream, h_in, h, T, H, gamma, x, ss, zero_rows, zero_cols);
+                             __bf16 *x, float *ss, __bf16 *zero_rows, int zero_cols, bool packed,
+                             hipStream_t stream) {
+  if (H % 128 != 0 || zero_cols % 128 != 0 || T < 1 || Tpad < T || Tpad % kGemmTile != 0) return hipErrorInvalidValue;
+  launch(KK_NORM, norm_input_kernel, dim3(Tpad), dim3(256), stream, h_in, h, T, H, gamma, x, ss, zero_rows, zero_cols,
+         packed ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -355,7 +522,24 @@ void launch_epi(const GemmArgs &g, int kind, dim3 grid, hipStream_t stream) {
   else launch(kind, gemm_kernel<1, F16, EPI>, grid, dim3(256), stream, g);
 }
 
+template <bool F16, int EPI>
+void launch_packed(const GemmArgs &g, int kind, dim3 grid, hipStream_t stream) {
+  if (g.rg == 4) launch(kind, gemm_packed_kernel<4, F16, EPI>, grid, dim3(256), stream, g);
+  else if (g.rg == 2) launch(kind, gemm_packed_kernel<2, F16, EPI>, grid, dim3(256), stream, g);
+  else launch(kind, gemm_packed_kernel<1, F16, EPI>, grid, dim3(256), stream, g);
+}
+
 }  // namespace
+
+hipError_t launch_pack_weight(const __bf16 *w, const __bf16 *w2, int rows, int cols, bool gate_up, __bf16 *out,
+                              hipStream_t stream) {
+  if (!w || !out || (gate_up && !w2) || rows <= 0 || cols <= 0 || rows % kGemmTile != 0 || cols % kGemmKStep != 0)
+    return hipErrorInvalidValue;
+  const int64_t pieces = (int64_t)rows * cols / 8;
+  hipLaunchKernelGGL(pack_weight_kernel, dim3((unsigned)((pieces + 255) / 256)), dim3(256), 0, stream, w, w2, rows,
+                     cols, gate_up ? 1 : 0, out);
+  return hipGetLastError();
+}
 
 hipError_t launch_gemm(const GemmArgs &g, bool f16, int epi, int kind, hipStream_t stream) {
   const int kg = g.rg == 4 ? 1 : g.rg == 2 ? 2 : g.rg == 1 ? 4 : 0;
@@ -367,6 +551,15 @@ hipError_t launch_gemm(const GemmArgs &g, bool f16, int epi, int kind, hipStream
     return hipErrorInvalidValue;
   const int nwg = g.n_slices * g.n_ttiles;
   const dim3 grid((nwg + 7) / 8 * 8);
+  if (g.a_packed) {
+    if (!g.act_packed) return hipErrorInvalidValue;
+    if (epi == kEpiSwiGLU) launch_packed<true, kEpiSwiGLU>(g, kind, grid, stream);
+    else if (epi == kEpiQKV) launch_packed<false, kEpiQKV>(g, kind, grid, stream);
+    else if (f16) launch_packed<true, kEpiResidual>(g, kind, grid, stream);
+    else launch_packed<false, kEpiResidual>(g, kind, grid, stream);
+    return hipGetLastError();
+  }
+  if (g.act_packed) return hipErrorInvalidValue;   // the LDS-ring kernel reads row-major activations
   if (epi == kEpiSwiGLU) launch_epi<true, kEpiSwiGLU>(g, kind, grid, stream);
   else if (epi == kEpiQKV) launch_epi<false, kEpiQKV>(g, kind, grid, stream);
   else if (f16) launch_epi<true, kEpiResidual>(g, kind, grid, stream);

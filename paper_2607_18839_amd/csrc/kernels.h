@@ -25,6 +25,16 @@ PlanDev plan_dev(const Plan &P, void *workspace);
 // Kernel kinds of the optional benchmark timing (hpd_kernel_timing).
 enum KernelKind { KK_SHARED = 0, KK_PRIVATE, KK_MERGE, KK_GEMM_QKV, KK_GEMM_O, KK_GEMM_GATE_UP,
                   KK_GEMM_DOWN, KK_NORM };
+// Element offset of (row, col) of a [rows][cols] 16-bit matrix in the packed
+// layout (tiles of 32 rows x 64 columns, 2048 elements each, ordered by row
+// tile then column tile; inside a tile, element e of 16-byte piece (j, l) is
+// row l % 32, column 32 (l / 32) + 8 j + e).  Four consecutive columns
+// starting at a multiple of 4 are contiguous.  cols % 64 == 0.
+__device__ __forceinline__ int64_t packed_offset(int row, int col, int cols) {
+  const int kk = col & 63, l = 32 * (kk >> 5) + (row & 31), j = (kk & 31) >> 3;
+  return ((int64_t)(row >> 5) * (cols >> 6) + (col >> 6)) * 2048 + j * 512 + l * 8 + (kk & 7);
+}
+
 // Per-kernel timing (benchmark support).  When timing is on, timed_events
 // hands out a pool pair for a launch of `kind` (else two nulls); launch()
 // then binds the pair to the kernel's own dispatch (start and end of its
@@ -41,10 +51,13 @@ void launch(int kind, void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream
   else hipLaunchKernelGGL(kernel, grid, block, 0, stream, args...);
 }
 
-// One attention layer: shared-prefix kernel, private kernel, merge kernel.
-// q/k/v in P.attn.dtype; out in P.attn.out_dtype; lse may be NULL.
+// One attention layer: the shared-prefix and private work (one launch for
+// bf16, two for fp32), then the merge.  q/k/v in P.attn.dtype; out in
+// P.attn.out_dtype, [T][Hq * 64], row-major or (out_packed, bf16 only) in
+// the packed layout; lse may be NULL.
 hipError_t launch_branch_attention(const Plan &P, const void *q, const void *shared_k,
                                    const void *shared_v, const void *priv_k, const void *priv_v,
-                                   void *out, float *lse, void *workspace, hipStream_t stream);
+                                   void *out, float *lse, void *workspace, hipStream_t stream,
+                                   bool out_packed = false);
 
 }  // namespace hpd

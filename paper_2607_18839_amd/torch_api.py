@@ -56,28 +56,55 @@ class BranchAttention:
         return out
 
 
+def pack_weight(w, stream=None):
+    """Packed copy (hpd_pack_weight) of a bf16 [rows][cols] device tensor."""
+    rows, cols = w.shape
+    out = torch.empty_like(w)
+    _lib.hpd_pack_weight(w.data_ptr(), rows, cols, out.data_ptr(), _stream(stream))
+    return out
+
+
+def pack_gate_up(w_gate, w_up, stream=None):
+    """Packed gate/up pair (hpd_pack_gate_up) of two bf16 [I][hidden] tensors."""
+    inter, hidden = w_gate.shape
+    out = torch.empty((2 * inter, hidden), dtype=w_gate.dtype, device=w_gate.device)
+    _lib.hpd_pack_gate_up(w_gate.data_ptr(), w_up.data_ptr(), inter, hidden, out.data_ptr(), _stream(stream))
+    return out
+
+
 class DecodeStep:
     """One decode step of the decoder stack for a fixed batch shape.
 
     ``weights`` maps 'w_qkv', 'w_o', 'w_gate', 'w_up', 'w_down' (and
     optionally 'g_attn_norm', 'g_mlp_norm') to lists of per-layer bf16 device
     tensors in torch Linear layout.  The tensors must stay alive while the
-    step is used.
+    step is used.  packed=True packs the projection weights once here
+    (HPD_WEIGHTS_PACKED, a device copy of the weights) and the step reads
+    the packed copies.
     """
 
     def __init__(self, num_q_heads, num_kv_heads, prefix_len, branch_page, num_new, past_len,
                  weights, hidden, intermediate, rms_eps=1e-6, prefix_row=None, priv_row=None,
-                 device="cuda", stream=None):
+                 device="cuda", stream=None, packed=False):
         self.attn = BranchAttention(num_q_heads, num_kv_heads, prefix_len, branch_page, num_new, past_len,
                                     dtype=torch.bfloat16, prefix_row=prefix_row, priv_row=priv_row,
                                     device=device, stream=stream)
         self.T = self.attn.T
         self.hidden = hidden
         self.num_layers = len(weights["w_qkv"])
+        fmt = _lib.HPD_WEIGHTS_TORCH
+        if packed:
+            weights = dict(weights)
+            weights["w_gate"] = [pack_gate_up(g, u, stream) for g, u in zip(weights["w_gate"], weights["w_up"])]
+            weights["w_up"] = weights["w_gate"]   # ignored by the packed format
+            for k in ("w_qkv", "w_o", "w_down"):
+                weights[k] = [pack_weight(w, stream) for w in weights[k]]
+            fmt = _lib.HPD_WEIGHTS_PACKED
+        self._weights = weights   # keeps packed copies alive
         ptrs = {k: [t.data_ptr() for t in v] for k, v in weights.items()}
         self.model = _lib.model_desc(self.num_layers, hidden, intermediate, rms_eps, ptrs["w_qkv"], ptrs["w_o"],
                                      ptrs["w_gate"], ptrs["w_up"], ptrs["w_down"], ptrs.get("g_attn_norm"),
-                                     ptrs.get("g_mlp_norm"))
+                                     ptrs.get("g_mlp_norm"), weight_format=fmt)
         self.plan_bytes = self.attn.ws_bytes
         self.ws_bytes = self.plan_bytes + _lib.hpd_decode_workspace_bytes(self.model, self.attn.plan)
         # one workspace holding the plan tables (uploaded) and the step's scratch

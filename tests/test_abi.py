@@ -148,3 +148,31 @@ def test_custom_row_offsets_are_kept():
     assert np.array_equal(info["prefix_row"], pr) and np.array_equal(info["priv_row"], vr)
     assert info["shared_rows"] == max(pr + st["prefix_len"])
     assert info["priv_rows"] == max(vr + st["past_len"] + st["num_new"])
+
+
+def test_pack_entry_points_validate_before_launching(lib):
+    assert _lib.hpd_packed_weight_bytes(32, 64) == 4096
+    assert _lib.hpd_packed_weight_bytes(8960, 1536) == 8960 * 1536 * 2
+    assert _lib.hpd_packed_weight_bytes(0, 64) == 0
+    fake = ctypes.c_void_p(4096)
+    assert lib.hpd_pack_weight(None, 32, 64, fake, None) == 1
+    assert lib.hpd_pack_weight(fake, 48, 64, fake, None) == 1          # rows % 32
+    assert lib.hpd_pack_weight(fake, 32, 96, fake, None) == 1          # cols % 64
+    assert lib.hpd_pack_weight(ctypes.c_void_p(4098), 32, 64, fake, None) == 1   # alignment
+    assert b"16-byte" in lib.hpd_last_error_message()
+    assert lib.hpd_pack_gate_up(fake, None, 16, 64, fake, None) == 1
+    assert lib.hpd_pack_gate_up(fake, fake, 24, 64, fake, None) == 1   # intermediate % 16
+    assert b"intermediate" in lib.hpd_last_error_message()
+
+
+def test_decode_step_checks_weight_format():
+    st = tiny_structures()[1]
+    plan = _plan(st, 4, 2)
+    fake = 4096
+    one = [fake]
+    for fmt, w_up, status, needle in ((7, one, 1, "weight_format"), (0, [None], 1, "NULL weight"),
+                                      (1, [None], 3, "workspace too small")):
+        model = _lib.model_desc(1, 256, 384, 1e-6, one, one, one, w_up, one, weight_format=fmt)
+        with pytest.raises(_lib.HpdError) as e:
+            _lib.hpd_decode_step(model, plan, fake, fake, one, one, one, one, 4096, 0)
+        assert e.value.status == status and needle in str(e.value), str(e.value)

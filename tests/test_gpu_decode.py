@@ -19,12 +19,12 @@ def _need_gpu():
         pytest.skip("no GPU")
 
 
-def run_decode(inp, canary=True):
+def run_decode(inp, canary=True, packed=False):
     """Runs hpd_decode_step on the inputs; returns (h_out, priv_k list, priv_v list) as numpy."""
     from paper_2607_18839_amd.torch_api import DecodeStep
     w = {k: [to_dev(a, "bf16") for a in getattr(inp, k)] for k in ("w_qkv", "w_o", "w_gate", "w_up", "w_down")}
     step = DecodeStep(inp.num_q_heads, inp.num_kv_heads, inp.prefix_len, inp.branch_page, inp.num_new,
-                      inp.past_len, w, inp.hidden, inp.intermediate, inp.rms_eps)
+                      inp.past_len, w, inp.hidden, inp.intermediate, inp.rms_eps, packed=packed)
     sk = [to_dev(a, "bf16") for a in inp.shared_k]
     sv = [to_dev(a, "bf16") for a in inp.shared_v]
     pk_np = [a.copy() for a in inp.priv_k]
@@ -67,11 +67,12 @@ def _check_cache(inp, pk, pv, nk, nv):
             assert mx <= BF16_MAX_ABS * 5 and rl <= BF16_REL_L2, f"layer {l} cache rows: {mx:.3e} {rl:.3e}"
 
 
+@pytest.mark.parametrize("packed", [False, True], ids=["torch", "packed"])
 @pytest.mark.parametrize("seed", [0, 1, 2])
-def test_small_stack(seed):
-    announce(f"decode small seed {seed}")
+def test_small_stack(seed, packed):
+    announce(f"decode small seed {seed} packed {packed}")
     inp = small_inputs(seed)
-    h, pk, pv = run_decode(inp)
+    h, pk, pv = run_decode(inp, packed=packed)
     ref, nk, nv = decode_step(inp)
     mx, rl = errors(h, ref)
     print(f"small stack seed {seed}: max abs {mx:.3e} rel L2 {rl:.3e}")
@@ -99,13 +100,15 @@ def _sub_batch(inp, branches):
     return sub, tok
 
 
-def test_full_c4_sampled_branches():
-    """c4 at full size (18 layers, 33 branches, 4096-token prefix) in the
-    configuration the benchmark times; the oracle recomputes 3 sampled
-    branches (layout, the longest and one more content branch) on their own."""
-    announce("decode c4 full, sampled branches")
+@pytest.mark.parametrize("packed", [False, True], ids=["torch", "packed"])
+def test_full_c4_sampled_branches(packed):
+    """c4 at full size (18 layers, 33 branches, 4096-token prefix); with
+    packed weights this is the configuration the benchmark times.  The
+    oracle recomputes 3 sampled branches (layout, the longest and one more
+    content branch) on their own."""
+    announce(f"decode c4 full, sampled branches, packed {packed}")
     inp = make_decode_inputs("c4", 0)
-    h, pk, pv = run_decode(inp, canary=False)
+    h, pk, pv = run_decode(inp, canary=False, packed=packed)
     longest = int(np.argmax(np.where(inp.is_layout, -1, inp.past_len)))
     sample = sorted({0, longest, 7})
     sub, tok = _sub_batch(inp, sample)
@@ -122,3 +125,6 @@ def test_decode_deterministic_and_hidden_alias():
     h1, pk1, _ = run_decode(inp)
     h2, pk2, _ = run_decode(inp)
     assert np.array_equal(h1, h2) and all(np.array_equal(a, b) for a, b in zip(pk1, pk2))
+    h3, pk3, _ = run_decode(inp, packed=True)
+    h4, pk4, _ = run_decode(inp, packed=True)
+    assert np.array_equal(h3, h4) and all(np.array_equal(a, b) for a, b in zip(pk3, pk4))

@@ -53,13 +53,14 @@ def test_attention_graph_replays():
         assert torch.isfinite(noise)
 
 
-def test_decode_graph_replays():
-    announce("graph: decode small stack")
+@pytest.mark.parametrize("packed", [False, True], ids=["torch", "packed"])
+def test_decode_graph_replays(packed):
+    announce(f"graph: decode small stack, packed {packed}")
     from paper_2607_18839_amd.torch_api import DecodeStep
     inp = small_inputs(4, layers=2)
     w = {k: [to_dev(a, "bf16") for a in getattr(inp, k)] for k in ("w_qkv", "w_o", "w_gate", "w_up", "w_down")}
     step = DecodeStep(inp.num_q_heads, inp.num_kv_heads, inp.prefix_len, inp.branch_page, inp.num_new,
-                      inp.past_len, w, inp.hidden, inp.intermediate, inp.rms_eps)
+                      inp.past_len, w, inp.hidden, inp.intermediate, inp.rms_eps, packed=packed)
     sk = [to_dev(a, "bf16") for a in inp.shared_k]
     sv = [to_dev(a, "bf16") for a in inp.shared_v]
     pk = [to_dev(a, "bf16") for a in inp.priv_k]
