@@ -359,7 +359,11 @@ template <typename T> struct WaveAttn {
   // next tile's K (kt_next, or none) and of this tile's V^T are issued first,
   // the softmax of this tile's raw scores s_cur runs while they are in flight,
   // then the next tile's QK^T MFMAs (into s_next) and this tile's PV and
-  // row-sum MFMAs are issued together.
+  // row-sum MFMAs are issued together.  FSUM: the row sums are instead taken
+  // in fp32 on the VALU into l (this lane's half of the keys), which keeps
+  // the exported log-sum-exp exact to fp32 rounding when a row sees only a
+  // few keys (the matrix-core sum adds bf16-rounded probabilities).
+  template <bool FSUM = false>
   __device__ __forceinline__ void step_ring(const unsigned char *kt_next, const unsigned char *vt, const int (&voff)[2],
                                             f32x16 (&s_cur)[2], f32x16 (&s_next)[2], int key0, int limit,
                                             bool masked, float c, int lane) {
@@ -400,6 +404,7 @@ template <typename T> struct WaveAttn {
       m = m_new;
 #pragma unroll
       for (int r = 0; r < 16; ++r) { o[0][r] *= alpha; o[1][r] *= alpha; lsum[r] *= alpha; }
+      l *= alpha;
     }
     const float m_use = m == -INFINITY ? 0.f : m;
     float p[32];
@@ -407,6 +412,12 @@ template <typename T> struct WaveAttn {
     for (int r = 0; r < 16; ++r) {
       p[r] = __builtin_amdgcn_exp2f(fmaf(s_cur[0][r], c, -m_use));
       p[16 + r] = __builtin_amdgcn_exp2f(fmaf(s_cur[1][r], c, -m_use));
+    }
+    if constexpr (FSUM) {
+      float ps = 0.f;
+#pragma unroll
+      for (int r = 0; r < 32; ++r) ps += p[r];
+      l += ps;
     }
     Frag<T> pf[4];
 #pragma unroll
@@ -429,11 +440,13 @@ template <typename T> struct WaveAttn {
                                                 vr[(b * 4 + st) * 2 + 1][0], vr[(b * 4 + st) * 2 + 1][1]});
         mma(o[b], va, pf[st]);
       }
-    Frag<T> ones;
+    if constexpr (!FSUM) {
+      Frag<T> ones;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) ones.v[e] = (__bf16)1.f;
+      for (int e = 0; e < 8; ++e) ones.v[e] = (__bf16)1.f;
 #pragma unroll
-    for (int st = 0; st < 4; ++st) mma(lsum, ones, pf[st]);
+      for (int st = 0; st < 4; ++st) mma(lsum, ones, pf[st]);
+    }
   }
 
   // bf16 tile from the LDS ring: K tile kt (Tile<bf16> swizzle), V tile vt.
@@ -679,26 +692,36 @@ __global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
 // copy count the same.
 constexpr int kPairRing = 4;
 
-template <typename T, bool WAVE_LOCAL>
-__device__ __forceinline__ void private_item(const AttnArgs &a, int item, int lane, unsigned char *lds);
-
-constexpr int kPrivPerWG = 8;   // private items per workgroup of the bf16 attention kernel
+// Private work items of the bf16 kernel: one per wave on kPrivPerWG waves of
+// a workgroup, each wave with kPrivWaveBytes of LDS for the item's K and V
+// tiles (an item has at most kPrivateChunkKeys = 128 keys: two tiles).
+constexpr int kPrivPerWG = 4;
+constexpr int kPrivWaveBytes = 2 * 2 * 64 * 128;
+static_assert(kPrivateChunkKeys <= 128, "a private item fits two tiles");
+__device__ __forceinline__ void private_item_ring(const AttnArgs &a, int item, int lane, unsigned char *lds);
 
 __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   using T = __bf16;
   using Tl = Tile<T>;
   constexpr int S = kPairRing, kTileBytes = 64 * 128, kTile = 2 * kTileBytes, kPair = 2 * kTile;
-  constexpr int kRingBytes = S * kPair, kPrivBytes = kPrivPerWG * Tl::kBytes;
+  constexpr int kRingBytes = S * kPair, kPrivBytes = kPrivPerWG * kPrivWaveBytes;
   __shared__ __attribute__((aligned(16))) unsigned char lds[kRingBytes > kPrivBytes ? kRingBytes : kPrivBytes];
 
-  const int per_xcd = gridDim.x / 8;
-  const int item = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (item >= a.n_shared) {
-    // workgroups past the shared items run the private items, one per wave
-    const int wave = threadIdx.x >> 6, pi = (item - a.n_shared) * kPrivPerWG + wave;
-    if (pi < a.n_private) private_item<T, true>(a, pi, threadIdx.x & 63, lds + wave * Tl::kBytes);
+  // The first workgroups (dispatched first, spread over the XCDs: a private
+  // item is the longer dependency chain) run the private items, kPrivPerWG
+  // per workgroup; their count is rounded up to a multiple of 8 so that the
+  // shared items keep the XCD-aware order of the other kernels.
+  const int n_priv_wg = (a.n_private + kPrivPerWG - 1) / kPrivPerWG;
+  const int n_priv_slots = (n_priv_wg + 7) / 8 * 8;
+  if ((int)blockIdx.x < n_priv_slots) {
+    const int wave = threadIdx.x >> 6, pi = blockIdx.x * kPrivPerWG + wave;
+    if (wave < kPrivPerWG && pi < a.n_private)
+      private_item_ring(a, pi, threadIdx.x & 63, lds + wave * kPrivWaveBytes);
     return;
   }
+  const int b = blockIdx.x - n_priv_slots, per_xcd = (gridDim.x - n_priv_slots) / 8;
+  const int item = (b % 8) * per_xcd + b / 8;
+  if (item >= a.n_shared) return;
   const int32_t *it = a.dev.shared_items + (int64_t)item * SI_NFIELDS;
   const int g = it[SI_KVH], row0 = it[SI_ROW0], nrows = it[SI_NROWS];
   const int key0 = it[SI_KEY0], key1 = it[SI_KEY1], slot = it[SI_SLOT], flags = it[SI_FLAGS];
@@ -804,20 +827,84 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   w.write_f16(lds + 4 * 34 * 64 * 4 + rw * 4096, (_Float16 *)a.dev.part_o, a.dev.part_lse, prow_of, lane, true);
 }
 
+// One private work item on one wave of the bf16 kernel, in the wave's own
+// kPrivWaveBytes of LDS (no other wave touches it).  Both K/V tiles of the
+// item are copied straight into LDS in the ring layout (tile 0, then the Q
+// loads, then tile 1), then processed with the ring arithmetic.  Key rows
+// past the item's range are clamped to its last key and masked.
+__device__ __forceinline__ void private_item_ring(const AttnArgs &a, int item, int lane, unsigned char *lds) {
+  using T = __bf16;
+  using Tl = Tile<T>;
+  constexpr int kTileBytes = 64 * 128;
+  const int32_t *it = a.dev.private_items + (int64_t)item * PI_NFIELDS;
+  const int g = it[PI_KVH], row0 = it[PI_ROW0], nrows = it[PI_NROWS];
+  const int key0 = it[PI_KEY0], key1 = it[PI_KEY1], slot = it[PI_SLOT], past = it[PI_PAST];
+  const int priv_row = it[PI_PRIV_ROW], q_row = it[PI_Q_ROW];
+
+  const int rloc = lane & 31;
+  const bool valid = rloc < nrows;
+  const int R = row0 + rloc;                            // stacked row of (branch, g)
+  const int j = valid ? R / a.G : 0;                    // draft index within the branch
+  const int t = q_row + j;
+  const int hq = g * a.G + (valid ? R % a.G : 0);
+  const int limit = valid ? min(key1, past + j + 1) : key1;   // bottom-right causal
+  const int wmin = wave_min(limit);
+  const int ntiles = (key1 - key0 + 63) / 64;           // 1 or 2
+
+  const int64_t stride = (int64_t)a.Hkv * D;
+  const T *kbase = (const T *)a.priv_k + ((int64_t)priv_row * a.Hkv + g) * D;
+  const T *vbase = (const T *)a.priv_v + ((int64_t)priv_row * a.Hkv + g) * D;
+  // tile c: 8 copies of K rows 8 i + lane / 8 (physical chunk lane % 8) and
+  // 8 of V, 16 per tile
+  const int rsub = lane >> 3, pch = lane & 7;
+  auto issue = [&](int c) {
+    unsigned char *st = lds + c * 2 * kTileBytes;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int row = 8 * i + rsub;
+      const int64_t r = min(key0 + 64 * c + row, key1 - 1);
+      dma16(kbase + r * stride + 8 * Tl::kchunk(row, pch), st + 1024 * i);
+      dma16(vbase + r * stride + 8 * vchunk(row, pch), st + kTileBytes + 1024 * i);
+    }
+  };
+  issue(0);
+  WaveAttn<T> w;
+  w.init((const T *)a.q + ((int64_t)t * a.Hq + hq) * D, valid, lane);
+  if (ntiles > 1) {
+    issue(1);
+    wait_vm<16>();   // tile 0 and the Q fragments
+  } else {
+    wait_vm<0>();
+  }
+  int voff[2];
+  WaveAttn<T>::vt_offsets(lane, voff);
+  f32x16 s_cur[2], s_next[2];
+  w.qk_ring(lds, s_cur, lane);
+  if (ntiles > 1) wait_vm<0>();   // tile 1 (its K is read by the first step)
+  w.step_ring<true>(ntiles > 1 ? lds + 2 * kTileBytes : nullptr, lds + kTileBytes, voff, s_cur, s_next, key0, limit,
+                    key0 + 64 > wmin, a.c, lane);
+  if (ntiles > 1) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) { s_cur[0][r] = s_next[0][r]; s_cur[1][r] = s_next[1][r]; }
+    w.step_ring<true>(nullptr, lds + 3 * kTileBytes, voff, s_cur, s_next, key0 + 64, limit, key0 + 128 > wmin, a.c,
+                      lane);
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the tiles are consumed; tile 0 becomes write scratch
+  auto prow_of = [&](int r) -> int64_t {
+    if (r >= nrows) return -1;
+    const int Rr = row0 + r, tr = q_row + Rr / a.G;
+    return ((int64_t)a.dev.token_slots[2 * tr] + slot) * a.Hq + g * a.G + Rr % a.G;
+  };
+  w.write_f16(lds, (_Float16 *)a.dev.part_o, a.dev.part_lse, prow_of, lane, false);
+}
+
 // ------------------------------------------------------------ private kernel
 
-// One private work item on one wave: the wave's own LDS tile `lds`
-// (Tile<T>::kBytes).  WAVE_LOCAL: the workgroup's other waves run other items,
-// so the tile hand-overs only need this wave's LDS operations to have
-// completed (they execute in order); otherwise the workgroup is this one wave
-// and a workgroup barrier is used.
-template <typename T, bool WAVE_LOCAL>
-__device__ __forceinline__ void private_item(const AttnArgs &a, int item, int lane, unsigned char *lds) {
+// One fp32 private work item on a one-wave workgroup, staged through the
+// LDS tile `lds` (Tile<float>::kBytes).
+__device__ __forceinline__ void private_item_f32(const AttnArgs &a, int item, int lane, unsigned char *lds) {
+  using T = float;
   constexpr int NT = 64;
-  auto sync = [] {
-    if constexpr (WAVE_LOCAL) asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    else __syncthreads();
-  };
   const int32_t *it = a.dev.private_items + (int64_t)item * PI_NFIELDS;
   const int g = it[PI_KVH], row0 = it[PI_ROW0], nrows = it[PI_NROWS];
   const int key0 = it[PI_KEY0], key1 = it[PI_KEY1], slot = it[PI_SLOT], past = it[PI_PAST];
@@ -842,30 +929,20 @@ __device__ __forceinline__ void private_item(const AttnArgs &a, int item, int la
   for (int k0 = key0; k0 < key1; k0 += 64) {
     ld.load(kbase + (int64_t)k0 * stride, stride, key1 - k0, lane);
     ld.load_v(vbase + (int64_t)k0 * stride, stride, key1 - k0, lane);
-    sync();   // previous tile fully consumed
+    __syncthreads();   // previous tile fully consumed
     ld.store(lds, lane);
-    sync();
+    __syncthreads();
     w.tile(lds, k0, limit, k0 + 64 > wmin, a.c, lane);
   }
-  if constexpr (sizeof(T) == 2) {
-    sync();   // the tile is consumed; its LDS becomes write scratch
-    auto prow_of = [&](int r) -> int64_t {
-      if (r >= nrows) return -1;
-      const int Rr = row0 + r, tr = q_row + Rr / a.G;
-      return ((int64_t)a.dev.token_slots[2 * tr] + slot) * a.Hq + g * a.G + Rr % a.G;
-    };
-    w.write_f16(lds, (_Float16 *)a.dev.part_o, a.dev.part_lse, prow_of, lane, false);
-  } else {
-    const int64_t prow = valid ? ((int64_t)a.dev.token_slots[2 * t] + slot) * a.Hq + hq : 0;
-    w.write(a.dev.part_o, a.dev.part_lse, prow, valid);
-  }
+  const int64_t prow = valid ? ((int64_t)a.dev.token_slots[2 * t] + slot) * a.Hq + hq : 0;
+  w.write(a.dev.part_o, a.dev.part_lse, prow, valid);
 }
 
 // fp32 private kernel: one wave per item.
 __global__ __launch_bounds__(64) void private_kernel_f32(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) unsigned char lds[Tile<float>::kBytes];
   if ((int)blockIdx.x >= a.n_private) return;
-  private_item<float, false>(a, blockIdx.x, threadIdx.x, lds);
+  private_item_f32(a, blockIdx.x, threadIdx.x, lds);
 }
 
 // ------------------------------------------------------------ merge kernel
@@ -966,8 +1043,9 @@ hipError_t launch_branch_attention(const Plan &P, const void *q, const void *sha
   const bool bf16 = P.attn.dtype == HPD_BF16;
   if (bf16) {
     // one launch: shared-prefix items, then the private items 8 per workgroup
-    const int nwg = a.n_shared + (a.n_private + kPrivPerWG - 1) / kPrivPerWG;
-    if (nwg > 0) launch(KK_SHARED, shared_prefix_ring_kernel, dim3((nwg + 7) / 8 * 8), dim3(512), stream, a);
+    const int n_priv_wg = (a.n_private + kPrivPerWG - 1) / kPrivPerWG;
+    const int nwg = (n_priv_wg + 7) / 8 * 8 + (a.n_shared + 7) / 8 * 8;
+    if (nwg > 0) launch(KK_SHARED, shared_prefix_ring_kernel, dim3(nwg), dim3(512), stream, a);
   } else {
     if (a.n_shared > 0)
       launch(KK_SHARED, shared_prefix_kernel<float>, dim3((a.n_shared + 7) / 8 * 8), dim3(256), stream, a);
