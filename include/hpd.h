@@ -163,7 +163,7 @@ hpd_status hpd_branch_attn_step(const hpd_plan *plan, const void *q, const void 
 /* The synthetic decoder stack (pre-norm GQA transformer with RMSNorm and a
  * SwiGLU MLP, section "Overview", paragraph "LLM Decoder").  Weights are bf16
  * device arrays in torch Linear layout W[out][in]; each field points to a
- * HOST array of num_layers device pointers. */
+ * HOST array of num_layers device pointers, each 16-byte aligned. */
 typedef struct {
   int32_t num_layers;           /* >= 1                                        */
   int32_t hidden;               /* positive multiple of 128                    */
@@ -181,10 +181,13 @@ typedef struct {
 
 /* Layout of the projection weights of an hpd_model_desc.
  * HPD_WEIGHTS_TORCH: the layouts above (torch Linear, W[out][in], bf16).
- * HPD_WEIGHTS_PACKED: every projection packed once with hpd_pack_weight
- *   (w_qkv, w_o, w_down) or hpd_pack_gate_up (w_gate points to the packed
- *   gate/up pair; w_up is ignored and may be NULL).  The decode step then
- *   reads each weight tile with whole contiguous 1 KB loads per wave. */
+ * HPD_WEIGHTS_PACKED: every projection packed once: w_qkv and w_o with
+ *   hpd_pack_weight, w_down with hpd_pack_weight_f16, and the gate/up pair
+ *   with hpd_pack_gate_up (w_gate points to it; w_up is ignored and may be
+ *   NULL).  The decode step then reads each weight tile with whole
+ *   contiguous 1 KB loads per wave, and the MLP weights already in the fp16
+ *   its MLP projections compute in (the same values the torch layout is
+ *   converted to on the fly, so both formats give identical results). */
 typedef enum { HPD_WEIGHTS_TORCH = 0, HPD_WEIGHTS_PACKED = 1 } hpd_weight_format;
 
 /* Packed layout of a bf16 matrix W[rows][cols] (rows % 32 == 0, cols % 64
@@ -199,12 +202,18 @@ typedef enum { HPD_WEIGHTS_TORCH = 0, HPD_WEIGHTS_PACKED = 1 } hpd_weight_format
 size_t hpd_packed_weight_bytes(int32_t rows, int32_t cols);
 hpd_status hpd_pack_weight(const void *w, int32_t rows, int32_t cols, void *out, void *stream);
 
+/* As hpd_pack_weight, with every element converted from bf16 to fp16
+ * (round to nearest even; fp16 subnormals below 2^-14, 0 below 2^-25; the
+ * bf16 inputs of a decoder stay far inside the fp16 range). */
+hpd_status hpd_pack_weight_f16(const void *w, int32_t rows, int32_t cols, void *out, void *stream);
+
 /* Packed gate/up pair of a SwiGLU MLP: w_gate, w_up are device
  * [intermediate][hidden] bf16 (intermediate % 16 == 0, hidden % 64 == 0);
  * out (hpd_packed_weight_bytes(2 intermediate, hidden) bytes) holds the
- * packed [2 intermediate][hidden] matrix whose row tile r is gate rows
- * 16 r .. 16 r + 15 followed by up rows 16 r .. 16 r + 15 (so a row tile
- * computes 16 gate and their 16 up outputs together). */
+ * packed [2 intermediate][hidden] fp16 matrix (converted as in
+ * hpd_pack_weight_f16) whose row tile r is gate rows 16 r .. 16 r + 15
+ * followed by up rows 16 r .. 16 r + 15 (so a row tile computes 16 gate
+ * and their 16 up outputs together). */
 hpd_status hpd_pack_gate_up(const void *w_gate, const void *w_up, int32_t intermediate, int32_t hidden,
                             void *out, void *stream);
 

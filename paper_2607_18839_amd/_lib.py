@@ -90,6 +90,8 @@ SIGNATURES = {
     "hpd_packed_weight_bytes": (ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int32]),
     "hpd_pack_weight": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                        ctypes.c_void_p]),
+    "hpd_pack_weight_f16": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                           ctypes.c_void_p]),
     "hpd_pack_gate_up": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                         ctypes.c_void_p, ctypes.c_void_p]),
     "hpd_kernel_timing": (ctypes.c_int, [ctypes.c_int, ctypes.c_int]),
@@ -225,6 +227,10 @@ def hpd_packed_weight_bytes(rows, cols):
 
 def hpd_pack_weight(w, rows, cols, out, stream=None):
     _check(load().hpd_pack_weight(w, rows, cols, out, stream), "hpd_pack_weight")
+
+
+def hpd_pack_weight_f16(w, rows, cols, out, stream=None):
+    _check(load().hpd_pack_weight_f16(w, rows, cols, out, stream), "hpd_pack_weight_f16")
 
 
 def hpd_pack_gate_up(w_gate, w_up, intermediate, hidden, out, stream=None):

@@ -139,16 +139,26 @@ size_t hpd_packed_weight_bytes(int32_t rows, int32_t cols) {
   return (size_t)rows * (size_t)cols * 2;
 }
 
-hpd_status hpd_pack_weight(const void *w, int32_t rows, int32_t cols, void *out, void *stream) {
-  if (!w || !out) return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_pack_weight: NULL pointer");
+static hpd_status pack_weight(const char *name, const void *w, int32_t rows, int32_t cols, bool to_f16, void *out,
+                              void *stream) {
+  const std::string fn(name);
+  if (!w || !out) return set_err(HPD_ERR_INVALID_ARGUMENT, fn + ": NULL pointer");
   if (rows <= 0 || cols <= 0 || rows % 32 != 0 || cols % 64 != 0)
-    return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_pack_weight: rows must be a positive multiple of 32, cols of 64");
+    return set_err(HPD_ERR_INVALID_ARGUMENT, fn + ": rows must be a positive multiple of 32, cols of 64");
   if (!aligned(w, 16) || !aligned(out, 16))
-    return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_pack_weight: pointers must be 16-byte aligned");
-  hipError_t e = hpd::launch_pack_weight((const __bf16 *)w, nullptr, rows, cols, false, (__bf16 *)out,
+    return set_err(HPD_ERR_INVALID_ARGUMENT, fn + ": pointers must be 16-byte aligned");
+  hipError_t e = hpd::launch_pack_weight((const __bf16 *)w, nullptr, rows, cols, false, to_f16, (__bf16 *)out,
                                          (hipStream_t)stream);
-  if (e != hipSuccess) return hip_err(e, "hpd_pack_weight");
+  if (e != hipSuccess) return hip_err(e, name);
   return HPD_OK;
+}
+
+hpd_status hpd_pack_weight(const void *w, int32_t rows, int32_t cols, void *out, void *stream) {
+  return pack_weight("hpd_pack_weight", w, rows, cols, false, out, stream);
+}
+
+hpd_status hpd_pack_weight_f16(const void *w, int32_t rows, int32_t cols, void *out, void *stream) {
+  return pack_weight("hpd_pack_weight_f16", w, rows, cols, true, out, stream);
 }
 
 hpd_status hpd_pack_gate_up(const void *w_gate, const void *w_up, int32_t intermediate, int32_t hidden, void *out,
@@ -160,7 +170,7 @@ hpd_status hpd_pack_gate_up(const void *w_gate, const void *w_up, int32_t interm
   if (!aligned(w_gate, 16) || !aligned(w_up, 16) || !aligned(out, 16))
     return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_pack_gate_up: pointers must be 16-byte aligned");
   hipError_t e = hpd::launch_pack_weight((const __bf16 *)w_gate, (const __bf16 *)w_up, 2 * intermediate, hidden,
-                                         true, (__bf16 *)out, (hipStream_t)stream);
+                                         true, true, (__bf16 *)out, (hipStream_t)stream);
   if (e != hipSuccess) return hip_err(e, "hpd_pack_gate_up");
   return HPD_OK;
 }

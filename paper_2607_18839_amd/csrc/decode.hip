@@ -96,9 +96,16 @@ hpd_status validate(const hpd_model_desc *m, const hpd_plan *plan, std::string *
     *err = "NULL weight array";
     return HPD_ERR_INVALID_ARGUMENT;
   }
+  auto misaligned = [](const void *p) { return ((uintptr_t)p & 15) != 0; };
   for (int l = 0; l < m->num_layers; ++l) {
     if (!m->w_qkv[l] || !m->w_o[l] || !m->w_gate[l] || (!packed && !m->w_up[l]) || !m->w_down[l]) {
       *err = "NULL weight of layer " + std::to_string(l);
+      return HPD_ERR_INVALID_ARGUMENT;
+    }
+    if (misaligned(m->w_qkv[l]) || misaligned(m->w_o[l]) || misaligned(m->w_gate[l]) ||
+        (!packed && misaligned(m->w_up[l])) || misaligned(m->w_down[l]) ||
+        (m->g_attn_norm && misaligned(m->g_attn_norm[l])) || (m->g_mlp_norm && misaligned(m->g_mlp_norm[l]))) {
+      *err = "weight or gain of layer " + std::to_string(l) + " not 16-byte aligned";
       return HPD_ERR_INVALID_ARGUMENT;
     }
   }

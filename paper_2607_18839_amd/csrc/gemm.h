@@ -60,9 +60,9 @@ hipError_t launch_norm_input(const float *h_in, float *h, int T, int Tpad, int H
                              __bf16 *x, float *ss, __bf16 *zero_rows, int zero_cols, bool packed,
                              hipStream_t stream);
 // W[rows][cols] -> packed layout (gate_up: interleave w (gate) and w2 (up),
-// each [rows / 2][cols]).
-hipError_t launch_pack_weight(const __bf16 *w, const __bf16 *w2, int rows, int cols, bool gate_up, __bf16 *out,
-                              hipStream_t stream);
+// each [rows / 2][cols]); to_f16: elements converted from bf16 to fp16.
+hipError_t launch_pack_weight(const __bf16 *w, const __bf16 *w2, int rows, int cols, bool gate_up, bool to_f16,
+                              __bf16 *out, hipStream_t stream);
 // f16: fp16 GEMM (bf16 weights converted to fp16 in registers, fp16
 // activations); epi: kEpi*.
 hipError_t launch_gemm(const GemmArgs &g, bool f16, int epi, int kind, hipStream_t stream);

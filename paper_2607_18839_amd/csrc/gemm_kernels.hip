@@ -59,26 +59,55 @@ __device__ __forceinline__ u32x4 bf16x8_to_f16x8(u32x4 v) {
   return r;
 }
 
-// Epilogue operands, loaded before a GEMM's main loop (no later step needs
-// them sooner, and the loop's waits retire them): the per-token sums of
-// squares (QKV, SwiGLU; up to 32 partials) or the residual row slice.
+// Epilogue operands of a tile.  Only the token's cache row (QKV, plan data)
+// is loaded before the main loop.  The residual row slice, the next norm's
+// weights and the per-token sums of squares were written or are read right
+// next to data the previous kernel wrote, and loading them early measurably
+// delays the loop's first steps (the loads retire in order), so the packed
+// kernel loads them in the epilogue.
+struct EpilogueIn {
+  f32x4 h[4], gamma[4];   // residual: h row slice and gamma (ones if none)
+  int dest;               // QKV: private cache row of the token
+  float inv_rms;          // QKV, SwiGLU: RMSNorm factor of the token
+};
+
 template <int EPI>
-__device__ __forceinline__ void prefetch_epilogue(const GemmArgs &g, int t, int tile, int half, f32x4 (&pre)[8]) {
+__device__ __forceinline__ void load_early(const GemmArgs &g, int t, EpilogueIn &in) {
+  if constexpr (EPI == kEpiQKV) in.dest = t < g.T ? g.dest[t] : 0;
+}
+
+template <int EPI>
+__device__ __forceinline__ void load_late(const GemmArgs &g, int t, int tile, int half, EpilogueIn &in) {
   if constexpr (EPI == kEpiResidual) {
     const float *hr = g.h + (int64_t)min(t, g.T - 1) * g.N + tile * kGemmTile + 4 * half;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) pre[i] = *(const f32x4 *)(hr + 8 * i);
-  } else {
-    const float *sr = g.ss_in + (int64_t)t * g.n_ss;
+    for (int i = 0; i < 4; ++i) in.h[i] = *(const f32x4 *)(hr + 8 * i);
+    if (g.x_out && g.gamma) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) pre[i] = *(const f32x4 *)(sr + 4 * min(i, g.n_ss / 4 - 1));
+      for (int i = 0; i < 4; ++i) {
+        const bf16x4 gv = *(const bf16x4 *)(g.gamma + tile * kGemmTile + 8 * i + 4 * half);
+        in.gamma[i] = f32x4{(float)gv[0], (float)gv[1], (float)gv[2], (float)gv[3]};
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) in.gamma[i] = f32x4{1.f, 1.f, 1.f, 1.f};
+    }
+  } else {
+    // per-token RMSNorm factor from the partial sums of squares
+    const float *sr = g.ss_in + (int64_t)t * g.n_ss;
+    float sum = 0.f;
+    for (int i = 0; i < g.n_ss; i += 4) {
+      const f32x4 v = *(const f32x4 *)(sr + i);
+      sum += (v[0] + v[1]) + (v[2] + v[3]);
+    }
+    in.inv_rms = 1.0f / sqrtf(sum * g.inv_H + g.eps);
   }
 }
 
 // Writes the finished 32 x 32 tile `tile` for token t (this lane: rows
 // 8 (r / 4) + 4 half + r % 4 of the tile, see below) through epilogue EPI.
 template <int EPI>
-__device__ __forceinline__ void epilogue(const GemmArgs &g, const f32x16 &acc, f32x4 (&pre)[8], int t, int tile,
+__device__ __forceinline__ void epilogue(const GemmArgs &g, const f32x16 &acc, EpilogueIn &in, int t, int tile,
                                          int half) {
   if constexpr (EPI == kEpiResidual) {
     // h += Y; x_out = h * gamma (the next norm's input, unnormalised) and the
@@ -90,10 +119,10 @@ __device__ __forceinline__ void epilogue(const GemmArgs &g, const f32x16 &acc, f
     for (int i = 0; i < 4; ++i) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        pre[i][r] += acc[4 * i + r];
-        ss = fmaf(pre[i][r], pre[i][r], ss);
+        in.h[i][r] += acc[4 * i + r];
+        ss = fmaf(in.h[i][r], in.h[i][r], ss);
       }
-      *(f32x4 *)(hr + 8 * i) = pre[i];
+      *(f32x4 *)(hr + 8 * i) = in.h[i];
     }
     if (!g.x_out) return;
     ss += __shfl_xor(ss, 32);
@@ -101,10 +130,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs &g, const f32x16 &acc, f
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int n = tile * kGemmTile + 8 * i + 4 * half;
-      f32x4 v = pre[i];
-      if (g.gamma)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] *= (float)g.gamma[n + r];
+      const f32x4 v = in.h[i] * in.gamma[i];
       const int64_t off = g.act_packed ? packed_offset(t, n, g.N) : (int64_t)t * g.N + n;
       if (g.x_out_f16) {
         f16x4 o;
@@ -119,20 +145,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs &g, const f32x16 &acc, f
       }
     }
   } else {
-    // per-token RMSNorm factor from the partial sums of squares
-    float sum = 0.f;
-    if (g.n_ss <= 32) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        if (4 * i < g.n_ss) sum += (pre[i][0] + pre[i][1]) + (pre[i][2] + pre[i][3]);
-    } else {
-      const float *sr = g.ss_in + (int64_t)t * g.n_ss;
-      for (int i = 0; i < g.n_ss; i += 4) {
-        const f32x4 v = *(const f32x4 *)(sr + i);
-        sum += (v[0] + v[1]) + (v[2] + v[3]);
-      }
-    }
-    const float inv_rms = 1.0f / sqrtf(sum * g.inv_H + g.eps);
+    const float inv_rms = in.inv_rms;
     if constexpr (EPI == kEpiQKV) {
       if (t >= g.T) return;
 #pragma unroll
@@ -142,8 +155,8 @@ __device__ __forceinline__ void epilogue(const GemmArgs &g, const f32x16 &acc, f
 #pragma unroll
         for (int r = 0; r < 4; ++r) v[r] = (__bf16)(acc[4 * i + r] * inv_rms);
         if (n < g.n_q) *(bf16x4 *)(g.q_out + (int64_t)t * g.n_q + n) = v;
-        else if (n < g.n_q + g.n_kv) *(bf16x4 *)(g.k_cache + (int64_t)g.dest[t] * g.n_kv + (n - g.n_q)) = v;
-        else *(bf16x4 *)(g.v_cache + (int64_t)g.dest[t] * g.n_kv + (n - g.n_q - g.n_kv)) = v;
+        else if (n < g.n_q + g.n_kv) *(bf16x4 *)(g.k_cache + (int64_t)in.dest * g.n_kv + (n - g.n_q)) = v;
+        else *(bf16x4 *)(g.v_cache + (int64_t)in.dest * g.n_kv + (n - g.n_q - g.n_kv)) = v;
       }
     } else {   // SwiGLU: m = silu(gate) * up, fp16; rows t >= T are written as zeros
 #pragma unroll
@@ -228,8 +241,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   const int t = tt * kGemmTile + frow;   // this lane's token in the epilogue
   const int tile = slice * RG + rg;      // 32-row tile of the output columns
 
-  f32x4 pre[8];
-  prefetch_epilogue<EPI>(g, t, tile, half, pre);
+  EpilogueIn ein;
+  load_early<EPI>(g, t, ein);
 
   // copy sources: instruction q of the K group covers tile q / 4 (row group
   // q / 4 < RG, else the token tile), rows 8 (q % 4) + lane / 8
@@ -321,7 +334,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
       for (int r = 0; r < 16; ++r) acc[r] += red[((k * RG + rg) * 16 + r) * 64 + lane];
   }
 
-  epilogue<EPI>(g, acc, pre, t, tile, half);
+  load_late<EPI>(g, t, tile, half, ein);
+  epilogue<EPI>(g, acc, ein, t, tile, half);
 }
 
 // The same projection with both operands in the packed layout (packed_offset:
@@ -347,8 +361,8 @@ __global__ __launch_bounds__(256) void gemm_packed_kernel(GemmArgs g) {
   const int tile = slice * RG + rg;
   const int ksteps = g.K / kGemmKStep, nsteps = ksteps / KG, ks0 = kgi * nsteps;
 
-  f32x4 pre[8];
-  prefetch_epilogue<EPI>(g, t, tile, half, pre);
+  EpilogueIn ein;
+  load_early<EPI>(g, t, ein);
 
   const __bf16 *arow = g.w0 + ((int64_t)tile * ksteps + ks0) * 2048 + lane * 8;
   const __bf16 *brow = g.x + ((int64_t)tt * ksteps + ks0) * 2048 + lane * 8;
@@ -365,11 +379,12 @@ __global__ __launch_bounds__(256) void gemm_packed_kernel(GemmArgs g) {
   f32x16 acc;
 #pragma unroll
   for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  // F16: the packed MLP weights are stored in fp16 already
   auto compute = [&](int slot) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       if constexpr (F16)
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, bf16x8_to_f16x8(a[slot][j])),
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a[slot][j]),
                                                      __builtin_bit_cast(f16x8, b[slot][j]), acc, 0, 0, 0);
       else
         acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[slot][j]),
@@ -391,10 +406,6 @@ __global__ __launch_bounds__(256) void gemm_packed_kernel(GemmArgs g) {
       compute(u % S);
     }
   };
-  auto prologue = [&](auto n) {
-#pragma unroll
-    for (int u = 0; u < decltype(n)::value; ++u) load(u, u);
-  };
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
   using I3 = std::integral_constant<int, 3>;
@@ -402,8 +413,11 @@ __global__ __launch_bounds__(256) void gemm_packed_kernel(GemmArgs g) {
   using I5 = std::integral_constant<int, 5>;
   using I6 = std::integral_constant<int, 6>;
   static_assert(S == 4, "the tail cases below cover REM = 1 .. 2 S - 2");
+  // unconditional (a step index past the end repeats the last step, unused),
+  // so that no load sits under a runtime condition
+#pragma unroll
+  for (int u = 0; u < S - 1; ++u) load(min(u, nsteps - 1), u);
   if (nsteps >= 2 * S - 1) {
-    prologue(I3{});
     const int n_main = (nsteps - (2 * S - 1)) / S + 1;
     for (int gi = 0; gi < n_main; ++gi) {
 #pragma unroll
@@ -421,15 +435,17 @@ __global__ __launch_bounds__(256) void gemm_packed_kernel(GemmArgs g) {
     }
   } else {
     switch (nsteps) {   // 1 .. 2 S - 2
-      case 1: prologue(I1{}); tail(0, I1{}); break;
-      case 2: prologue(I2{}); tail(0, I2{}); break;
-      case 3: prologue(I3{}); tail(0, I3{}); break;
-      case 4: prologue(I3{}); tail(0, I4{}); break;
-      case 5: prologue(I3{}); tail(0, I5{}); break;
-      default: prologue(I3{}); tail(0, I6{}); break;
+      case 1: tail(0, I1{}); break;
+      case 2: tail(0, I2{}); break;
+      case 3: tail(0, I3{}); break;
+      case 4: tail(0, I4{}); break;
+      case 5: tail(0, I5{}); break;
+      default: tail(0, I6{}); break;
     }
   }
 
+  // the epilogue's own loads overlap the K-group hand-over
+  if (kgi == 0) load_late<EPI>(g, t, tile, half, ein);
   if constexpr (KG > 1) {
     // K groups 1.. hand their tiles to K group 0, which adds them in order
     __shared__ float red[(KG - 1) * RG * 16 * 64];
@@ -444,15 +460,16 @@ __global__ __launch_bounds__(256) void gemm_packed_kernel(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[r] += red[((k * RG + rg) * 16 + r) * 64 + lane];
   }
-  epilogue<EPI>(g, acc, pre, t, tile, half);
+  epilogue<EPI>(g, acc, ein, t, tile, half);
 }
 
 // Packs W[rows][cols] (bf16) into the packed layout: one thread per 16-byte
 // piece of the output.  gate_up: rows are the pair's interleaved rows (row tile
 // r = gate rows 16 r .. 16 r + 15, then up rows 16 r .. 16 r + 15) read from
-// w (gate) and w2 (up), each [rows / 2][cols].
+// w (gate) and w2 (up), each [rows / 2][cols].  to_f16: the elements are
+// converted to fp16 (as the torch-layout kernels convert them on the fly).
 __global__ __launch_bounds__(256) void pack_weight_kernel(const __bf16 *w, const __bf16 *w2, int rows, int cols,
-                                                          int gate_up, __bf16 *out) {
+                                                          int gate_up, int to_f16, __bf16 *out) {
   const int64_t piece = (int64_t)blockIdx.x * 256 + threadIdx.x;   // 8 elements each
   if (piece * 8 >= (int64_t)rows * cols) return;
   const int64_t tile_id = piece / 256;
@@ -467,7 +484,8 @@ __global__ __launch_bounds__(256) void pack_weight_kernel(const __bf16 *w, const
   } else {
     src = w + (int64_t)r * cols + c;
   }
-  *(u32x4 *)(out + piece * 8) = *(const u32x4 *)src;
+  const u32x4 v = *(const u32x4 *)src;
+  *(u32x4 *)(out + piece * 8) = to_f16 ? bf16x8_to_f16x8(v) : v;
 }
 
 // Start of a step: h = h_in, x = h * gamma (bf16), sums of squares of h over
@@ -531,13 +549,13 @@ void launch_packed(const GemmArgs &g, int kind, dim3 grid, hipStream_t stream) {
 
 }  // namespace
 
-hipError_t launch_pack_weight(const __bf16 *w, const __bf16 *w2, int rows, int cols, bool gate_up, __bf16 *out,
-                              hipStream_t stream) {
+hipError_t launch_pack_weight(const __bf16 *w, const __bf16 *w2, int rows, int cols, bool gate_up, bool to_f16,
+                              __bf16 *out, hipStream_t stream) {
   if (!w || !out || (gate_up && !w2) || rows <= 0 || cols <= 0 || rows % kGemmTile != 0 || cols % kGemmKStep != 0)
     return hipErrorInvalidValue;
   const int64_t pieces = (int64_t)rows * cols / 8;
   hipLaunchKernelGGL(pack_weight_kernel, dim3((unsigned)((pieces + 255) / 256)), dim3(256), 0, stream, w, w2, rows,
-                     cols, gate_up ? 1 : 0, out);
+                     cols, gate_up ? 1 : 0, to_f16 ? 1 : 0, out);
   return hipGetLastError();
 }
 

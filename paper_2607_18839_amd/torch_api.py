@@ -56,18 +56,20 @@ class BranchAttention:
         return out
 
 
-def pack_weight(w, stream=None):
-    """Packed copy (hpd_pack_weight) of a bf16 [rows][cols] device tensor."""
+def pack_weight(w, stream=None, f16=False):
+    """Packed copy of a bf16 [rows][cols] device tensor: bf16
+    (hpd_pack_weight) or converted to fp16 (hpd_pack_weight_f16)."""
     rows, cols = w.shape
-    out = torch.empty_like(w)
-    _lib.hpd_pack_weight(w.data_ptr(), rows, cols, out.data_ptr(), _stream(stream))
+    out = torch.empty(w.shape, dtype=torch.float16 if f16 else w.dtype, device=w.device)
+    fn = _lib.hpd_pack_weight_f16 if f16 else _lib.hpd_pack_weight
+    fn(w.data_ptr(), rows, cols, out.data_ptr(), _stream(stream))
     return out
 
 
 def pack_gate_up(w_gate, w_up, stream=None):
-    """Packed gate/up pair (hpd_pack_gate_up) of two bf16 [I][hidden] tensors."""
+    """Packed fp16 gate/up pair (hpd_pack_gate_up) of two bf16 [I][hidden] tensors."""
     inter, hidden = w_gate.shape
-    out = torch.empty((2 * inter, hidden), dtype=w_gate.dtype, device=w_gate.device)
+    out = torch.empty((2 * inter, hidden), dtype=torch.float16, device=w_gate.device)
     _lib.hpd_pack_gate_up(w_gate.data_ptr(), w_up.data_ptr(), inter, hidden, out.data_ptr(), _stream(stream))
     return out
 
@@ -97,8 +99,9 @@ class DecodeStep:
             weights = dict(weights)
             weights["w_gate"] = [pack_gate_up(g, u, stream) for g, u in zip(weights["w_gate"], weights["w_up"])]
             weights["w_up"] = weights["w_gate"]   # ignored by the packed format
-            for k in ("w_qkv", "w_o", "w_down"):
+            for k in ("w_qkv", "w_o"):
                 weights[k] = [pack_weight(w, stream) for w in weights[k]]
+            weights["w_down"] = [pack_weight(w, stream, f16=True) for w in weights["w_down"]]
             fmt = _lib.HPD_WEIGHTS_PACKED
         self._weights = weights   # keeps packed copies alive
         ptrs = {k: [t.data_ptr() for t in v] for k, v in weights.items()}

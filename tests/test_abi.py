@@ -171,6 +171,7 @@ def test_decode_step_checks_weight_format():
     fake = 4096
     one = [fake]
     for fmt, w_up, status, needle in ((7, one, 1, "weight_format"), (0, [None], 1, "NULL weight"),
+                                      (0, [fake + 2], 1, "16-byte aligned"),
                                       (1, [None], 3, "workspace too small")):
         model = _lib.model_desc(1, 256, 384, 1e-6, one, one, one, w_up, one, weight_format=fmt)
         with pytest.raises(_lib.HpdError) as e:
