@@ -621,7 +621,38 @@ struct AttnArgs {
   int n_shared, n_private;
   int Hq, Hkv, G;
   float c;   // softmax scale * log2(e)
+  Plan::RegularShared reg;
 };
+
+// Fields of shared work item `item`: computed from its index for a regular
+// plan (one page, no fork offsets: items ordered kv head, split, row group),
+// else read from the plan's table (a dependent load at the head of every
+// workgroup's chain, which the regular form avoids).
+struct SharedItem {
+  int g, row0, nrows, key0, key1, slot, flags, prefix_row, page_q_row;
+};
+__device__ __forceinline__ SharedItem shared_item(const AttnArgs &a, int item) {
+  SharedItem si;
+  if (a.reg.on) {
+    const int rgi = item % a.reg.groups, rest = item / a.reg.groups;
+    const int s = rest % a.reg.splits;
+    si.g = rest / a.reg.splits;
+    si.row0 = rgi * kSharedWaves * kTileRows;
+    si.nrows = min(kSharedWaves * kTileRows, a.reg.rows - si.row0);
+    si.key0 = s * a.reg.split_keys;
+    si.key1 = min(a.reg.prefix_len, si.key0 + a.reg.split_keys);
+    si.slot = s;
+    si.flags = 0;
+    si.prefix_row = a.reg.prefix_row;
+    si.page_q_row = a.reg.page_q_row;
+  } else {
+    const int32_t *it = a.dev.shared_items + (int64_t)item * SI_NFIELDS;
+    si.g = it[SI_KVH]; si.row0 = it[SI_ROW0]; si.nrows = it[SI_NROWS];
+    si.key0 = it[SI_KEY0]; si.key1 = it[SI_KEY1]; si.slot = it[SI_SLOT]; si.flags = it[SI_FLAGS];
+    si.prefix_row = it[SI_PREFIX_ROW]; si.page_q_row = it[SI_PAGE_Q_ROW];
+  }
+  return si;
+}
 
 template <typename T>
 __global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
@@ -635,10 +666,10 @@ __global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
   const int per_xcd = gridDim.x / 8;
   const int item = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
   if (item >= a.n_shared) return;
-  const int32_t *it = a.dev.shared_items + (int64_t)item * SI_NFIELDS;
-  const int g = it[SI_KVH], row0 = it[SI_ROW0], nrows = it[SI_NROWS];
-  const int key0 = it[SI_KEY0], key1 = it[SI_KEY1], slot = it[SI_SLOT], flags = it[SI_FLAGS];
-  const int prefix_row = it[SI_PREFIX_ROW], page_q_row = it[SI_PAGE_Q_ROW];
+  const SharedItem si = shared_item(a, item);
+  const int g = si.g, row0 = si.row0, nrows = si.nrows;
+  const int key0 = si.key0, key1 = si.key1, slot = si.slot, flags = si.flags;
+  const int prefix_row = si.prefix_row, page_q_row = si.page_q_row;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int rloc = wave * 32 + (lane & 31);
@@ -722,10 +753,10 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   const int b = blockIdx.x - n_priv_slots, per_xcd = (gridDim.x - n_priv_slots) / 8;
   const int item = (b % 8) * per_xcd + b / 8;
   if (item >= a.n_shared) return;
-  const int32_t *it = a.dev.shared_items + (int64_t)item * SI_NFIELDS;
-  const int g = it[SI_KVH], row0 = it[SI_ROW0], nrows = it[SI_NROWS];
-  const int key0 = it[SI_KEY0], key1 = it[SI_KEY1], slot = it[SI_SLOT], flags = it[SI_FLAGS];
-  const int prefix_row = it[SI_PREFIX_ROW], page_q_row = it[SI_PAGE_Q_ROW];
+  const SharedItem si = shared_item(a, item);
+  const int g = si.g, row0 = si.row0, nrows = si.nrows;
+  const int key0 = si.key0, key1 = si.key1, slot = si.slot, flags = si.flags;
+  const int prefix_row = si.prefix_row, page_q_row = si.page_q_row;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int rw = wave & 3, par = wave >> 2;             // row group, key-tile parity
@@ -1040,6 +1071,7 @@ hipError_t launch_branch_attention(const Plan &P, const void *q, const void *sha
   a.Hkv = P.attn.num_kv_heads;
   a.G = P.G;
   a.c = P.scale * kLog2e;
+  a.reg = P.regular;
   const bool bf16 = P.attn.dtype == HPD_BF16;
   if (bf16) {
     // one launch: shared-prefix items, then the private items 8 per workgroup

@@ -208,6 +208,17 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
         }
   }
 
+  if (np == 1 && !P.has_fork && P.prefix_len[0] > 0 && P.page_T[0] > 0 && P.prefix_row[0] <= INT32_MAX) {
+    P.regular.on = 1;
+    P.regular.groups = (int32_t)ceil_div((int64_t)P.page_T[0] * G, group_rows);
+    P.regular.splits = page_splits[0];
+    P.regular.split_keys = page_split_keys[0];
+    P.regular.rows = P.page_T[0] * G;
+    P.regular.prefix_len = P.prefix_len[0];
+    P.regular.prefix_row = (int32_t)P.prefix_row[0];
+    P.regular.page_q_row = P.page_q_row[0];
+  }
+
   // ---- private work items: (branch, kv head, row tile, key chunk)
   for (int i = 0; i < nb; ++i) {
     const int keys = P.past_len[i] + P.num_new[i];

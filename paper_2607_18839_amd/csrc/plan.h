@@ -56,6 +56,13 @@ struct Plan {
   std::vector<int32_t> token_dest;                    // [T] private row of token t: priv_row + L + j
   int64_t num_slots = 0;                              // partial rows = num_slots * Hq
   int32_t split_keys = 0;                             // prefix keys per shared work item
+  // One page without fork offsets: its shared items are (kv head, split, row
+  // group) in that nesting order and the kernels compute an item's fields
+  // from its index instead of reading the table.
+  struct RegularShared {
+    int32_t on = 0, groups = 0, splits = 0, split_keys = 0, rows = 0, prefix_len = 0, prefix_row = 0,
+            page_q_row = 0;
+  } regular;
 
   // device workspace layout (byte offsets, 256-aligned)
   size_t off_shared_items = 0, off_private_items = 0, off_token_slots = 0,

@@ -177,3 +177,32 @@ def test_decode_step_checks_weight_format():
         with pytest.raises(_lib.HpdError) as e:
             _lib.hpd_decode_step(model, plan, fake, fake, one, one, one, one, 4096, 0)
         assert e.value.status == status and needle in str(e.value), str(e.value)
+
+
+@pytest.mark.parametrize("name,st", _structures(), ids=lambda x: x if isinstance(x, str) else "")
+@pytest.mark.parametrize("Hq,Hkv", [(16, 2), (12, 2), (4, 4)])
+def test_single_page_items_follow_the_index_formula(name, st, Hq, Hkv):
+    """For one page without fork offsets the kernels compute a shared item's
+    fields from its index (kv head, split, row group nesting) instead of
+    reading the table: the table must be exactly that formula."""
+    if len(st["prefix_len"]) != 1 or st["prefix_len"][0] == 0:
+        pytest.skip("not a single-page plan")
+    G = Hq // Hkv
+    info = _lib.hpd_plan_query(_plan(st, Hq, Hkv))
+    items = info["shared_items"]
+    S = _lib.SI
+    rows = info["T"] * G
+    groups = -(-rows // 128)
+    split_keys = items[0][S["key1"]] - items[0][S["key0"]] if len(items) > 1 else st["prefix_len"][0]
+    splits = len(items) // (Hkv * groups)
+    assert len(items) == Hkv * splits * groups
+    P = int(st["prefix_len"][0])
+    for i, it in enumerate(items):
+        rgi, rest = i % groups, i // groups
+        s, g = rest % splits, rest // splits
+        k0 = s * split_keys
+        want = dict(page=0, kvh=g, row0=128 * rgi, nrows=min(128, rows - 128 * rgi), key0=k0,
+                    key1=min(P, k0 + split_keys), slot=s, flags=0, prefix_row=info["prefix_row"][0],
+                    page_q_row=0)
+        for k, v in want.items():
+            assert it[S[k]] == v, (i, k, it[S[k]], v)
