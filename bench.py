@@ -144,6 +144,28 @@ def _kernel_pass(torch, _lib, step, K, W, queue_cycles=20_000_000):
             if not k.startswith("_") and c}
 
 
+def _phase_pass(torch, _lib, step, K, W, work, queue_cycles=2_000_000):
+    """Per-kernel durations with the attention phases in launches of their own
+    (hpd_attn_phase_isolation): the shared-prefix items alone (MFMA-bound) and
+    the private items alone (HBM-bound), next to the co-scheduled launch."""
+    _lib.hpd_attn_phase_isolation(True)
+    try:
+        kern = _kernel_pass(torch, _lib, step, K, W, queue_cycles)
+    finally:
+        _lib.hpd_attn_phase_isolation(False)
+    out = {}
+    sh, pr = kern.get("shared_prefix", {}).get("avg_us"), kern.get("private", {}).get("avg_us")
+    if sh:
+        out["shared_only_us"] = sh
+        out["shared_mfma_frac"] = work["shared_flop"] / sh / 1e6 / BF16_PEAK_TFLOPS
+    if pr:
+        out["private_us"] = pr
+        out["private_algorithmic_bytes"] = work["private_bytes"]
+        out["private_gbs"] = work["private_bytes"] / pr / 1e3
+        out["private_hbm_frac"] = work["private_bytes"] / pr / 1e3 / HBM_PEAK_GBS
+    return out
+
+
 def _traffic(kind):
     """HBM bytes per launch of kernel kind from profiles/traffic_c4.md (rocprofv3
     FETCH_SIZE / WRITE_SIZE runs scaled by a plain copy kernel's readings), or
@@ -211,6 +233,8 @@ def bench_attention(args, torch, _lib):
     if pr:
         kern["private"].update(bytes=w["private_bytes"], gbs=w["private_bytes"] / pr / 1e3,
                                hbm_frac=w["private_bytes"] / pr / 1e3 / HBM_PEAK_GBS)
+    if b.dtype == "bf16":
+        kern["phases_isolated"] = _phase_pass(torch, _lib, step, min(args.steps, 20), args.warmup, w)
     roof = None
     if sh:
         ach = sh_flop / sh / 1e6
@@ -306,6 +330,7 @@ def bench_decode(args, torch, _lib):
             k.update(bound="hbm", bytes=gw[name], gbs=gw[name] / us / 1e3, frac=gw[name] / us / 1e3 / HBM_PEAK_GBS)
         k["total_us_per_step"] = us * k["launches"] / min(args.steps, 10)
     dom = max(kern, key=lambda n: kern[n]["total_us_per_step"])
+    kern["phases_isolated"] = _phase_pass(torch, _lib, step, min(args.steps, 10), args.warmup, aw)
     d = kern[dom]
     if d.get("bound") == "mfma":
         roof = {"bound": "mfma", "kernel": dom, "achieved": d["tflops"], "peak": BF16_PEAK_TFLOPS,

@@ -270,8 +270,16 @@ hpd_status hpd_kernel_times_read(hpd_kernel_times *out, int keep_pairs);
 /* Kind k: 0 shared_prefix, 1 private, 2 merge, 3 gemm_qkv, 4 gemm_o,
  * 5 gemm_gate_up, 6 gemm_down, 7 norm_input.  With bf16 inputs kind 0 is
  * one launch that runs the shared-prefix and the private work items (kind 1
- * is then never launched). */
+ * is then never launched) unless phase isolation is on. */
 const char *hpd_kernel_kind_name(int kind);
+
+/* Phase isolation (benchmark support, process-wide, default off).  When on,
+ * the bf16 attention enqueues its private work items as a launch of their
+ * own (kind 1) after the shared-prefix launch (kind 0) instead of running
+ * both in one launch, so each phase can be timed and profiled on its own.
+ * Results are bit-identical either way.  Not to be changed while a step is
+ * being enqueued or captured. */
+hpd_status hpd_attn_phase_isolation(int enable);
 
 const char *hpd_status_string(hpd_status status);
 const char *hpd_last_error_message(void);

@@ -95,6 +95,7 @@ SIGNATURES = {
     "hpd_pack_gate_up": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                         ctypes.c_void_p, ctypes.c_void_p]),
     "hpd_kernel_timing": (ctypes.c_int, [ctypes.c_int, ctypes.c_int]),
+    "hpd_attn_phase_isolation": (ctypes.c_int, [ctypes.c_int]),
     "hpd_kernel_times_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int]),
     "hpd_kernel_kind_name": (ctypes.c_char_p, [ctypes.c_int]),
     "hpd_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -278,3 +279,7 @@ def declared_symbols(header=None):
     header = header or os.path.join(os.path.dirname(_HERE), "include", "hpd.h")
     text = open(header).read()
     return sorted(set(re.findall(r"\b(hpd_[a-z_]+)\s*\(", text)))
+
+
+def hpd_attn_phase_isolation(enable):
+    _check(load().hpd_attn_phase_isolation(1 if enable else 0), "hpd_attn_phase_isolation")

@@ -622,6 +622,7 @@ struct AttnArgs {
   int Hq, Hkv, G;
   float c;   // softmax scale * log2(e)
   Plan::RegularShared reg;
+  int priv_first;   // bf16 kernel: private workgroups take the first grid slots
 };
 
 // Fields of shared work item `item`: computed from its index for a regular
@@ -738,19 +739,25 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   constexpr int kRingBytes = S * kPair, kPrivBytes = kPrivPerWG * kPrivWaveBytes;
   __shared__ __attribute__((aligned(16))) unsigned char lds[kRingBytes > kPrivBytes ? kRingBytes : kPrivBytes];
 
-  // The first workgroups (dispatched first, spread over the XCDs: a private
-  // item is the longer dependency chain) run the private items, kPrivPerWG
-  // per workgroup; their count is rounded up to a multiple of 8 so that the
-  // shared items keep the XCD-aware order of the other kernels.
+  // Workgroups run either kPrivPerWG private items or one shared item.  Both
+  // ranges are rounded up to multiples of 8 so that the shared items keep
+  // the XCD-aware order of the other kernels.  priv_first (the grid fits the
+  // chip in one round): the private range comes first, so the longer
+  // dependency chain of a private item starts first; otherwise the shared
+  // items, the larger work, are dispatched first and the private items fill
+  // in behind them.
   const int n_priv_wg = (a.n_private + kPrivPerWG - 1) / kPrivPerWG;
-  const int n_priv_slots = (n_priv_wg + 7) / 8 * 8;
-  if ((int)blockIdx.x < n_priv_slots) {
-    const int wave = threadIdx.x >> 6, pi = blockIdx.x * kPrivPerWG + wave;
+  const int n_priv_slots = (n_priv_wg + 7) / 8 * 8, n_shared_slots = (a.n_shared + 7) / 8 * 8;
+  const int priv0 = a.priv_first ? 0 : n_shared_slots, shared0 = a.priv_first ? n_priv_slots : 0;
+  const int bid = blockIdx.x;
+  if (bid >= priv0 && bid < priv0 + n_priv_slots) {
+    const int wave = threadIdx.x >> 6, pi = (bid - priv0) * kPrivPerWG + wave;
     if (wave < kPrivPerWG && pi < a.n_private)
       private_item_ring(a, pi, threadIdx.x & 63, lds + wave * kPrivWaveBytes);
     return;
   }
-  const int b = blockIdx.x - n_priv_slots, per_xcd = (gridDim.x - n_priv_slots) / 8;
+  const int b = bid - shared0, per_xcd = n_shared_slots / 8;
+  if (b < 0 || b >= n_shared_slots) return;
   const int item = (b % 8) * per_xcd + b / 8;
   if (item >= a.n_shared) return;
   const SharedItem si = shared_item(a, item);
@@ -1045,6 +1052,18 @@ __global__ __launch_bounds__(256) void merge_kernel(PlanDev dev, TO *out, float 
 
 }  // namespace
 
+// Compute units of the current device (cached per device).
+int num_cus() {
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    cus[dev] = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0 ? n : 256;
+  }
+  return cus[dev];
+}
+
 PlanDev plan_dev(const Plan &P, void *workspace) {
   unsigned char *ws = (unsigned char *)workspace;
   PlanDev d;
@@ -1062,7 +1081,7 @@ PlanDev plan_dev(const Plan &P, void *workspace) {
 hipError_t launch_branch_attention(const Plan &P, const void *q, const void *shared_k,
                                    const void *shared_v, const void *priv_k, const void *priv_v,
                                    void *out, float *lse, void *workspace, hipStream_t stream, bool out_packed) {
-  AttnArgs a;
+  AttnArgs a{};
   a.q = q; a.shared_k = shared_k; a.shared_v = shared_v; a.priv_k = priv_k; a.priv_v = priv_v;
   a.dev = plan_dev(P, workspace);
   a.n_shared = P.num_shared_items();
@@ -1074,10 +1093,23 @@ hipError_t launch_branch_attention(const Plan &P, const void *q, const void *sha
   a.reg = P.regular;
   const bool bf16 = P.attn.dtype == HPD_BF16;
   if (bf16) {
-    // one launch: shared-prefix items, then the private items 8 per workgroup
-    const int n_priv_wg = (a.n_private + kPrivPerWG - 1) / kPrivPerWG;
-    const int nwg = (n_priv_wg + 7) / 8 * 8 + (a.n_shared + 7) / 8 * 8;
-    if (nwg > 0) launch(KK_SHARED, shared_prefix_ring_kernel, dim3(nwg), dim3(512), stream, a);
+    // one launch: the private items (kPrivPerWG per workgroup) and the
+    // shared-prefix items; phase isolation: the shared items, then the
+    // private items, in launches of their own
+    auto grid = [](const AttnArgs &x) {
+      const int n_priv_wg = (x.n_private + kPrivPerWG - 1) / kPrivPerWG;
+      return (n_priv_wg + 7) / 8 * 8 + (x.n_shared + 7) / 8 * 8;
+    };
+    a.priv_first = grid(a) <= num_cus() ? 1 : 0;
+    if (attn_phase_isolation()) {
+      AttnArgs sh = a, pr = a;
+      sh.n_private = 0;
+      pr.n_shared = 0;
+      if (sh.n_shared > 0) launch(KK_SHARED, shared_prefix_ring_kernel, dim3(grid(sh)), dim3(512), stream, sh);
+      if (pr.n_private > 0) launch(KK_PRIVATE, shared_prefix_ring_kernel, dim3(grid(pr)), dim3(512), stream, pr);
+    } else if (grid(a) > 0) {
+      launch(KK_SHARED, shared_prefix_ring_kernel, dim3(grid(a)), dim3(512), stream, a);
+    }
   } else {
     if (a.n_shared > 0)
       launch(KK_SHARED, shared_prefix_kernel<float>, dim3((a.n_shared + 7) / 8 * 8), dim3(256), stream, a);

@@ -43,6 +43,7 @@ struct TimedEvents {
   hipEvent_t start = nullptr, stop = nullptr;
 };
 TimedEvents timed_events(int kind);
+bool attn_phase_isolation();   // hpd_attn_phase_isolation
 
 template <typename... KArgs, typename... Args>
 void launch(int kind, void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t stream, Args... args) {

@@ -6,6 +6,7 @@
 // nothing.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -22,6 +23,7 @@ struct Pair {
 
 std::mutex g_mu;
 bool g_enabled = false;
+std::atomic<bool> g_phase_isolation{false};
 std::vector<Pair> g_pool;
 size_t g_used = 0;
 double g_total_ms[HPD_NUM_KERNEL_KINDS] = {};
@@ -49,9 +51,16 @@ TimedEvents timed_events(int kind) {
   return ev;
 }
 
+bool attn_phase_isolation() { return g_phase_isolation.load(std::memory_order_relaxed); }
+
 }  // namespace hpd
 
 extern "C" {
+
+hpd_status hpd_attn_phase_isolation(int enable) {
+  hpd::g_phase_isolation.store(enable != 0, std::memory_order_relaxed);
+  return HPD_OK;
+}
 
 hpd_status hpd_kernel_timing(int enable, int max_launches) {
   std::lock_guard<std::mutex> lk(hpd::g_mu);

@@ -85,3 +85,38 @@ def test_decode_graph_replays(packed):
         for l in range(len(pk)):
             assert torch.equal(pk[l], eager_k[l])
         assert torch.isfinite(noise)
+
+
+def test_phase_isolation_is_bit_identical():
+    """The phase-isolated launch order (shared-prefix items, then private
+    items, as two launches) gives the same bits as the co-scheduled launch."""
+    announce("phase isolation: attention c3 + decode small stack")
+    from paper_2607_18839_amd import _lib
+    from paper_2607_18839_amd.torch_api import BranchAttention, DecodeStep
+    b = make_attn_batch("c3", 1)
+    layer = BranchAttention(b.num_q_heads, b.num_kv_heads, b.prefix_len, b.branch_page, b.num_new, b.past_len)
+    ins = [to_dev(getattr(b, f), "bf16") for f in ("q", "shared_k", "shared_v", "priv_k", "priv_v")]
+    lse0 = torch.empty((layer.T, b.num_q_heads), dtype=torch.float32, device="cuda")
+    lse1 = torch.empty_like(lse0)
+    inp = small_inputs(6, layers=2)
+    w = {k: [to_dev(a, "bf16") for a in getattr(inp, k)] for k in ("w_qkv", "w_o", "w_gate", "w_up", "w_down")}
+    step = DecodeStep(inp.num_q_heads, inp.num_kv_heads, inp.prefix_len, inp.branch_page, inp.num_new,
+                      inp.past_len, w, inp.hidden, inp.intermediate, inp.rms_eps, packed=True)
+    sk = [to_dev(a, "bf16") for a in inp.shared_k]
+    sv = [to_dev(a, "bf16") for a in inp.shared_v]
+    h = torch.from_numpy(inp.hidden_in).cuda()
+    outs = []
+    try:
+        for iso in (False, True):
+            _lib.hpd_attn_phase_isolation(iso)
+            o = layer(*ins, lse=lse1 if iso else lse0).clone()
+            pk = [to_dev(a, "bf16") for a in inp.priv_k]
+            pv = [to_dev(a, "bf16") for a in inp.priv_v]
+            d = step(h, sk, sv, pk, pv).clone()
+            torch.cuda.synchronize()
+            outs.append((o, d, pk))
+    finally:
+        _lib.hpd_attn_phase_isolation(False)
+    assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(lse0, lse1)
+    assert torch.equal(outs[0][1], outs[1][1])
+    assert all(torch.equal(x, y) for x, y in zip(outs[0][2], outs[1][2]))
