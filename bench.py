@@ -1,6 +1,6 @@
 """Benchmark of the branch-parallel decode step on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4|c3|c5|c2|c1]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4|c3|c3f|c5|c2|c1]
 
 A step is one pass of the whole hot path over one batch of seeded synthetic
 input already resident in HBM.  The default workload is c4, the full decode
@@ -51,18 +51,18 @@ def parse():
 
 # ----------------------------------------------------------------- algorithmic work
 
-def attn_work(prefix_len, branch_page, num_new, past_len, Hq, Hkv, D, s_in, s_out):
+def attn_work(prefix_len, branch_page, num_new, past_len, Hq, Hkv, D, s_in, s_out, fork_len=None):
     """Algorithmic FLOPs / bytes of the shared and private phases (method's
-    definition: what must be read and computed, not implementation scratch)."""
+    definition: what must be read and computed, not implementation scratch).
+    With fork offsets a branch's tokens meet only its F_b visible prefix keys."""
     prefix_len = np.asarray(prefix_len, np.int64)
     num_new = np.asarray(num_new, np.int64)
     past_len = np.asarray(past_len, np.int64)
     T = int(num_new.sum())
-    page_T = np.zeros(len(prefix_len), np.int64)
-    np.add.at(page_T, np.asarray(branch_page), num_new)
     q_bytes = T * Hq * D * s_in
     o_bytes = T * Hq * D * s_out
-    shared_flop = int(4 * Hq * D * np.sum(page_T * prefix_len))
+    F = prefix_len[np.asarray(branch_page)] if fork_len is None else np.asarray(fork_len, np.int64)
+    shared_flop = int(4 * Hq * D * np.sum(num_new * F))
     shared_bytes = int(2 * prefix_len.sum() * Hkv * D * s_in + q_bytes + o_bytes)
     priv_keys = past_len + num_new
     private_bytes = int(2 * priv_keys.sum() * Hkv * D * s_in + q_bytes + o_bytes)
@@ -200,7 +200,7 @@ def bench_attention(args, torch, _lib):
     tdt = torch.bfloat16 if b.dtype == "bf16" else torch.float32
     s_in = 2 if b.dtype == "bf16" else 4
     layer = BranchAttention(b.num_q_heads, b.num_kv_heads, b.prefix_len, b.branch_page, b.num_new,
-                            b.past_len, dtype=tdt)
+                            b.past_len, dtype=tdt, fork_len=b.fork_len)
 
     def dev(a):
         if b.dtype == "bf16":
@@ -220,7 +220,7 @@ def bench_attention(args, torch, _lib):
     ms, timed, pct = _graph_time(torch, step, reps, args.steps, args.warmup)
     kern = _kernel_pass(torch, _lib, step, min(args.steps, 20), args.warmup, queue_cycles=2_000_000)
     w = attn_work(b.prefix_len, b.branch_page, b.num_new, b.past_len, b.num_q_heads, b.num_kv_heads, 64,
-                  s_in, s_in)
+                  s_in, s_in, b.fork_len)
     peak_mfma = BF16_PEAK_TFLOPS if b.dtype == "bf16" else FP32_PEAK_TFLOPS
     sh = kern.get("shared_prefix", {}).get("avg_us")
     pr = kern.get("private", {}).get("avg_us")
@@ -250,6 +250,9 @@ def bench_attention(args, torch, _lib):
                    "branches": b.num_branches, "branch_tokens": w["T"],
                    "prefix_len_total": int(b.prefix_len.sum()),
                    "private_rows": int((b.past_len + b.num_new).sum()), "heads": [b.num_q_heads, b.num_kv_heads, 64],
+                   "fork_offsets": None if b.fork_len is None else
+                   {"visible_prefix_keys": int(np.asarray(b.fork_len, np.int64).sum()),
+                    "rule": "layout branch whole prefix; content branches uniform in [1024, P]"},
                    "cache": "warm" if args.warm else f"cold ({reps} input replicas rotated)"},
         "roofline": roof, "kernels": kern,
     }

@@ -706,8 +706,11 @@ __global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
     if (i + 1 < ntiles) ld.store(lds[(i + 1) & 1], tid);
     __syncthreads();
   }
-  const int64_t prow = valid ? ((int64_t)a.dev.token_slots[2 * t] + slot) * a.Hq + hq : 0;
-  if (wave_active) w.write(a.dev.part_o, a.dev.part_lse, prow, valid);
+  // a row writes its partial of this split only if it sees the split's first
+  // key (fork offsets: the planner gives it no slot otherwise)
+  const bool writes = valid && limit > key0;
+  const int64_t prow = writes ? ((int64_t)a.dev.token_slots[2 * t] + slot) * a.Hq + hq : 0;
+  if (wave_active) w.write(a.dev.part_o, a.dev.part_lse, prow, writes);
 }
 
 // bf16 shared-prefix kernel: same items and arithmetic as shared_prefix_kernel,
@@ -816,7 +819,9 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   if (npairs > 1) issue(1);
   if (npairs > 2) issue(2);
   wait_pair(min(npairs - 1, 2));
-  const int my_prow = valid ? (my_slots + slot) * a.Hq + hq : -1;
+  // a row writes its partial of this split only if it sees the split's first
+  // key (fork offsets: the planner gives it no slot otherwise)
+  const int my_prow = valid && limit > key0 ? (my_slots + slot) * a.Hq + hq : -1;
   ring_barrier();   // pair 0 visible to every wave
   f32x16 s_cur[2], s_next[2];
   if (wave_active && par < ntiles) w.qk_ring(lds + par * kTile, s_cur, lane);

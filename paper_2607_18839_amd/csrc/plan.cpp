@@ -168,11 +168,19 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
         ceil_div(ceil_div(P.prefix_len[p], page_splits[p]), kSharedSplitUnit)) : 0;
     if (page_split_keys[p] > 0) page_splits[p] = (int32_t)ceil_div(P.prefix_len[p], page_split_keys[p]);
   }
+  // Shared splits a branch sees: those starting below its visible prefix
+  // (all of its page's splits without fork offsets).  Its tokens' partial
+  // slots are those splits, then its private chunks.
+  std::vector<int32_t> vis_splits(nb);
+  for (int i = 0; i < nb; ++i) {
+    const int p = P.branch_page[i];
+    vis_splits[i] = page_split_keys[p] > 0 ? (int32_t)ceil_div((int64_t)P.fork[i], page_split_keys[p]) : 0;
+  }
   P.token_slots.resize(2 * (size_t)P.T);
   int64_t slot = 0;
   for (int i = 0; i < nb; ++i) {
     const int chunks = (int)ceil_div((int64_t)P.past_len[i] + P.num_new[i], kPrivateChunkKeys);
-    const int cnt = page_splits[P.branch_page[i]] + chunks;
+    const int cnt = vis_splits[i] + chunks;
     for (int j = 0; j < P.num_new[i]; ++j) {
       P.token_slots[2 * (size_t)(P.q_row[i] + j)] = (int32_t)slot;
       P.token_slots[2 * (size_t)(P.q_row[i] + j) + 1] = cnt;
@@ -184,7 +192,11 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
     return fail(err, HPD_ERR_INVALID_ARGUMENT, "too many partial rows");
 
   // ---- shared-prefix work items: (page, kv head, key split, row group);
-  // items that read the same key range are adjacent.
+  // items that read the same key range are adjacent.  With fork offsets an
+  // item's key range ends at the largest visible prefix among its rows, an
+  // item no row of which sees its first key is not emitted, and a row writes
+  // its partial of the split only if it sees the split's first key (the
+  // kernels apply the same rule).
   const int group_rows = kSharedWaves * kTileRows;
   for (int p = 0; p < np; ++p) {
     const int Pp = P.prefix_len[p];
@@ -194,11 +206,17 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
       for (int s = 0; s < page_splits[p]; ++s)
         for (int r0 = 0; r0 < R; r0 += group_rows) {
           const int nr = std::min(group_rows, R - r0);
-          const int k0 = s * page_split_keys[p], k1 = std::min(Pp, k0 + page_split_keys[p]);
+          const int k0 = s * page_split_keys[p];
+          int k1 = std::min(Pp, k0 + page_split_keys[p]);
           int flags = 0;
-          if (P.has_fork)
+          if (P.has_fork) {
+            int max_fork = 0;
+            for (int r = r0; r < r0 + nr; ++r) max_fork = std::max(max_fork, P.token_fork[P.page_q_row[p] + r / G]);
+            if (max_fork <= k0) continue;
+            k1 = std::min(k1, max_fork);
             for (int r = r0; r < r0 + nr; ++r)
               if (P.token_fork[P.page_q_row[p] + r / G] < k1) flags |= SI_FLAG_FORK;
+          }
           int32_t it[SI_NFIELDS] = {};
           it[SI_PAGE] = p; it[SI_KVH] = g; it[SI_ROW0] = r0; it[SI_NROWS] = nr;
           it[SI_KEY0] = k0; it[SI_KEY1] = k1; it[SI_SLOT] = s; it[SI_FLAGS] = flags;
@@ -223,7 +241,7 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   for (int i = 0; i < nb; ++i) {
     const int keys = P.past_len[i] + P.num_new[i];
     const int R = P.num_new[i] * G;
-    const int splits = page_splits[P.branch_page[i]];
+    const int splits = vis_splits[i];
     for (int g = 0; g < Hkv; ++g)
       for (int r0 = 0; r0 < R; r0 += kTileRows)
         for (int c = 0; c * kPrivateChunkKeys < keys; ++c) {

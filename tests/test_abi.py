@@ -206,3 +206,47 @@ def test_single_page_items_follow_the_index_formula(name, st, Hq, Hkv):
                     page_q_row=0)
         for k, v in want.items():
             assert it[S[k]] == v, (i, k, it[S[k]], v)
+
+
+@pytest.mark.parametrize("name,st", _structures(), ids=lambda x: x if isinstance(x, str) else "")
+@pytest.mark.parametrize("Hq,Hkv", [(16, 2), (4, 4)])
+def test_fork_work_lists_cover_visible_keys_once(name, st, Hq, Hkv):
+    """With fork offsets: each (token, head) row meets each of its F_b visible
+    shared keys in exactly one item, and each of its partial slots is written
+    exactly once, a row writing a shared split's partial only when it sees
+    the split's first key (the kernels' rule)."""
+    G = Hq // Hkv
+    rng = np.random.default_rng(len(st["num_new"]) * 7 + Hq)
+    P_b = st["prefix_len"][st["branch_page"]]
+    fork = np.array([rng.integers(0, P + 1) for P in P_b], np.int32)
+    if len(fork) > 1:
+        fork[0], fork[1] = 0, P_b[1]
+    info = _lib.hpd_plan_query(_plan(st, Hq, Hkv, fork_len=fork))
+    T = info["T"]
+    cp = canonical_plan(st["prefix_len"], st["branch_page"], st["num_new"], st["past_len"], fork)
+    tb = cp["token_branch"]
+    S, Pi = _lib.SI, _lib.PI
+    slot_writes = np.zeros((info["num_partial_slots"], Hq), np.int64)
+    cov = [np.zeros((Hq, int(fork[tb[t]])), np.int64) for t in range(T)]
+    for it in info["shared_items"]:
+        p, g, k0, k1 = it[S["page"]], it[S["kvh"]], it[S["key0"]], it[S["key1"]]
+        assert k0 < k1
+        for r in range(it[S["row0"]], it[S["row0"]] + it[S["nrows"]]):
+            t = cp["page_q_row"][p] + r // G
+            h = g * G + r % G
+            F = int(fork[tb[t]])
+            cov[t][h, k0:min(k1, F)] += 1
+            if F > k0:
+                first, cnt = info["token_slots"][t]
+                assert 0 <= it[S["slot"]] < cnt
+                slot_writes[first + it[S["slot"]], h] += 1
+    for it in info["private_items"]:
+        b, g = it[Pi["branch"]], it[Pi["kvh"]]
+        for r in range(it[Pi["row0"]], it[Pi["row0"]] + it[Pi["nrows"]]):
+            t = cp["q_row"][b] + r // G
+            first, cnt = info["token_slots"][t]
+            assert 0 <= it[Pi["slot"]] < cnt
+            slot_writes[first + it[Pi["slot"]], g * G + r % G] += 1
+    for t in range(T):
+        assert np.all(cov[t] == 1), t
+    assert np.all(slot_writes == 1)

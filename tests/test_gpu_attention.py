@@ -22,12 +22,12 @@ def _need_gpu():
         pytest.skip("no GPU")
 
 
-@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c5"])
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c3f", "c5"])
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_workload_parity(name, seed):
     announce(f"workload {name} seed {seed}")
     b = make_attn_batch(name, seed)
-    O, lse = run_batch(b)
+    O, lse = run_batch(b, fork_len=b.fork_len)
     Oref, lref = attention_for_batch(b)
     mx, rl = assert_parity(O, Oref, b.dtype, f"{name}/{seed}")
     assert np.abs(lse - lref).max() <= LSE_ABS

@@ -83,3 +83,20 @@ def test_packing_shapes():
     assert b.priv_k.shape == (int((b.past_len + b.num_new).sum()), 2, 64)
     c1 = make_attn_batch("c1", 0)
     assert c1.q.dtype == np.float32 and list(c1.past_len) == [8, 16, 32, 32]
+
+
+def test_fork_workload_extends_c3():
+    """c3f is c3 (same structure and values for a seed) plus fork offsets:
+    the layout branch sees the whole prefix, content branches a uniform
+    integer in [1024, P]."""
+    for seed in (0, 1):
+        a, b = make_attn_batch("c3", seed), make_attn_batch("c3f", seed)
+        assert a.fork_len is None
+        for f in ("prefix_len", "branch_page", "num_new", "past_len", "q", "shared_k", "shared_v", "priv_k",
+                  "priv_v"):
+            assert np.array_equal(getattr(a, f), getattr(b, f)), f
+        P = int(b.prefix_len[0])
+        assert b.fork_len.dtype == np.int32 and b.fork_len.shape == (b.num_branches,)
+        assert b.fork_len[b.is_layout].tolist() == [P]
+        c = b.fork_len[~b.is_layout]
+        assert c.min() >= 1024 and c.max() <= P and len(set(c.tolist())) > 20

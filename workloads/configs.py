@@ -61,6 +61,19 @@ CONFIGS = {
         model=dict(num_layers=18, hidden=1024, intermediate=3072,
                    weight_std=0.02, rms_eps=1e-6),
     ),
+    # c3 with per-branch fork offsets (tree-shaped prefix): a content branch
+    # sees the page's prefix only up to its fork point F_b, drawn uniform in
+    # [1024, P] (1024 = the visual-token part every branch sees); the layout
+    # branch sees the whole prefix.  Drawn after all of c3's values, so the
+    # structure and values equal c3's for the same seed.
+    "c3f": dict(
+        name="c3f", dtype="bf16", num_q_heads=16, num_kv_heads=2, head_dim=64,
+        num_pages=1, prefix=("fixed", 4096),
+        layout=dict(k=1, past=("fixed", 512)),
+        content_count=("fixed", 32), content_k=4,
+        content_past=("lognormal", 128.0, 1.0, 8, 1024),
+        fork=dict(visual=1024),
+    ),
     # Ragged multi-page batch: 16 pages, prefix U[1024, 4096], 4..32 content branches.
     "c5": dict(
         name="c5", dtype="bf16", num_q_heads=16, num_kv_heads=2, head_dim=64,

@@ -186,16 +186,31 @@ def attn_batch_from_structure(structure, num_q_heads, num_kv_heads, head_dim,
                      **vals)
 
 
+def draw_fork_len(structure, visual, rng):
+    """Per-branch visible prefix F_b: the layout branch sees its page's whole
+    prefix, a content branch a uniform integer in [min(visual, P), P]."""
+    out = []
+    for b, p in enumerate(structure["branch_page"]):
+        P = int(structure["prefix_len"][p])
+        if structure["is_layout"][b]:
+            out.append(P)
+        else:
+            out.append(int(rng.integers(min(visual, P), P + 1)))
+    return np.asarray(out, dtype=np.int32)
+
+
 def make_attn_batch(cfg_or_name, seed):
-    """Structure then values of one single-layer workload, from one stream."""
+    """Structure then values (then fork offsets, if the workload has them) of
+    one single-layer workload, from one stream."""
     cfg = get_config(cfg_or_name) if isinstance(cfg_or_name, str) else cfg_or_name
     rng = np.random.default_rng(seed)
     st = make_structure(cfg, rng)
     vals = _values_for(st, cfg["num_q_heads"], cfg["num_kv_heads"], cfg["head_dim"],
                        cfg["dtype"], rng)
+    fork = draw_fork_len(st, cfg["fork"]["visual"], rng) if cfg.get("fork") else None
     return AttnBatch(name=cfg["name"], seed=seed, dtype=cfg["dtype"],
                      num_q_heads=cfg["num_q_heads"], num_kv_heads=cfg["num_kv_heads"],
-                     head_dim=cfg["head_dim"], **st, **vals)
+                     head_dim=cfg["head_dim"], fork_len=fork, **st, **vals)
 
 
 @dataclass
