@@ -62,7 +62,8 @@ typedef enum {
   HPD_ERR_UNSUPPORTED = 2,
   HPD_ERR_WORKSPACE_TOO_SMALL = 3,
   HPD_ERR_HIP = 4,
-  HPD_ERR_HOST_ALLOC = 5
+  HPD_ERR_HOST_ALLOC = 5,
+  HPD_ERR_OUT_OF_BLOCKS = 6
 } hpd_status;
 
 typedef enum { HPD_F32 = 0, HPD_BF16 = 1 } hpd_dtype;
@@ -76,6 +77,26 @@ typedef struct {
   int32_t dtype;         /* hpd_dtype of q, shared_k/v, priv_k/v              */
   int32_t out_dtype;     /* hpd_dtype of out                                  */
 } hpd_attn_desc;
+
+/* Paged K/V (the paged-KV memory model of the inference workflow: section
+ * "Inference Workflow", Algorithm 1, where a forked branch shares its page's
+ * prefix by reference and keeps only its own incremental KV).  K and V rows
+ * live in blocks of block_rows rows of a pool: shared_k/v and priv_k/v are
+ * then the pool bases ([num_blocks * block_rows][Hkv][D]; the same pool may
+ * be passed for both).  Row i of page p's prefix is pool row
+ * blocks[page_block0[p] + i / block_rows] * block_rows + i % block_rows, and
+ * row i of branch b's private rows (its L_b past rows, then its k_b new rows)
+ * likewise from branch_block0[b].  Page p uses ceil(P_p / block_rows) entries
+ * of `blocks`, branch b ceil((L_b + k_b) / block_rows).  HOST arrays, read
+ * only inside hpd_plan_create.  hpd_kv_pool below manages such blocks. */
+typedef struct {
+  int32_t block_rows;            /* rows per block, a positive multiple of 64  */
+  int32_t num_blocks;            /* blocks in the pool(s); ids 0..num_blocks-1 */
+  int32_t num_entries;           /* length of `blocks`                         */
+  const int32_t *blocks;         /* [num_entries] block ids                    */
+  const int32_t *page_block0;    /* [num_pages] first entry of page p          */
+  const int32_t *branch_block0;  /* [num_branches] first entry of branch b     */
+} hpd_paged_kv;
 
 /* A ragged batch of pages and branches.  HOST arrays, read only inside
  * hpd_plan_create.  Branches are grouped by page (branch_page non-decreasing);
@@ -92,6 +113,8 @@ typedef struct {
   const int64_t *priv_row;    /* [nb] first private row of branch b;
                                  NULL = packed (exclusive sum of L_b + k_b)    */
   const int32_t *fork_len;    /* [nb] visible prefix F_b in 0..P_p; NULL = P_p */
+  const hpd_paged_kv *paged;  /* NULL = contiguous rows (prefix_row, priv_row);
+                                 else paged K/V, prefix_row and priv_row NULL  */
 } hpd_batch_desc;
 
 /* Opaque, immutable execution plan: the canonical ragged bookkeeping (row
@@ -110,8 +133,9 @@ typedef struct {
   const int32_t *page_q_row;      /* [num_pages] first token of page p         */
   const int32_t *page_T;          /* [num_pages] tokens of page p              */
   const int32_t *visible;         /* [T] keys seen by token t: F_b + L_b + j + 1 */
-  int64_t shared_rows;            /* rows shared_k/v must hold (max end row)   */
-  int64_t priv_rows;              /* rows priv_k/v must hold (max end row)     */
+  int64_t shared_rows;            /* rows shared_k/v must hold (max end row;
+                                     paged: the pool, num_blocks * block_rows) */
+  int64_t priv_rows;              /* rows priv_k/v must hold (likewise)        */
   int32_t num_shared_items;       /* work items of the shared-prefix kernel    */
   int32_t num_private_items;      /* work items of the private kernel          */
   const int32_t *shared_items;    /* [num_shared_items][12] fields: csrc/plan.h  */
@@ -280,6 +304,54 @@ const char *hpd_kernel_kind_name(int kind);
  * Results are bit-identical either way.  Not to be changed while a step is
  * being enqueued or captured. */
 hpd_status hpd_attn_phase_isolation(int enable);
+
+/* Host manager of paged K/V blocks (section "Inference Workflow",
+ * Algorithm 1: KV owned per request, a forked branch sharing its page's
+ * prefix by reference, rejected drafts rolled back).  A pool hands out block
+ * ids 0..num_blocks-1 of block_rows rows each; the device K/V pools
+ * themselves are the caller's.  A sequence is either a root (a page's
+ * prefix) or a branch forked from a root: the branch sees the root's first
+ * fork_len rows without copying them (the root's blocks stay allocated while
+ * any branch forked from it lives) and owns its private rows.  Host memory
+ * only; a pool is not thread-safe.  Freed blocks are reused last-freed
+ * first.
+ *
+ *  hpd_kv_seq_new       parent = -1: new root; else a branch of root
+ *                       `parent` (a live root, not a branch) seeing its first
+ *                       fork_len (0..parent length) rows.  New sequences are
+ *                       empty.
+ *  hpd_kv_seq_reserve   grows a sequence to new_len rows (append), taking
+ *                       blocks from the pool; HPD_ERR_OUT_OF_BLOCKS, with
+ *                       nothing changed, when the pool has too few.
+ *  hpd_kv_seq_truncate  shrinks to new_len rows (rollback of rejected
+ *                       drafts), returning whole blocks past it; a root
+ *                       cannot shrink below a live branch's fork_len.
+ *  hpd_kv_seq_release   ends a sequence: a branch returns its blocks; a root
+ *                       returns its blocks once its last branch is released.
+ *  hpd_kv_seq_info      length, block count, parent (-1 for a root) and
+ *                       fork_len of a live sequence.
+ *  hpd_kv_seq_blocks    copies its block ids (capacity entries at most).
+ *  hpd_kv_batch_tables  fills hpd_paged_kv tables for a batch: the block ids
+ *                       of each page's root, then of each branch,
+ *                       concatenated into blocks_out (capacity entries),
+ *                       with page_block0_out / branch_block0_out; *entries is
+ *                       the length needed (HPD_ERR_INVALID_ARGUMENT if above
+ *                       capacity). */
+typedef struct hpd_kv_pool hpd_kv_pool;
+hpd_status hpd_kv_pool_create(int32_t num_blocks, int32_t block_rows, hpd_kv_pool **out);
+void hpd_kv_pool_destroy(hpd_kv_pool *pool);
+int32_t hpd_kv_pool_free_blocks(const hpd_kv_pool *pool);
+hpd_status hpd_kv_seq_new(hpd_kv_pool *pool, int32_t parent, int32_t fork_len, int32_t *seq);
+hpd_status hpd_kv_seq_reserve(hpd_kv_pool *pool, int32_t seq, int32_t new_len);
+hpd_status hpd_kv_seq_truncate(hpd_kv_pool *pool, int32_t seq, int32_t new_len);
+hpd_status hpd_kv_seq_release(hpd_kv_pool *pool, int32_t seq);
+hpd_status hpd_kv_seq_info(const hpd_kv_pool *pool, int32_t seq, int32_t *len, int32_t *num_blocks,
+                           int32_t *parent, int32_t *fork_len);
+hpd_status hpd_kv_seq_blocks(const hpd_kv_pool *pool, int32_t seq, int32_t *blocks_out, int32_t capacity);
+hpd_status hpd_kv_batch_tables(const hpd_kv_pool *pool, int32_t num_pages, const int32_t *page_seq,
+                               int32_t num_branches, const int32_t *branch_seq, int32_t *blocks_out,
+                               int32_t capacity, int32_t *page_block0_out, int32_t *branch_block0_out,
+                               int32_t *entries);
 
 const char *hpd_status_string(hpd_status status);
 const char *hpd_last_error_message(void);

@@ -19,7 +19,8 @@ HPD_MAX_K = 16
 HPD_HEAD_DIM = 64
 HPD_F32, HPD_BF16 = 0, 1
 STATUS = {0: "HPD_OK", 1: "HPD_ERR_INVALID_ARGUMENT", 2: "HPD_ERR_UNSUPPORTED",
-          3: "HPD_ERR_WORKSPACE_TOO_SMALL", 4: "HPD_ERR_HIP", 5: "HPD_ERR_HOST_ALLOC"}
+          3: "HPD_ERR_WORKSPACE_TOO_SMALL", 4: "HPD_ERR_HIP", 5: "HPD_ERR_HOST_ALLOC",
+          6: "HPD_ERR_OUT_OF_BLOCKS"}
 
 # Work-item record widths and fields (paper_2607_18839_amd/csrc/plan.h).
 SI_NFIELDS = PI_NFIELDS = 12
@@ -44,10 +45,16 @@ class hpd_attn_desc(ctypes.Structure):
                 ("dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32)]
 
 
+class hpd_paged_kv(ctypes.Structure):
+    _fields_ = [("block_rows", ctypes.c_int32), ("num_blocks", ctypes.c_int32), ("num_entries", ctypes.c_int32),
+                ("blocks", c_i32p), ("page_block0", c_i32p), ("branch_block0", c_i32p)]
+
+
 class hpd_batch_desc(ctypes.Structure):
     _fields_ = [("num_pages", ctypes.c_int32), ("prefix_len", c_i32p), ("prefix_row", c_i64p),
                 ("num_branches", ctypes.c_int32), ("branch_page", c_i32p), ("num_new", c_i32p),
-                ("past_len", c_i32p), ("priv_row", c_i64p), ("fork_len", c_i32p)]
+                ("past_len", c_i32p), ("priv_row", c_i64p), ("fork_len", c_i32p),
+                ("paged", ctypes.POINTER(hpd_paged_kv))]
 
 
 class hpd_plan_info(ctypes.Structure):
@@ -96,6 +103,17 @@ SIGNATURES = {
                                         ctypes.c_void_p, ctypes.c_void_p]),
     "hpd_kernel_timing": (ctypes.c_int, [ctypes.c_int, ctypes.c_int]),
     "hpd_attn_phase_isolation": (ctypes.c_int, [ctypes.c_int]),
+    "hpd_kv_pool_create": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_void_p)]),
+    "hpd_kv_pool_destroy": (None, [ctypes.c_void_p]),
+    "hpd_kv_pool_free_blocks": (ctypes.c_int32, [ctypes.c_void_p]),
+    "hpd_kv_seq_new": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, c_i32p]),
+    "hpd_kv_seq_reserve": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32]),
+    "hpd_kv_seq_truncate": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32]),
+    "hpd_kv_seq_release": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32]),
+    "hpd_kv_seq_info": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, c_i32p, c_i32p, c_i32p, c_i32p]),
+    "hpd_kv_seq_blocks": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, c_i32p, ctypes.c_int32]),
+    "hpd_kv_batch_tables": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, c_i32p, ctypes.c_int32, c_i32p,
+                                           c_i32p, ctypes.c_int32, c_i32p, c_i32p, c_i32p]),
     "hpd_kernel_times_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int]),
     "hpd_kernel_kind_name": (ctypes.c_char_p, [ctypes.c_int]),
     "hpd_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -158,18 +176,27 @@ class Plan:
 
 def hpd_plan_create(num_q_heads, num_kv_heads, prefix_len, branch_page, num_new, past_len,
                     head_dim=HPD_HEAD_DIM, softmax_scale=0.0, dtype=HPD_BF16, out_dtype=None,
-                    prefix_row=None, priv_row=None, fork_len=None):
+                    prefix_row=None, priv_row=None, fork_len=None, paged=None):
+    """paged: None, or a dict with block_rows, num_blocks, blocks, page_block0,
+    branch_block0 (hpd_paged_kv)."""
     lib = load()
     attn = hpd_attn_desc(num_q_heads, num_kv_heads, head_dim, softmax_scale, dtype,
                          dtype if out_dtype is None else out_dtype)
     arrs = dict(prefix_len=_i32(prefix_len), branch_page=_i32(branch_page), num_new=_i32(num_new),
                 past_len=_i32(past_len), prefix_row=_i64(prefix_row), priv_row=_i64(priv_row),
                 fork_len=_i32(fork_len))
+    pg = None
+    if paged is not None:
+        for k in ("blocks", "page_block0", "branch_block0"):
+            arrs["pg_" + k] = _i32(paged[k])
+        pg = hpd_paged_kv(int(paged["block_rows"]), int(paged["num_blocks"]), len(arrs["pg_blocks"]),
+                          _ptr(arrs["pg_blocks"], c_i32p), _ptr(arrs["pg_page_block0"], c_i32p),
+                          _ptr(arrs["pg_branch_block0"], c_i32p))
     batch = hpd_batch_desc(len(arrs["prefix_len"]), _ptr(arrs["prefix_len"], c_i32p),
                            _ptr(arrs["prefix_row"], c_i64p), len(arrs["num_new"]),
                            _ptr(arrs["branch_page"], c_i32p), _ptr(arrs["num_new"], c_i32p),
                            _ptr(arrs["past_len"], c_i32p), _ptr(arrs["priv_row"], c_i64p),
-                           _ptr(arrs["fork_len"], c_i32p))
+                           _ptr(arrs["fork_len"], c_i32p), None if pg is None else ctypes.pointer(pg))
     h = ctypes.c_void_p()
     _check(lib.hpd_plan_create(ctypes.byref(attn), ctypes.byref(batch), ctypes.byref(h)), "hpd_plan_create")
     return Plan(h, attn)
@@ -283,3 +310,63 @@ def declared_symbols(header=None):
 
 def hpd_attn_phase_isolation(enable):
     _check(load().hpd_attn_phase_isolation(1 if enable else 0), "hpd_attn_phase_isolation")
+
+
+class KvPool:
+    """hpd_kv_pool: host manager of paged K/V block ids (the device pools are
+    the caller's).  Sequences are roots (a page's prefix) or branches forked
+    from a root."""
+
+    def __init__(self, num_blocks, block_rows):
+        h = ctypes.c_void_p()
+        _check(load().hpd_kv_pool_create(num_blocks, block_rows, ctypes.byref(h)), "hpd_kv_pool_create")
+        self.handle, self.num_blocks, self.block_rows = h, int(num_blocks), int(block_rows)
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.hpd_kv_pool_destroy(self.handle)
+            self.handle = None
+
+    def free_blocks(self):
+        return int(load().hpd_kv_pool_free_blocks(self.handle))
+
+    def new(self, parent=-1, fork_len=0):
+        out = ctypes.c_int32()
+        _check(load().hpd_kv_seq_new(self.handle, parent, fork_len, ctypes.byref(out)), "hpd_kv_seq_new")
+        return out.value
+
+    def reserve(self, seq, new_len):
+        _check(load().hpd_kv_seq_reserve(self.handle, seq, new_len), "hpd_kv_seq_reserve")
+
+    def truncate(self, seq, new_len):
+        _check(load().hpd_kv_seq_truncate(self.handle, seq, new_len), "hpd_kv_seq_truncate")
+
+    def release(self, seq):
+        _check(load().hpd_kv_seq_release(self.handle, seq), "hpd_kv_seq_release")
+
+    def info(self, seq):
+        v = [ctypes.c_int32() for _ in range(4)]
+        _check(load().hpd_kv_seq_info(self.handle, seq, *[ctypes.byref(x) for x in v]), "hpd_kv_seq_info")
+        return dict(len=v[0].value, num_blocks=v[1].value, parent=v[2].value, fork_len=v[3].value)
+
+    def blocks(self, seq):
+        n = self.info(seq)["num_blocks"]
+        out = np.zeros(max(n, 1), np.int32)
+        _check(load().hpd_kv_seq_blocks(self.handle, seq, _ptr(out, c_i32p), n), "hpd_kv_seq_blocks")
+        return out[:n]
+
+    def batch_tables(self, page_seqs, branch_seqs):
+        """hpd_paged_kv fields (a dict for hpd_plan_create's `paged`)."""
+        ps, bs = _i32(page_seqs), _i32(branch_seqs)
+        n = ctypes.c_int32()
+        p0, b0 = np.zeros(max(len(ps), 1), np.int32), np.zeros(max(len(bs), 1), np.int32)
+        lib = load()
+        st = lib.hpd_kv_batch_tables(self.handle, len(ps), _ptr(ps, c_i32p), len(bs), _ptr(bs, c_i32p), None, 0,
+                                     _ptr(p0, c_i32p), _ptr(b0, c_i32p), ctypes.byref(n))
+        blocks = np.zeros(max(n.value, 1), np.int32)
+        if st != 0 or n.value > 0:
+            _check(lib.hpd_kv_batch_tables(self.handle, len(ps), _ptr(ps, c_i32p), len(bs), _ptr(bs, c_i32p),
+                                           _ptr(blocks, c_i32p), n.value, _ptr(p0, c_i32p), _ptr(b0, c_i32p),
+                                           ctypes.byref(n)), "hpd_kv_batch_tables")
+        return dict(block_rows=self.block_rows, num_blocks=self.num_blocks, blocks=blocks[:n.value],
+                    page_block0=p0[:len(ps)], branch_block0=b0[:len(bs)])

@@ -43,6 +43,7 @@ const char *hpd_status_string(hpd_status s) {
     case HPD_ERR_WORKSPACE_TOO_SMALL: return "HPD_ERR_WORKSPACE_TOO_SMALL";
     case HPD_ERR_HIP: return "HPD_ERR_HIP";
     case HPD_ERR_HOST_ALLOC: return "HPD_ERR_HOST_ALLOC";
+    case HPD_ERR_OUT_OF_BLOCKS: return "HPD_ERR_OUT_OF_BLOCKS";
   }
   return "HPD_ERR_UNKNOWN";
 }

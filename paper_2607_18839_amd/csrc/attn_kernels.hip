@@ -623,7 +623,16 @@ struct AttnArgs {
   float c;   // softmax scale * log2(e)
   Plan::RegularShared reg;
   int priv_first;   // bf16 kernel: private workgroups take the first grid slots
+  int paged;        // K/V rows through the plan's tile tables
 };
+
+// K/V row of key i of a sequence (a page's prefix or a branch's private
+// rows) whose item field `base` is its first row, or with paged K/V its first
+// tile-table entry; i0 is the first key of i's 64-key tile (a multiple of 64),
+// so the table entry is wave-uniform.
+__device__ __forceinline__ int64_t kv_row(const AttnArgs &a, const int32_t *tiles, int base, int i0, int i) {
+  return a.paged ? (int64_t)tiles[base + (i0 >> 6)] + (i - i0) : (int64_t)base + i;
+}
 
 // Fields of shared work item `item`: computed from its index for a regular
 // plan (one page, no fork offsets: items ordered kv head, split, row group),
@@ -684,23 +693,24 @@ __global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
   const int wmin = wave_min(valid ? limit : key1);
 
   const int64_t stride = (int64_t)a.Hkv * D;
-  const T *kbase = (const T *)a.shared_k + ((int64_t)prefix_row * a.Hkv + g) * D;
-  const T *vbase = (const T *)a.shared_v + ((int64_t)prefix_row * a.Hkv + g) * D;
+  const T *kbase = (const T *)a.shared_k + (int64_t)g * D;
+  const T *vbase = (const T *)a.shared_v + (int64_t)g * D;
+  auto row = [&](int k0) { return kv_row(a, a.dev.shared_tiles, prefix_row, k0, k0) * stride; };
 
   WaveAttn<T> w;
   w.init((const T *)a.q + ((int64_t)t * a.Hq + hq) * D, valid, lane);
 
   TileLoader<T, NT> ld;
   const int ntiles = (key1 - key0 + 63) / 64;
-  ld.load(kbase + (int64_t)key0 * stride, stride, key1 - key0, tid);
-  ld.load_v(vbase + (int64_t)key0 * stride, stride, key1 - key0, tid);
+  ld.load(kbase + row(key0), stride, key1 - key0, tid);
+  ld.load_v(vbase + row(key0), stride, key1 - key0, tid);
   ld.store(lds[0], tid);
   __syncthreads();
   for (int i = 0; i < ntiles; ++i) {
     const int k0 = key0 + 64 * i;
     if (i + 1 < ntiles) {
-      ld.load(kbase + (int64_t)(k0 + 64) * stride, stride, key1 - k0 - 64, tid);
-      ld.load_v(vbase + (int64_t)(k0 + 64) * stride, stride, key1 - k0 - 64, tid);
+      ld.load(kbase + row(k0 + 64), stride, key1 - k0 - 64, tid);
+      ld.load_v(vbase + row(k0 + 64), stride, key1 - k0 - 64, tid);
     }
     if (wave_active) w.tile(lds[i & 1], k0, limit, k0 + 64 > wmin, a.c, lane);
     if (i + 1 < ntiles) ld.store(lds[(i + 1) & 1], tid);
@@ -781,8 +791,8 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   const int wmin = wave_min(valid ? limit : key1);
 
   const int64_t stride = (int64_t)a.Hkv * D;
-  const T *kbase = (const T *)a.shared_k + ((int64_t)prefix_row * a.Hkv + g) * D;
-  const T *vbase = (const T *)a.shared_v + ((int64_t)prefix_row * a.Hkv + g) * D;
+  const T *kbase = (const T *)a.shared_k + (int64_t)g * D;
+  const T *vbase = (const T *)a.shared_v + (int64_t)g * D;
   int voff[2];
   WaveAttn<T>::vt_offsets(lane, voff);
 
@@ -792,10 +802,16 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   const int kq0 = Tl::kchunk(crow, pch), kq1 = Tl::kchunk(crow + 8, pch);
   const int vq0 = vchunk(crow, pch), vq1 = vchunk(crow + 8, pch);
   const int ntiles = (key1 - key0 + 63) / 64, npairs = (ntiles + 1) / 2;
+  // paged K/V: lane l holds the pool row of the item's tile l (at most 64
+  // tiles per item), read with a uniform lane index when a tile is issued
+  const int tile_row = a.paged && lane < ntiles ? a.dev.shared_tiles[prefix_row + (key0 >> 6) + lane] : 0;
   auto issue = [&](int j) {
     unsigned char *st = lds + (j % S) * kPair + par * kTile;
     const int k0 = key0 + 64 * (2 * j + par);
-    const int64_t r0 = min(k0 + crow, key1 - 1), r1 = min(k0 + crow + 8, key1 - 1);
+    // the last pair's missing odd tile re-reads the item's last tile
+    const int ti = min(2 * j + par, ntiles - 1), kt = key0 + 64 * ti;
+    const int64_t base = a.paged ? (int64_t)__builtin_amdgcn_readlane(tile_row, ti) : (int64_t)prefix_row + kt;
+    const int64_t r0 = base + (min(k0 + crow, key1 - 1) - kt), r1 = base + (min(k0 + crow + 8, key1 - 1) - kt);
     dma16(kbase + r0 * stride + 8 * kq0, st + 1024 * (2 * rw));
     dma16(kbase + r1 * stride + 8 * kq1, st + 1024 * (2 * rw + 1));
     dma16(vbase + r0 * stride + 8 * vq0, st + kTileBytes + 1024 * (2 * rw));
@@ -895,17 +911,21 @@ __device__ __forceinline__ void private_item_ring(const AttnArgs &a, int item, i
   const int ntiles = (key1 - key0 + 63) / 64;           // 1 or 2
 
   const int64_t stride = (int64_t)a.Hkv * D;
-  const T *kbase = (const T *)a.priv_k + ((int64_t)priv_row * a.Hkv + g) * D;
-  const T *vbase = (const T *)a.priv_v + ((int64_t)priv_row * a.Hkv + g) * D;
+  const T *kbase = (const T *)a.priv_k + (int64_t)g * D;
+  const T *vbase = (const T *)a.priv_v + (int64_t)g * D;
+  // paged K/V: lanes 0 and 1 hold the pool rows of the item's two tiles
+  const int tile_row = a.paged && lane < ntiles ? a.dev.priv_tiles[priv_row + (key0 >> 6) + lane] : 0;
   // tile c: 8 copies of K rows 8 i + lane / 8 (physical chunk lane % 8) and
   // 8 of V, 16 per tile
   const int rsub = lane >> 3, pch = lane & 7;
   auto issue = [&](int c) {
     unsigned char *st = lds + c * 2 * kTileBytes;
+    const int kt = key0 + 64 * c;
+    const int64_t base = a.paged ? (int64_t)__builtin_amdgcn_readlane(tile_row, c) : (int64_t)priv_row + kt;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int row = 8 * i + rsub;
-      const int64_t r = min(key0 + 64 * c + row, key1 - 1);
+      const int64_t r = base + (min(kt + row, key1 - 1) - kt);
       dma16(kbase + r * stride + 8 * Tl::kchunk(row, pch), st + 1024 * i);
       dma16(vbase + r * stride + 8 * vchunk(row, pch), st + kTileBytes + 1024 * i);
     }
@@ -963,15 +983,16 @@ __device__ __forceinline__ void private_item_f32(const AttnArgs &a, int item, in
   const int wmin = wave_min(limit);
 
   const int64_t stride = (int64_t)a.Hkv * D;
-  const T *kbase = (const T *)a.priv_k + ((int64_t)priv_row * a.Hkv + g) * D;
-  const T *vbase = (const T *)a.priv_v + ((int64_t)priv_row * a.Hkv + g) * D;
+  const T *kbase = (const T *)a.priv_k + (int64_t)g * D;
+  const T *vbase = (const T *)a.priv_v + (int64_t)g * D;
 
   WaveAttn<T> w;
   w.init((const T *)a.q + ((int64_t)t * a.Hq + hq) * D, valid, lane);
   TileLoader<T, NT> ld;
   for (int k0 = key0; k0 < key1; k0 += 64) {
-    ld.load(kbase + (int64_t)k0 * stride, stride, key1 - k0, lane);
-    ld.load_v(vbase + (int64_t)k0 * stride, stride, key1 - k0, lane);
+    const int64_t r = kv_row(a, a.dev.priv_tiles, priv_row, k0, k0) * stride;
+    ld.load(kbase + r, stride, key1 - k0, lane);
+    ld.load_v(vbase + r, stride, key1 - k0, lane);
     __syncthreads();   // previous tile fully consumed
     ld.store(lds, lane);
     __syncthreads();
@@ -1072,6 +1093,8 @@ int num_cus() {
 PlanDev plan_dev(const Plan &P, void *workspace) {
   unsigned char *ws = (unsigned char *)workspace;
   PlanDev d;
+  d.shared_tiles = (const int32_t *)(ws + P.off_shared_tiles);
+  d.priv_tiles = (const int32_t *)(ws + P.off_priv_tiles);
   d.shared_items = (const int32_t *)(ws + P.off_shared_items);
   d.private_items = (const int32_t *)(ws + P.off_private_items);
   d.token_slots = (const int32_t *)(ws + P.off_token_slots);
@@ -1096,6 +1119,7 @@ hipError_t launch_branch_attention(const Plan &P, const void *q, const void *sha
   a.G = P.G;
   a.c = P.scale * kLog2e;
   a.reg = P.regular;
+  a.paged = P.paged ? 1 : 0;
   const bool bf16 = P.attn.dtype == HPD_BF16;
   if (bf16) {
     // one launch: the private items (kPrivPerWG per workgroup) and the

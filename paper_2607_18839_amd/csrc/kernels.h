@@ -10,6 +10,8 @@ namespace hpd {
 
 // Device views of the plan tables inside a workspace.
 struct PlanDev {
+  const int32_t *shared_tiles;   // paged K/V: pool row of each 64-key tile
+  const int32_t *priv_tiles;
   const int32_t *shared_items;
   const int32_t *private_items;
   const int32_t *token_slots;

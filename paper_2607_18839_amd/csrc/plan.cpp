@@ -98,6 +98,32 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
     P.fork[i] = F;
   }
 
+  // ---- paged K/V: validation
+  const hpd_paged_kv *pg = b.paged;
+  if (pg) {
+    if (b.prefix_row || b.priv_row)
+      return fail(err, HPD_ERR_INVALID_ARGUMENT, "paged K/V: prefix_row and priv_row must be NULL");
+    if (pg->block_rows <= 0 || pg->block_rows % 64 != 0)
+      return fail(err, HPD_ERR_INVALID_ARGUMENT, "paged K/V: block_rows must be a positive multiple of 64");
+    if (pg->num_blocks <= 0 || (int64_t)pg->num_blocks * pg->block_rows > INT32_MAX)
+      return fail(err, HPD_ERR_INVALID_ARGUMENT, "paged K/V: num_blocks * block_rows must be in 1..2^31 - 1");
+    if (pg->num_entries < 0 || (pg->num_entries > 0 && !pg->blocks) || !pg->page_block0 || !pg->branch_block0)
+      return fail(err, HPD_ERR_INVALID_ARGUMENT, "paged K/V: NULL table");
+    for (int32_t e = 0; e < pg->num_entries; ++e)
+      if (pg->blocks[e] < 0 || pg->blocks[e] >= pg->num_blocks)
+        return fail(err, HPD_ERR_INVALID_ARGUMENT, "paged K/V: block id out of range");
+    auto span_ok = [&](int32_t first, int64_t rows) {
+      const int64_t n = (rows + pg->block_rows - 1) / pg->block_rows;
+      return first >= 0 && first + n <= pg->num_entries;
+    };
+    for (int p = 0; p < np; ++p)
+      if (!span_ok(pg->page_block0[p], P.prefix_len[p]))
+        return fail(err, HPD_ERR_INVALID_ARGUMENT, "paged K/V: page_block0[" + std::to_string(p) + "] out of range");
+    for (int i = 0; i < nb; ++i)
+      if (!span_ok(pg->branch_block0[i], (int64_t)P.past_len[i] + P.num_new[i]))
+        return fail(err, HPD_ERR_INVALID_ARGUMENT, "paged K/V: branch_block0[" + std::to_string(i) + "] out of range");
+  }
+
   // ---- canonical bookkeeping
   P.prefix_row.resize(np);
   int64_t acc = 0;
@@ -124,6 +150,25 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   }
   if (P.shared_rows > INT32_MAX || P.priv_rows > INT32_MAX)
     return fail(err, HPD_ERR_INVALID_ARGUMENT, "K/V row index exceeds 2^31 - 1");
+  // pool row of row i of a paged sequence whose blocks start at entry first
+  auto pool_row = [&](int32_t first, int64_t i) -> int32_t {
+    return (int32_t)((int64_t)pg->blocks[first + i / pg->block_rows] * pg->block_rows + i % pg->block_rows);
+  };
+  if (pg) {
+    P.paged = true;
+    P.shared_rows = P.priv_rows = (int64_t)pg->num_blocks * pg->block_rows;
+    P.page_tile0.resize(np);
+    for (int p = 0; p < np; ++p) {
+      P.page_tile0[p] = (int32_t)P.shared_tiles.size();
+      for (int64_t i = 0; i < P.prefix_len[p]; i += 64) P.shared_tiles.push_back(pool_row(pg->page_block0[p], i));
+    }
+    P.branch_tile0.resize(nb);
+    for (int i = 0; i < nb; ++i) {
+      P.branch_tile0[i] = (int32_t)P.priv_tiles.size();
+      for (int64_t r = 0; r < (int64_t)P.past_len[i] + P.num_new[i]; r += 64)
+        P.priv_tiles.push_back(pool_row(pg->branch_block0[i], r));
+    }
+  }
   P.T = (int)tacc;
   P.page_T.assign(np, 0);
   for (int i = 0; i < nb; ++i) P.page_T[P.branch_page[i]] += P.num_new[i];
@@ -140,7 +185,8 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
     for (int j = 0; j < P.num_new[i]; ++j) {
       P.visible[P.q_row[i] + j] = P.fork[i] + P.past_len[i] + j + 1;
       P.token_fork[P.q_row[i] + j] = P.fork[i];
-      P.token_dest[P.q_row[i] + j] = (int32_t)(P.priv_row[i] + P.past_len[i] + j);
+      P.token_dest[P.q_row[i] + j] = pg ? pool_row(pg->branch_block0[i], (int64_t)P.past_len[i] + j)
+                                        : (int32_t)(P.priv_row[i] + P.past_len[i] + j);
     }
 
   // ---- partial slots per token
@@ -158,7 +204,8 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   int64_t units = shared_items_for(kSharedSplitUnit);
   int64_t mult = std::max<int64_t>(1, ceil_div(units, kSharedTargetItems));
   while (shared_items_for(kSharedSplitUnit * mult) > kSharedTargetItems) ++mult;   // ceilings per page
-  P.split_keys = (int32_t)std::min<int64_t>(kSharedSplitUnit * mult, INT32_MAX / 2);
+  // (paged K/V: at most 64 tiles per item, each item's tile rows fit a wave)
+  P.split_keys = (int32_t)std::min<int64_t>(kSharedSplitUnit * mult, b.paged ? 4096 : INT32_MAX / 2);
   // each page's prefix is cut into page_splits[p] ranges of equal length
   // (rounded up to kSharedSplitUnit), so one page's items are balanced
   std::vector<int32_t> page_splits(np), page_split_keys(np);
@@ -220,13 +267,14 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
           int32_t it[SI_NFIELDS] = {};
           it[SI_PAGE] = p; it[SI_KVH] = g; it[SI_ROW0] = r0; it[SI_NROWS] = nr;
           it[SI_KEY0] = k0; it[SI_KEY1] = k1; it[SI_SLOT] = s; it[SI_FLAGS] = flags;
-          it[SI_PREFIX_ROW] = (int32_t)P.prefix_row[p]; it[SI_PAGE_Q_ROW] = P.page_q_row[p];
+          it[SI_PREFIX_ROW] = pg ? P.page_tile0[p] : (int32_t)P.prefix_row[p];
+          it[SI_PAGE_Q_ROW] = P.page_q_row[p];
           it[SI_PAGE_ROWS] = R;
           P.shared_items.insert(P.shared_items.end(), it, it + SI_NFIELDS);
         }
   }
 
-  if (np == 1 && !P.has_fork && P.prefix_len[0] > 0 && P.page_T[0] > 0 && P.prefix_row[0] <= INT32_MAX) {
+  if (np == 1 && !P.has_fork && !pg && P.prefix_len[0] > 0 && P.page_T[0] > 0 && P.prefix_row[0] <= INT32_MAX) {
     P.regular.on = 1;
     P.regular.groups = (int32_t)ceil_div((int64_t)P.page_T[0] * G, group_rows);
     P.regular.splits = page_splits[0];
@@ -251,7 +299,8 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
           it[PI_KEY0] = c * kPrivateChunkKeys;
           it[PI_KEY1] = std::min(keys, (c + 1) * kPrivateChunkKeys);
           it[PI_SLOT] = splits + c; it[PI_PAST] = P.past_len[i];
-          it[PI_PRIV_ROW] = (int32_t)P.priv_row[i]; it[PI_Q_ROW] = P.q_row[i];
+          it[PI_PRIV_ROW] = pg ? P.branch_tile0[i] : (int32_t)P.priv_row[i];
+          it[PI_Q_ROW] = P.q_row[i];
           it[PI_NUM_NEW] = P.num_new[i];
           P.private_items.insert(P.private_items.end(), it, it + PI_NFIELDS);
         }
@@ -259,6 +308,10 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
 
   // ---- workspace layout: tables (uploaded once) then partials
   size_t off = 0;
+  P.off_shared_tiles = off;
+  off = align256(off + P.shared_tiles.size() * sizeof(int32_t));
+  P.off_priv_tiles = off;
+  off = align256(off + P.priv_tiles.size() * sizeof(int32_t));
   P.off_shared_items = off;
   off = align256(off + P.shared_items.size() * sizeof(int32_t));
   P.off_private_items = off;
@@ -282,6 +335,8 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   auto put = [&](size_t at, const std::vector<int32_t> &v) {
     if (!v.empty()) std::memcpy(P.table_image.data() + at, v.data(), v.size() * sizeof(int32_t));
   };
+  put(P.off_shared_tiles, P.shared_tiles);
+  put(P.off_priv_tiles, P.priv_tiles);
   put(P.off_shared_items, P.shared_items);
   put(P.off_private_items, P.private_items);
   put(P.off_token_slots, P.token_slots);

@@ -16,6 +16,9 @@ namespace hpd {
 // of them over the same prefix key range [key_begin, key_end).
 // Stacked row r of (page p, kv head g) is query head g * G + r % G of token
 // page_q_row[p] + r / G.
+// SI_PREFIX_ROW / PI_PRIV_ROW: the first K/V row of the page's prefix /
+// branch's private rows, or with paged K/V its first entry in the shared /
+// private tile table.
 enum SharedItemField {
   SI_PAGE = 0, SI_KVH, SI_ROW0, SI_NROWS, SI_KEY0, SI_KEY1, SI_SLOT, SI_FLAGS,
   SI_PREFIX_ROW, SI_PAGE_Q_ROW, SI_PAGE_ROWS, SI_RESERVED, SI_NFIELDS
@@ -50,6 +53,13 @@ struct Plan {
   std::vector<int32_t> q_row, page_q_row, page_T, visible;
   int64_t shared_rows = 0, priv_rows = 0;
 
+  // Paged K/V: physical row of the first key of every 64-key tile, per page
+  // prefix (page_tile0[p] + i) and per branch (branch_tile0[b] + i).  Shared
+  // and private work items then carry a tile-table offset where contiguous
+  // plans carry a first row.
+  bool paged = false;
+  std::vector<int32_t> shared_tiles, priv_tiles, page_tile0, branch_tile0;
+
   std::vector<int32_t> shared_items, private_items;   // [n][SI_NFIELDS / PI_NFIELDS]
   std::vector<int32_t> token_slots;                   // [T][2]: first slot, count
   std::vector<int32_t> token_fork;                    // [T] visible prefix per token
@@ -65,6 +75,7 @@ struct Plan {
   } regular;
 
   // device workspace layout (byte offsets, 256-aligned)
+  size_t off_shared_tiles = 0, off_priv_tiles = 0;
   size_t off_shared_items = 0, off_private_items = 0, off_token_slots = 0,
          off_token_fork = 0, off_token_dest = 0, off_counters = 0, off_part_o = 0, off_part_lse = 0, table_bytes = 0,
          workspace_bytes = 0;

@@ -28,14 +28,14 @@ class BranchAttention:
 
     def __init__(self, num_q_heads, num_kv_heads, prefix_len, branch_page, num_new, past_len,
                  dtype=torch.bfloat16, out_dtype=None, fork_len=None, prefix_row=None,
-                 priv_row=None, softmax_scale=0.0, device="cuda", stream=None):
+                 priv_row=None, softmax_scale=0.0, device="cuda", stream=None, paged=None):
         self.dtype = dtype
         self.out_dtype = dtype if out_dtype is None else out_dtype
         self.num_q_heads = num_q_heads
         self.plan = _lib.hpd_plan_create(num_q_heads, num_kv_heads, prefix_len, branch_page, num_new,
                                          past_len, softmax_scale=softmax_scale, dtype=DT[dtype],
                                          out_dtype=DT[self.out_dtype], prefix_row=prefix_row,
-                                         priv_row=priv_row, fork_len=fork_len)
+                                         priv_row=priv_row, fork_len=fork_len, paged=paged)
         self.info = _lib.hpd_plan_query(self.plan)
         self.T = self.info["T"]
         self.ws_bytes = self.plan.workspace_bytes
@@ -87,10 +87,10 @@ class DecodeStep:
 
     def __init__(self, num_q_heads, num_kv_heads, prefix_len, branch_page, num_new, past_len,
                  weights, hidden, intermediate, rms_eps=1e-6, prefix_row=None, priv_row=None,
-                 device="cuda", stream=None, packed=False):
+                 device="cuda", stream=None, packed=False, fork_len=None, paged=None):
         self.attn = BranchAttention(num_q_heads, num_kv_heads, prefix_len, branch_page, num_new, past_len,
                                     dtype=torch.bfloat16, prefix_row=prefix_row, priv_row=priv_row,
-                                    device=device, stream=stream)
+                                    device=device, stream=stream, fork_len=fork_len, paged=paged)
         self.T = self.attn.T
         self.hidden = hidden
         self.num_layers = len(weights["w_qkv"])

@@ -28,14 +28,14 @@ def to_dev(a, dtype, device="cuda"):
 
 
 def run_batch(b, out_dtype=None, fork_len=None, prefix_row=None, priv_row=None,
-              shared_k=None, shared_v=None, priv_k=None, priv_v=None, with_lse=True):
+              shared_k=None, shared_v=None, priv_k=None, priv_v=None, with_lse=True, paged=None):
     """Runs one attention layer of a workload batch on the GPU.
     Returns (O float64 numpy [T][Hq][D], lse numpy [T][Hq])."""
     tdt = torch.bfloat16 if b.dtype == "bf16" else torch.float32
     odt = tdt if out_dtype is None else out_dtype
     layer = BranchAttention(b.num_q_heads, b.num_kv_heads, b.prefix_len, b.branch_page, b.num_new,
                             b.past_len, dtype=tdt, out_dtype=odt, fork_len=fork_len,
-                            prefix_row=prefix_row, priv_row=priv_row)
+                            prefix_row=prefix_row, priv_row=priv_row, paged=paged)
     q = to_dev(b.q, b.dtype)
     sk = shared_k if shared_k is not None else to_dev(b.shared_k, b.dtype)
     sv = shared_v if shared_v is not None else to_dev(b.shared_v, b.dtype)
