@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--weights", choices=("packed", "torch"), default="packed",
                     help="c4: projection weights packed once at load (HPD_WEIGHTS_PACKED) or in torch layout")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--paged", type=int, default=0, metavar="BLOCK_ROWS",
+                    help="K/V through block tables of this many rows (hpd_kv_pool, fragmented pool); 0 = contiguous")
     return ap.parse_args()
 
 
@@ -166,6 +168,52 @@ def _phase_pass(torch, _lib, step, K, W, work, queue_cycles=2_000_000):
     return out
 
 
+def _paged_layout(_lib, st, block_rows, seed):
+    """Block tables for a batch from an hpd_kv_pool whose free list was first
+    fragmented (short sequences reserved, then released in random order), and
+    the pool row of every packed shared / private row."""
+    rng = np.random.default_rng(seed + 1000)
+    B = block_rows
+    nblk = lambda n: -(-int(n) // B)
+    need = sum(nblk(P) for P in st["prefix_len"]) + sum(nblk(L + k) for L, k in zip(st["past_len"], st["num_new"]))
+    pool = _lib.KvPool(need + 64, B)
+    junk = []
+    for _ in range(32):
+        j = pool.new()
+        pool.reserve(j, int(rng.integers(1, 3)) * B)
+        junk.append(j)
+    for j in rng.permutation(len(junk)):
+        pool.release(junk[int(j)])
+    roots = []
+    for P in st["prefix_len"]:
+        r = pool.new()
+        pool.reserve(r, int(P))
+        roots.append(r)
+    kids = []
+    fork = st.get("fork_len")
+    for i, p in enumerate(st["branch_page"]):
+        k = pool.new(roots[int(p)], int(st["prefix_len"][int(p)]) if fork is None else int(fork[i]))
+        pool.reserve(k, int(st["past_len"][i] + st["num_new"][i]))
+        kids.append(k)
+    pg = pool.batch_tables(roots, kids)
+    blocks = np.asarray(pg["blocks"], np.int64)
+
+    def rows(first, n):
+        i = np.arange(int(n))
+        return blocks[int(first) + i // B] * B + i % B
+    sh = np.concatenate([rows(pg["page_block0"][p], P) for p, P in enumerate(st["prefix_len"])])
+    pr = np.concatenate([rows(pg["branch_block0"][b], L + k)
+                         for b, (L, k) in enumerate(zip(st["past_len"], st["num_new"]))])
+    return pg, sh, pr, pg["num_blocks"] * B
+
+
+def _to_pool(torch, t, rows, n_rows):
+    """Device pool tensor holding packed row i of t at pool row rows[i]."""
+    out = torch.zeros((n_rows,) + tuple(t.shape[1:]), dtype=t.dtype, device=t.device)
+    out[torch.from_numpy(rows).to(t.device)] = t
+    return out
+
+
 def _traffic(kind):
     """HBM bytes per launch of kernel kind from profiles/traffic_c4.md (rocprofv3
     FETCH_SIZE / WRITE_SIZE runs scaled by a plain copy kernel's readings), or
@@ -199,14 +247,21 @@ def bench_attention(args, torch, _lib):
     b = make_attn_batch(args.workload, args.seed)
     tdt = torch.bfloat16 if b.dtype == "bf16" else torch.float32
     s_in = 2 if b.dtype == "bf16" else 4
+    st = dict(prefix_len=b.prefix_len, branch_page=b.branch_page, num_new=b.num_new, past_len=b.past_len,
+              fork_len=b.fork_len)
+    pg = _paged_layout(_lib, st, args.paged, args.seed) if args.paged else None
     layer = BranchAttention(b.num_q_heads, b.num_kv_heads, b.prefix_len, b.branch_page, b.num_new,
-                            b.past_len, dtype=tdt, fork_len=b.fork_len)
+                            b.past_len, dtype=tdt, fork_len=b.fork_len, paged=pg and pg[0])
 
     def dev(a):
         if b.dtype == "bf16":
             return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
         return torch.from_numpy(a).cuda()
     base = [dev(getattr(b, f)) for f in ("q", "shared_k", "shared_v", "priv_k", "priv_v")]
+    if pg:
+        _, sh_rows, pr_rows, n_pool = pg
+        base = base[:1] + [_to_pool(torch, t, r, n_pool) for t, r in
+                           zip(base[1:], (sh_rows, sh_rows, pr_rows, pr_rows))]
     per = sum(t.numel() * t.element_size() for t in base)
     reps = 1 if args.warm else max(1, int(np.ceil((1 << 30) / per)))
     replicas = [base] + [[t.clone() for t in base] for _ in range(reps - 1)]
@@ -253,7 +308,8 @@ def bench_attention(args, torch, _lib):
                    "fork_offsets": None if b.fork_len is None else
                    {"visible_prefix_keys": int(np.asarray(b.fork_len, np.int64).sum()),
                     "rule": "layout branch whole prefix; content branches uniform in [1024, P]"},
-                   "cache": "warm" if args.warm else f"cold ({reps} input replicas rotated)"},
+                   "cache": "warm" if args.warm else f"cold ({reps} input replicas rotated)",
+                   "kv": f"paged ({args.paged}-row blocks, fragmented pool)" if args.paged else "contiguous"},
         "roofline": roof, "kernels": kern,
     }
     if not args.no_cpu_baseline:
@@ -304,9 +360,15 @@ def bench_decode(args, torch, _lib):
     sv = [dev(a) for a in inp.shared_v]
     pk = [dev(a) for a in inp.priv_k]
     pv = [dev(a) for a in inp.priv_v]
+    st = dict(prefix_len=inp.prefix_len, branch_page=inp.branch_page, num_new=inp.num_new, past_len=inp.past_len)
+    pg = _paged_layout(_lib, st, args.paged, args.seed) if args.paged else None
+    if pg:
+        _, sh_rows, pr_rows, n_pool = pg
+        sk, sv = [_to_pool(torch, t, sh_rows, n_pool) for t in sk], [_to_pool(torch, t, sh_rows, n_pool) for t in sv]
+        pk, pv = [_to_pool(torch, t, pr_rows, n_pool) for t in pk], [_to_pool(torch, t, pr_rows, n_pool) for t in pv]
     step_obj = DecodeStep(inp.num_q_heads, inp.num_kv_heads, inp.prefix_len, inp.branch_page, inp.num_new,
                           inp.past_len, w, inp.hidden, inp.intermediate, inp.rms_eps,
-                          packed=args.weights == "packed")
+                          packed=args.weights == "packed", paged=pg and pg[0])
     del w   # the packed copies are held by step_obj; the torch-layout tensors are not read again
     h_in = torch.from_numpy(inp.hidden_in).cuda()
     h_out = torch.empty_like(h_in)
@@ -352,7 +414,8 @@ def bench_decode(args, torch, _lib):
                    "layers": inp.num_layers, "hidden": H, "intermediate": I, "heads": [Hq, Hkv, D],
                    "branch_tokens": T, "branches": int(len(inp.num_new)), "prefix_len": int(inp.prefix_len[0]),
                    "private_rows": int((inp.past_len + inp.num_new).sum()),
-                   "weights": args.weights + (" (packed once before timing)" if args.weights == "packed" else "")},
+                   "weights": args.weights + (" (packed once before timing)" if args.weights == "packed" else ""),
+                   "kv": f"paged ({args.paged}-row blocks, fragmented pool)" if args.paged else "contiguous"},
         "roofline": roof, "kernels": kern,
     }
     if not args.no_cpu_baseline:
