@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--weights", choices=("packed", "torch"), default="packed",
                     help="c4: projection weights packed once at load (HPD_WEIGHTS_PACKED) or in torch layout")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--pmtp", action="store_true",
+                    help="c4: each step also runs P-MTP verification and drafting (LM head, 151,936-token vocab)")
     ap.add_argument("--paged", type=int, default=0, metavar="BLOCK_ROWS",
                     help="K/V through block tables of this many rows (hpd_kv_pool, fragmented pool); 0 = contiguous")
     return ap.parse_args()
@@ -373,9 +375,26 @@ def bench_decode(args, torch, _lib):
     h_in = torch.from_numpy(inp.hidden_in).cuda()
     h_out = torch.empty_like(h_in)
     stream = torch.cuda.current_stream()
+    vd = None
+    if args.pmtp:
+        from paper_2607_18839_amd.torch_api import VerifyDraft
+        from workloads import get_config, make_pmtp_inputs
+        c = get_config("c4")["pmtp"]
+        pm = make_pmtp_inputs(inp.hidden, c["vocab"], c["draft_inner"], c["weight_std"], args.seed)
+        vd = VerifyDraft(step_obj, {k: dev(getattr(pm, k)) for k in ("lm_head", "embed", "w_draft_gate",
+                                                                     "w_draft_up", "w_draft_down")})
+        del pm
+        tokens_in = torch.from_numpy(np.random.default_rng(args.seed).integers(0, c["vocab"], size=step_obj.T)
+                                     .astype(np.int32)).cuda()
+        nbr = len(inp.num_new)
+        ver = torch.empty(step_obj.T, dtype=torch.int32, device="cuda")
+        nacc = torch.empty(nbr, dtype=torch.int32, device="cuda")
+        drafts = torch.empty((nbr, _lib.HPD_MAX_K), dtype=torch.int32, device="cuda")
 
     def step(i):
         step_obj(h_in, sk, sv, pk, pv, hidden_out=h_out)
+        if vd is not None:
+            vd(h_out, tokens_in, ver, nacc, drafts)
 
     ms, timed, pct = _graph_time(torch, step, 1, args.steps, args.warmup)
     kern = _kernel_pass(torch, _lib, step, min(args.steps, 10), args.warmup)
@@ -393,6 +412,9 @@ def bench_decode(args, torch, _lib):
                      frac=aw["private_bytes"] / us / 1e3 / HBM_PEAK_GBS)
         elif name in gw:
             k.update(bound="hbm", bytes=gw[name], gbs=gw[name] / us / 1e3, frac=gw[name] / us / 1e3 / HBM_PEAK_GBS)
+        elif name == "lm_head" and vd is not None:   # the LM head's weights once per launch
+            lb = vd.vocab * H * 2
+            k.update(bound="hbm", bytes=lb, gbs=lb / us / 1e3, frac=lb / us / 1e3 / HBM_PEAK_GBS)
         k["total_us_per_step"] = us * k["launches"] / min(args.steps, 10)
     dom = max(kern, key=lambda n: kern[n]["total_us_per_step"])
     kern["phases_isolated"] = _phase_pass(torch, _lib, step, min(args.steps, 10), args.warmup, aw)
@@ -415,7 +437,10 @@ def bench_decode(args, torch, _lib):
                    "branch_tokens": T, "branches": int(len(inp.num_new)), "prefix_len": int(inp.prefix_len[0]),
                    "private_rows": int((inp.past_len + inp.num_new).sum()),
                    "weights": args.weights + (" (packed once before timing)" if args.weights == "packed" else ""),
-                   "kv": f"paged ({args.paged}-row blocks, fragmented pool)" if args.paged else "contiguous"},
+                   "kv": f"paged ({args.paged}-row blocks, fragmented pool)" if args.paged else "contiguous",
+                   "pmtp": None if vd is None else
+                   {"vocab": vd.vocab, "draft_inner": vd.draft_inner,
+                    "per_step": "verification of all T positions + drafting of each branch's next window"}},
         "roofline": roof, "kernels": kern,
     }
     if not args.no_cpu_baseline:

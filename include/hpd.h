@@ -272,6 +272,64 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan,
                            void *const *priv_k, void *const *priv_v,
                            void *workspace, size_t workspace_bytes, void *stream);
 
+/* ---- P-MTP verification and drafting (section "Integration with P-MTP";
+ * Algorithm 1, speculative decoding and verification).  After a decode step
+ * the k_b hidden states of branch b are projected through the LM head: the
+ * token fed at position j (tokens_in: position 0 is the branch's last
+ * accepted token, positions 1.. its drafts) is verified against the argmax at
+ * position j - 1, and the branch accepts its longest verified prefix of
+ * drafts, n_acc.  The argmax y* at the first unverified position is the
+ * step's bonus token and the first token of the next step's window; the
+ * lightweight residual MLP then drafts the rest of the window from that
+ * position's hidden state: f <- f + SwiGLU(RMSNorm([f ; embed(token)]))
+ * W_down^T, next token = argmax of the LM head on RMSNorm(f), as often as
+ * the branch's window needs.
+ *
+ *  vocab            V, a positive multiple of 128
+ *  draft_inner      I_d, inner width of the draft MLP, a multiple of 128
+ *  lm_head          [V][hidden] bf16, packed with hpd_pack_weight (shared by
+ *                   verification and drafting)
+ *  g_final          [hidden] bf16 gain of the RMSNorm before the LM head;
+ *                   NULL = ones
+ *  embed            [V][hidden] bf16 token embedding, row-major
+ *  w_draft_gate_up  gate/up of the draft MLP, [I_d][2 hidden] each, packed
+ *                   with hpd_pack_gate_up
+ *  w_draft_down     [hidden][I_d], packed with hpd_pack_weight_f16
+ *
+ * Argmax ties go to the smallest token id.  The LM head runs on the bf16
+ * rounding of x = h * g_final; the positive per-token RMSNorm factor does not
+ * change the argmax and is not applied.  All pointers 16-byte aligned. */
+typedef struct {
+  int32_t vocab;
+  int32_t draft_inner;
+  const void *lm_head;
+  const void *g_final;
+  const void *embed;
+  const void *w_draft_gate_up;
+  const void *w_draft_down;
+} hpd_pmtp_desc;
+
+/* Bytes of device workspace hpd_verify_draft_step needs on top of
+ * hpd_plan_workspace_bytes. */
+size_t hpd_pmtp_workspace_bytes(const hpd_model_desc *model, const hpd_pmtp_desc *pmtp, const hpd_plan *plan);
+
+/* One verification + drafting pass for every branch of the plan.
+ * hidden      device float [T][hidden]: the decode step's output
+ * tokens_in   device int32 [T]: the token fed at each position, ids < V
+ * verified    device int32 [T]: argmax token at each position (written)
+ * n_acc       device int32 [num_branches]: accepted drafts, 0..k_b - 1
+ * draft_out   device int32 [num_branches][HPD_MAX_K]: the next window of
+ *             branch b in entries 0..k_b - 1 (entry 0 the bonus token);
+ *             later entries unspecified
+ * workspace   >= hpd_plan_workspace_bytes + hpd_pmtp_workspace_bytes,
+ *             256-byte aligned, uploaded with hpd_plan_upload (it may be the
+ *             decode step's workspace if it is large enough for both).
+ * The plan must be HPD_BF16. */
+hpd_status hpd_verify_draft_step(const hpd_model_desc *model, const hpd_pmtp_desc *pmtp, const hpd_plan *plan,
+                                 const float *hidden, const int32_t *tokens_in, int32_t *verified,
+                                 int32_t *n_acc, int32_t *draft_out, void *workspace, size_t workspace_bytes,
+                                 void *stream);
+
 /* ---- Benchmark support: per-kernel timing with HIP events.
  * When enabled, every kernel a step enqueues is launched with a pair of HIP
  * events bound to its own dispatch (hipExtLaunchKernel), so each pair spans
@@ -283,7 +341,7 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan,
  * eager launches: do not enable it while capturing a graph.  keep_pairs = 1
  * keeps the pairs assigned after the read (re-read after re-running the same
  * launches); keep_pairs = 0 releases them. */
-#define HPD_NUM_KERNEL_KINDS 8
+#define HPD_NUM_KERNEL_KINDS 12
 typedef struct {
   int64_t count[HPD_NUM_KERNEL_KINDS];
   double total_ms[HPD_NUM_KERNEL_KINDS];
@@ -292,7 +350,9 @@ typedef struct {
 hpd_status hpd_kernel_timing(int enable, int max_launches);
 hpd_status hpd_kernel_times_read(hpd_kernel_times *out, int keep_pairs);
 /* Kind k: 0 shared_prefix, 1 private, 2 merge, 3 gemm_qkv, 4 gemm_o,
- * 5 gemm_gate_up, 6 gemm_down, 7 norm_input.  With bf16 inputs kind 0 is
+ * 5 gemm_gate_up, 6 gemm_down, 7 norm_input, 8 lm_head, 9 verify,
+ * 10 draft_mlp (the draft MLP's two projections and its input),
+ * 11 draft_token.  With bf16 inputs kind 0 is
  * one launch that runs the shared-prefix and the private work items (kind 1
  * is then never launched) unless phase isolation is on. */
 const char *hpd_kernel_kind_name(int kind);

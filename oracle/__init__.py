@@ -25,9 +25,10 @@ Modules:
   attention  full attention, its shared/private partials and their LSE merge
   decode     one decode step of the synthetic decoder stack
   paged      the rows a paged K/V batch describes (block-table gather)
+  pmtp       P-MTP verification (LM head argmax, acceptance) and drafting
 
 Every function is pinned by the CPU tests against something other than
 itself: brute force, library routines (torch SDPA in fp64), closed forms and
 invariants.  No function here is "parity unpinned".
 """
-from . import attention, decode, paged, plan  # noqa: F401
+from . import attention, decode, paged, plan, pmtp  # noqa: F401

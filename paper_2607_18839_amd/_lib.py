@@ -80,6 +80,12 @@ class hpd_model_desc(ctypes.Structure):
 HPD_WEIGHTS_TORCH, HPD_WEIGHTS_PACKED = 0, 1
 
 
+class hpd_pmtp_desc(ctypes.Structure):
+    _fields_ = [("vocab", ctypes.c_int32), ("draft_inner", ctypes.c_int32), ("lm_head", ctypes.c_void_p),
+                ("g_final", ctypes.c_void_p), ("embed", ctypes.c_void_p), ("w_draft_gate_up", ctypes.c_void_p),
+                ("w_draft_down", ctypes.c_void_p)]
+
+
 # Every symbol include/hpd.h declares, with its ctypes signature.
 SIGNATURES = {
     "hpd_plan_create": (ctypes.c_int, [ctypes.POINTER(hpd_attn_desc), ctypes.POINTER(hpd_batch_desc),
@@ -103,6 +109,12 @@ SIGNATURES = {
                                         ctypes.c_void_p, ctypes.c_void_p]),
     "hpd_kernel_timing": (ctypes.c_int, [ctypes.c_int, ctypes.c_int]),
     "hpd_attn_phase_isolation": (ctypes.c_int, [ctypes.c_int]),
+    "hpd_pmtp_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(hpd_model_desc), ctypes.POINTER(hpd_pmtp_desc),
+                                                   ctypes.c_void_p]),
+    "hpd_verify_draft_step": (ctypes.c_int, [ctypes.POINTER(hpd_model_desc), ctypes.POINTER(hpd_pmtp_desc),
+                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                             ctypes.c_void_p]),
     "hpd_kv_pool_create": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_void_p)]),
     "hpd_kv_pool_destroy": (None, [ctypes.c_void_p]),
     "hpd_kv_pool_free_blocks": (ctypes.c_int32, [ctypes.c_void_p]),
@@ -277,7 +289,7 @@ def hpd_decode_step(model, plan, hidden_in, hidden_out, shared_k, shared_v, priv
                                   stream), "hpd_decode_step")
 
 
-HPD_NUM_KERNEL_KINDS = 8
+HPD_NUM_KERNEL_KINDS = 12
 
 
 class hpd_kernel_times(ctypes.Structure):
@@ -370,3 +382,14 @@ class KvPool:
                                            ctypes.byref(n)), "hpd_kv_batch_tables")
         return dict(block_rows=self.block_rows, num_blocks=self.num_blocks, blocks=blocks[:n.value],
                     page_block0=p0[:len(ps)], branch_block0=b0[:len(bs)])
+
+
+def hpd_pmtp_workspace_bytes(model, pmtp, plan):
+    return int(load().hpd_pmtp_workspace_bytes(ctypes.byref(model), ctypes.byref(pmtp), plan.handle))
+
+
+def hpd_verify_draft_step(model, pmtp, plan, hidden, tokens_in, verified, n_acc, draft_out, workspace,
+                          workspace_bytes, stream=None):
+    _check(load().hpd_verify_draft_step(ctypes.byref(model), ctypes.byref(pmtp), plan.handle, hidden, tokens_in,
+                                        verified, n_acc, draft_out, workspace, workspace_bytes, stream),
+           "hpd_verify_draft_step")

@@ -20,7 +20,7 @@ PEAKS = os.path.join(PKG, "peaks")   # microbenchmark executable (bench.py --pea
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-HIP_SOURCES = ["attn_kernels.hip", "gemm_kernels.hip", "decode.hip", "timing.hip", "api.hip"]
+HIP_SOURCES = ["attn_kernels.hip", "gemm_kernels.hip", "decode.hip", "pmtp.hip", "timing.hip", "api.hip"]
 CXX_SOURCES = ["plan.cpp", "kv_pool.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-I" + os.path.join(ROOT, "include"), "-I" + CSRC]

@@ -1095,6 +1095,8 @@ PlanDev plan_dev(const Plan &P, void *workspace) {
   PlanDev d;
   d.shared_tiles = (const int32_t *)(ws + P.off_shared_tiles);
   d.priv_tiles = (const int32_t *)(ws + P.off_priv_tiles);
+  d.branch_q_row = (const int32_t *)(ws + P.off_branch_q_row);
+  d.branch_new = (const int32_t *)(ws + P.off_branch_new);
   d.shared_items = (const int32_t *)(ws + P.off_shared_items);
   d.private_items = (const int32_t *)(ws + P.off_private_items);
   d.token_slots = (const int32_t *)(ws + P.off_token_slots);

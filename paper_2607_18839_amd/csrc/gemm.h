@@ -11,7 +11,7 @@ namespace hpd {
 
 constexpr int kGemmTile = 32;             // weight rows and tokens of one wave's output tile
 constexpr int kGemmKStep = 64;            // K per pipeline step (4 MFMAs of 16)
-constexpr int kEpiQKV = 0, kEpiResidual = 1, kEpiSwiGLU = 2;
+constexpr int kEpiQKV = 0, kEpiResidual = 1, kEpiSwiGLU = 2, kEpiArgmax = 3;
 
 // One projection Y[t][n] = sum_k X[t][k] W[n][k] over the full K range.  A
 // workgroup of 4 waves owns the output tile of 32 rg weight rows x 32
@@ -47,12 +47,24 @@ struct GemmArgs {
   __bf16 *x_out; bool x_out_f16;            // [Tpad][N]; rows < T written
   const __bf16 *gamma;                      // [N] bf16, NULL = ones
   float *ss_out;                            // [Tpad][N / 32]
+  // argmax epilogue (LM head): per token and 32-row tile the largest logit
+  // as an ordered key (argmax_key), amax[t][N / 32]
+  uint64_t *amax;
   // layouts: a_packed: w0 is packed (packed_offset; SwiGLU: the interleaved
   // gate/up pair, w1 unused); act_packed: x, x_out and m_out are packed.
   // a_packed requires act_packed; row-major weights require row-major
   // activations.
   bool a_packed, act_packed;
 };
+
+// Ordered 64-bit key of a logit and its row id: comparing keys as unsigned
+// integers orders by value, and equal values by the smaller id.
+__device__ __forceinline__ uint64_t argmax_key(float v, int id) {
+  uint32_t u = __float_as_uint(v);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((uint64_t)u << 32) | (uint32_t)(0xFFFFFFFFu - (uint32_t)id);
+}
+__device__ __forceinline__ int argmax_id(uint64_t key) { return (int)(0xFFFFFFFFu - (uint32_t)key); }
 
 // Start of a step: h = h_in (if different), x = h * gamma, ss, and zero rows
 // T..Tpad-1 of x and of `zero_rows` ([Tpad][zero_cols]).
@@ -66,6 +78,9 @@ hipError_t launch_pack_weight(const __bf16 *w, const __bf16 *w2, int rows, int c
 // f16: fp16 GEMM (bf16 weights converted to fp16 in registers, fp16
 // activations); epi: kEpi*.
 hipError_t launch_gemm(const GemmArgs &g, bool f16, int epi, int kind, hipStream_t stream);
+// LM head with the argmax epilogue (bf16, packed operands) for Tpad <= 160:
+// 128 rows per workgroup against every token tile; n_slices = N / 128.
+hipError_t launch_lm_argmax(const GemmArgs &g, int kind, hipStream_t stream);
 
 // Row groups per workgroup for an N x K projection over Tpad tokens, from a
 // model of the bytes each CU has to stream.

@@ -78,7 +78,9 @@ __device__ __forceinline__ void load_early(const GemmArgs &g, int t, EpilogueIn 
 
 template <int EPI>
 __device__ __forceinline__ void load_late(const GemmArgs &g, int t, int tile, int half, EpilogueIn &in) {
-  if constexpr (EPI == kEpiResidual) {
+  if constexpr (EPI == kEpiArgmax) {
+    // nothing: the argmax needs no norm factor (a positive per-token scale)
+  } else if constexpr (EPI == kEpiResidual) {
     const float *hr = g.h + (int64_t)min(t, g.T - 1) * g.N + tile * kGemmTile + 4 * half;
 #pragma unroll
     for (int i = 0; i < 4; ++i) in.h[i] = *(const f32x4 *)(hr + 8 * i);
@@ -109,7 +111,21 @@ __device__ __forceinline__ void load_late(const GemmArgs &g, int t, int tile, in
 template <int EPI>
 __device__ __forceinline__ void epilogue(const GemmArgs &g, const f32x16 &acc, EpilogueIn &in, int t, int tile,
                                          int half) {
-  if constexpr (EPI == kEpiResidual) {
+  if constexpr (EPI == kEpiArgmax) {
+    // the tile's largest logit for token t (rows 8 (r / 4) + 4 half + r % 4
+    // of this lane, the other 16 in lane ^ 32), ties to the smaller row
+    uint64_t best = 0;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const uint64_t k = argmax_key(acc[r], tile * kGemmTile + 8 * (r >> 2) + 4 * half + (r & 3));
+      best = k > best ? k : best;
+    }
+    const uint64_t other = ((uint64_t)(uint32_t)__shfl_xor((int)(best >> 32), 32) << 32) |
+                           (uint32_t)__shfl_xor((int)(uint32_t)best, 32);
+    best = other > best ? other : best;
+    if (half == 0) g.amax[(int64_t)t * (g.N / kGemmTile) + tile] = best;
+    return;
+  } else if constexpr (EPI == kEpiResidual) {
     // h += Y; x_out = h * gamma (the next norm's input, unnormalised) and the
     // sum of squares of h over this 32-column tile
     if (t >= g.T) return;
@@ -463,6 +479,71 @@ __global__ __launch_bounds__(256) void gemm_packed_kernel(GemmArgs g) {
   epilogue<EPI>(g, acc, ein, t, tile, half);
 }
 
+// LM head with the argmax epilogue for up to 5 token tiles (T <= 160): a
+// workgroup of 4 waves owns 128 vocabulary rows (32 per wave) against every
+// token tile at once, so its weight rows are streamed once however many
+// tokens there are (the generic kernel re-reads them once per token tile).
+// Per K step the waves copy their own 4 KB weight tile and, 1 KB each, the
+// step's token tiles into an LDS ring of 4 steps (direct global -> LDS
+// copies, 3 steps ahead; a wave issues 4 + NTT copies per step), then read
+// their fragments from LDS.
+template <int NTT>
+__global__ __launch_bounds__(256) void lm_argmax_kernel(GemmArgs g) {
+  constexpr int SB = 4, kA = 4 * 4096, kB = NTT * 4096, kStage = kA + kB;
+  static_assert(SB * kStage <= 160 * 1024, "LDS");
+  __shared__ __attribute__((aligned(16))) unsigned char lds[SB * kStage];
+  const int per_xcd = gridDim.x / 8;
+  const int slice = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (slice >= g.n_slices) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int frow = lane & 31, half = lane >> 5;
+  const int tile = slice * 4 + wave, ksteps = g.K / kGemmKStep;
+  const __bf16 *asrc = g.w0 + (int64_t)tile * ksteps * 2048 + lane * 8;
+  auto issue = [&](int step) {
+    unsigned char *st = lds + (step % SB) * kStage;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dma16(asrc + (int64_t)step * 2048 + 512 * j, st + wave * 4096 + 1024 * j);
+#pragma unroll
+    for (int i = 0; i < NTT; ++i) {
+      const int q = wave + 4 * i, tt = q >> 2, j = q & 3;   // token tile tt, piece j
+      dma16(g.x + ((int64_t)tt * ksteps + step) * 2048 + 512 * j + lane * 8, st + kA + 1024 * q);
+    }
+  };
+  f32x16 acc[NTT];
+#pragma unroll
+  for (int tt = 0; tt < NTT; ++tt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[tt][r] = 0.f;
+  for (int s = 0; s < SB - 1 && s < ksteps; ++s) issue(s);
+  for (int c = 0; c < ksteps; ++c) {
+    // step c landed (this wave's copies; the steps after it may stay in
+    // flight), and visible to every wave; the slot of step c - 1 is free
+    const int pending = min(SB - 2, ksteps - 1 - c);
+    if (pending >= 2) wait_vm<2 * (4 + NTT)>();
+    else if (pending == 1) wait_vm<4 + NTT>();
+    else wait_vm<0>();
+    ring_barrier();
+    if (c + SB - 1 < ksteps) issue(c + SB - 1);
+    const unsigned char *st = lds + (c % SB) * kStage;
+    u32x4 a[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) a[j] = *(const u32x4 *)(st + wave * 4096 + 1024 * j + 16 * lane);
+#pragma unroll
+    for (int tt = 0; tt < NTT; ++tt) {
+      u32x4 b[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = *(const u32x4 *)(st + kA + 1024 * (4 * tt + j) + 16 * lane);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[j]),
+                                                          __builtin_bit_cast(bf16x8, b[j]), acc[tt], 0, 0, 0);
+    }
+  }
+  EpilogueIn none;
+#pragma unroll
+  for (int tt = 0; tt < NTT; ++tt) epilogue<kEpiArgmax>(g, acc[tt], none, tt * kGemmTile + frow, tile, half);
+}
+
 // Packs W[rows][cols] (bf16) into the packed layout: one thread per 16-byte
 // piece of the output.  gate_up: rows are the pair's interleaved rows (row tile
 // r = gate rows 16 r .. 16 r + 15, then up rows 16 r .. 16 r + 15) read from
@@ -559,19 +640,38 @@ hipError_t launch_pack_weight(const __bf16 *w, const __bf16 *w2, int rows, int c
   return hipGetLastError();
 }
 
+hipError_t launch_lm_argmax(const GemmArgs &g, int kind, hipStream_t stream) {
+  const int ntt = g.Tpad / kGemmTile;
+  if (ntt < 1 || ntt > 5 || g.Tpad % kGemmTile || g.N % (4 * kGemmTile) || g.K % kGemmKStep || !g.amax ||
+      !g.a_packed || !g.act_packed || g.n_slices != g.N / (4 * kGemmTile))
+    return hipErrorInvalidValue;
+  const dim3 grid((g.n_slices + 7) / 8 * 8), block(256);
+  switch (ntt) {
+    case 1: launch(kind, lm_argmax_kernel<1>, grid, block, stream, g); break;
+    case 2: launch(kind, lm_argmax_kernel<2>, grid, block, stream, g); break;
+    case 3: launch(kind, lm_argmax_kernel<3>, grid, block, stream, g); break;
+    case 4: launch(kind, lm_argmax_kernel<4>, grid, block, stream, g); break;
+    default: launch(kind, lm_argmax_kernel<5>, grid, block, stream, g); break;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm(const GemmArgs &g, bool f16, int epi, int kind, hipStream_t stream) {
   const int kg = g.rg == 4 ? 1 : g.rg == 2 ? 2 : g.rg == 1 ? 4 : 0;
   if (kg == 0 || g.K <= 0 || g.K % (kGemmKStep * kg) != 0 || g.Tpad % kGemmTile != 0 ||
       g.n_ttiles * kGemmTile != g.Tpad || g.T < 1 || g.T > g.Tpad || g.N != g.n_slices * kGemmTile * g.rg ||
       (epi == kEpiSwiGLU && (g.N != 2 * g.I || !f16)) || (epi == kEpiQKV && f16))
     return hipErrorInvalidValue;
-  if (epi == kEpiResidual ? (!g.h || (g.x_out && !g.ss_out)) : (!g.ss_in || g.n_ss < 4 || g.n_ss % 4 != 0))
+  if (epi != kEpiArgmax &&
+      (epi == kEpiResidual ? (!g.h || (g.x_out && !g.ss_out)) : (!g.ss_in || g.n_ss < 4 || g.n_ss % 4 != 0)))
     return hipErrorInvalidValue;
   const int nwg = g.n_slices * g.n_ttiles;
   const dim3 grid((nwg + 7) / 8 * 8);
+  if (epi == kEpiArgmax && (!g.amax || f16 || !g.a_packed)) return hipErrorInvalidValue;
   if (g.a_packed) {
     if (!g.act_packed) return hipErrorInvalidValue;
-    if (epi == kEpiSwiGLU) launch_packed<true, kEpiSwiGLU>(g, kind, grid, stream);
+    if (epi == kEpiArgmax) launch_packed<false, kEpiArgmax>(g, kind, grid, stream);
+    else if (epi == kEpiSwiGLU) launch_packed<true, kEpiSwiGLU>(g, kind, grid, stream);
     else if (epi == kEpiQKV) launch_packed<false, kEpiQKV>(g, kind, grid, stream);
     else if (f16) launch_packed<true, kEpiResidual>(g, kind, grid, stream);
     else launch_packed<false, kEpiResidual>(g, kind, grid, stream);

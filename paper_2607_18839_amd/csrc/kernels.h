@@ -12,6 +12,8 @@ namespace hpd {
 struct PlanDev {
   const int32_t *shared_tiles;   // paged K/V: pool row of each 64-key tile
   const int32_t *priv_tiles;
+  const int32_t *branch_q_row;   // [nb] first token of branch b
+  const int32_t *branch_new;     // [nb] k_b
   const int32_t *shared_items;
   const int32_t *private_items;
   const int32_t *token_slots;
@@ -26,7 +28,7 @@ PlanDev plan_dev(const Plan &P, void *workspace);
 
 // Kernel kinds of the optional benchmark timing (hpd_kernel_timing).
 enum KernelKind { KK_SHARED = 0, KK_PRIVATE, KK_MERGE, KK_GEMM_QKV, KK_GEMM_O, KK_GEMM_GATE_UP,
-                  KK_GEMM_DOWN, KK_NORM };
+                  KK_GEMM_DOWN, KK_NORM, KK_LM_HEAD, KK_VERIFY, KK_DRAFT_MLP, KK_DRAFT_TOKEN };
 // Element offset of (row, col) of a [rows][cols] 16-bit matrix in the packed
 // layout (tiles of 32 rows x 64 columns, 2048 elements each, ordered by row
 // tile then column tile; inside a tile, element e of 16-byte piece (j, l) is

@@ -312,6 +312,10 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   off = align256(off + P.shared_tiles.size() * sizeof(int32_t));
   P.off_priv_tiles = off;
   off = align256(off + P.priv_tiles.size() * sizeof(int32_t));
+  P.off_branch_q_row = off;
+  off = align256(off + P.q_row.size() * sizeof(int32_t));
+  P.off_branch_new = off;
+  off = align256(off + P.num_new.size() * sizeof(int32_t));
   P.off_shared_items = off;
   off = align256(off + P.shared_items.size() * sizeof(int32_t));
   P.off_private_items = off;
@@ -337,6 +341,8 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   };
   put(P.off_shared_tiles, P.shared_tiles);
   put(P.off_priv_tiles, P.priv_tiles);
+  put(P.off_branch_q_row, P.q_row);
+  put(P.off_branch_new, P.num_new);
   put(P.off_shared_items, P.shared_items);
   put(P.off_private_items, P.private_items);
   put(P.off_token_slots, P.token_slots);

@@ -75,7 +75,7 @@ struct Plan {
   } regular;
 
   // device workspace layout (byte offsets, 256-aligned)
-  size_t off_shared_tiles = 0, off_priv_tiles = 0;
+  size_t off_shared_tiles = 0, off_priv_tiles = 0, off_branch_q_row = 0, off_branch_new = 0;
   size_t off_shared_items = 0, off_private_items = 0, off_token_slots = 0,
          off_token_fork = 0, off_token_dest = 0, off_counters = 0, off_part_o = 0, off_part_lse = 0, table_bytes = 0,
          workspace_bytes = 0;

@@ -124,3 +124,45 @@ class DecodeStep:
                              [t.data_ptr() for t in priv_k], [t.data_ptr() for t in priv_v],
                              self.workspace.data_ptr(), self.ws_bytes, _stream(stream))
         return hidden_out
+
+
+class VerifyDraft:
+    """P-MTP verification and drafting after a decode step (hpd_verify_draft_step).
+
+    ``pmtp`` maps 'lm_head' [V][hidden], 'embed' [V][hidden], 'w_draft_gate',
+    'w_draft_up' [I_d][2 hidden], 'w_draft_down' [hidden][I_d] (bf16 device
+    tensors, torch Linear layout) and optionally 'g_final' [hidden]; the
+    projections are packed once here.  ``step`` is the DecodeStep whose plan
+    and workspace it shares (the workspace is enlarged if needed).
+    """
+
+    def __init__(self, step, pmtp, stream=None):
+        self.step = step
+        self.vocab, self.hidden = pmtp["lm_head"].shape
+        self.draft_inner = pmtp["w_draft_gate"].shape[0]
+        self._w = dict(lm_head=pack_weight(pmtp["lm_head"], stream),
+                       gate_up=pack_gate_up(pmtp["w_draft_gate"], pmtp["w_draft_up"], stream),
+                       down=pack_weight(pmtp["w_draft_down"], stream, f16=True),
+                       embed=pmtp["embed"].contiguous(), g_final=pmtp.get("g_final"))
+        g = self._w["g_final"]
+        self.desc = _lib.hpd_pmtp_desc(self.vocab, self.draft_inner, self._w["lm_head"].data_ptr(),
+                                       None if g is None else g.data_ptr(), self._w["embed"].data_ptr(),
+                                       self._w["gate_up"].data_ptr(), self._w["down"].data_ptr())
+        plan = step.attn.plan
+        self.ws_bytes = step.plan_bytes + _lib.hpd_pmtp_workspace_bytes(step.model, self.desc, plan)
+        if self.ws_bytes > step.ws_bytes:   # one workspace for both steps
+            step.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=step.workspace.device)
+            step.ws_bytes = self.ws_bytes
+            _lib.hpd_plan_upload(plan, step.workspace.data_ptr(), step.ws_bytes, _stream(stream))
+        self.T = step.T
+
+    def __call__(self, hidden, tokens_in, verified=None, n_acc=None, draft_out=None, stream=None):
+        dev = hidden.device
+        nb = len(self.step.attn.info["q_row"])
+        verified = torch.empty(self.T, dtype=torch.int32, device=dev) if verified is None else verified
+        n_acc = torch.empty(nb, dtype=torch.int32, device=dev) if n_acc is None else n_acc
+        draft_out = torch.empty((nb, _lib.HPD_MAX_K), dtype=torch.int32, device=dev) if draft_out is None else draft_out
+        _lib.hpd_verify_draft_step(self.step.model, self.desc, self.step.attn.plan, hidden.data_ptr(),
+                                   tokens_in.data_ptr(), verified.data_ptr(), n_acc.data_ptr(), draft_out.data_ptr(),
+                                   self.step.workspace.data_ptr(), self.step.ws_bytes, _stream(stream))
+        return verified, n_acc, draft_out

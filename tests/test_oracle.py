@@ -82,3 +82,87 @@ def test_paged_rows_match_a_per_row_loop_and_invert_a_scatter():
     sk, sv, pk, pv = gather_packed(pool, pool, pool, pool, st, paged)
     n_sh = int(st["prefix_len"].sum())
     assert np.array_equal(sk, packed[:n_sh]) and np.array_equal(pk, packed[n_sh:])
+
+
+# ---------------------------------------------------------------- P-MTP
+
+def test_pmtp_argmax_ties_go_to_the_smallest_id():
+    from oracle.pmtp import argmax_first
+    z = np.array([[1.0, 3.0, 3.0, -1.0], [0.0, 0.0, 0.0, 0.0], [-2.0, -1.0, -3.0, -1.0]])
+    assert argmax_first(z).tolist() == [1, 0, 1]
+
+
+def test_pmtp_acceptance_matches_its_definition_by_brute_force():
+    """n_acc = the largest n such that drafts 1..n all equal the verified token
+    one position earlier (brute force over every n)."""
+    from oracle.pmtp import accepted
+    rng = np.random.default_rng(0)
+    for _ in range(500):
+        k = int(rng.integers(1, 8))
+        fed = rng.integers(0, 3, size=k)
+        ver = rng.integers(0, 3, size=k)
+        want = max(n for n in range(k) if all(ver[i - 1] == fed[i] for i in range(1, n + 1)))
+        assert accepted(ver, fed) == want
+
+
+def test_pmtp_verify_closed_form():
+    """Unit-vector LM head: the argmax at a position is the coordinate where
+    its hidden state peaks; planted drafts are accepted up to the first plant
+    that disagrees."""
+    from oracle.pmtp import verify
+    V, H = 16, 8
+    w_lm = np.zeros((V, H))
+    w_lm[np.arange(H) * 2, np.arange(H)] = 1.0          # token 2c reads coordinate c
+    num_new = np.array([4, 1, 3])
+    peak = np.array([3, 5, 1, 0, 7, 2, 2, 6])            # per position
+    hidden = np.full((8, H), 0.01) + np.eye(H)[peak] * 4.0
+    tokens_in = np.array([9, 6, 10, 5, 3, 1, 4, 0])      # branch 0: drafts 6, 10 verified, 5 not
+    ver, n_acc, bonus, seed, _ = verify(hidden, tokens_in, num_new, None, w_lm)
+    assert ver.tolist() == (2 * peak).tolist()
+    assert n_acc.tolist() == [2, 0, 1] and bonus.tolist() == [2, 14, 4] and seed.tolist() == [2, 4, 6]
+
+
+def test_pmtp_draft_without_mlp_repeats_the_bonus_position():
+    """A zero down projection leaves the draft state unchanged, so every
+    drafted token is the LM head argmax of the seed state (closed form)."""
+    from oracle.pmtp import argmax_first, draft, lm_logits
+    rng = np.random.default_rng(1)
+    V, H, I = 32, 16, 8
+    f0 = rng.standard_normal((3, H))
+    w_lm = rng.standard_normal((V, H))
+    toks, logits = draft(f0, np.array([1, 2, 3]), 3, rng.standard_normal((V, H)), rng.standard_normal((I, 2 * H)),
+                         rng.standard_normal((I, 2 * H)), np.zeros((H, I)), None, w_lm, 1e-6)
+    base = argmax_first(lm_logits(f0, None, w_lm))
+    assert all(np.array_equal(toks[:, s], base) for s in range(3))
+
+
+def test_pmtp_draft_mlp_matches_torch():
+    """One draft advance against torch's own RMSNorm and SiLU in fp64 (library
+    routines)."""
+    import torch
+    from oracle.pmtp import draft_mlp
+    rng = np.random.default_rng(2)
+    V, H, I = 20, 16, 24
+    f = rng.standard_normal((5, H))
+    tok = rng.integers(0, V, size=5)
+    E, Wg, Wu, Wd = (rng.standard_normal(s) for s in ((V, H), (I, 2 * H), (I, 2 * H), (H, I)))
+    got = draft_mlp(f, tok, E, Wg, Wu, Wd, 1e-6)
+    t = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+    d = torch.cat([t(f), t(E)[torch.from_numpy(tok)]], dim=-1)
+    x = torch.nn.functional.rms_norm(d, (2 * H,), eps=1e-6)
+    want = t(f) + (torch.nn.functional.silu(x @ t(Wg).T) * (x @ t(Wu).T)) @ t(Wd).T
+    assert np.allclose(got, want.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_pmtp_lm_input_rounding_is_bf16():
+    """The LM head's input rounding equals the generator's integer bf16
+    rounding (round to nearest even on the bit pattern)."""
+    from oracle.pmtp import lm_logits
+    from workloads.gen import bf16_bits_to_f64, f64_to_bf16_bits
+    rng = np.random.default_rng(3)
+    h = rng.standard_normal((4, 64)) * 3
+    g = rng.standard_normal(64)
+    eye = np.eye(64)
+    got = lm_logits(h, g, eye)
+    want = bf16_bits_to_f64(f64_to_bf16_bits(h * g))
+    assert np.array_equal(got, want)

@@ -13,5 +13,6 @@ from .gen import (  # noqa: F401
     f64_to_bf16_bits,
     make_attn_batch,
     make_decode_inputs,
+    make_pmtp_inputs,
     make_structure,
 )

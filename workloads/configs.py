@@ -60,6 +60,10 @@ CONFIGS = {
         content_past=("lognormal", 128.0, 1.0, 8, 1024),
         model=dict(num_layers=18, hidden=1024, intermediate=3072,
                    weight_std=0.02, rms_eps=1e-6),
+        # P-MTP verification and drafting: the Qwen3 vocabulary size and a
+        # draft MLP as wide as the hidden state (neither is stated for the
+        # parser; readings in the design notes)
+        pmtp=dict(vocab=151936, draft_inner=1024, weight_std=0.02),
     ),
     # c3 with per-branch fork offsets (tree-shaped prefix): a content branch
     # sees the page's prefix only up to its fork point F_b, drawn uniform in

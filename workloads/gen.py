@@ -296,3 +296,29 @@ def make_decode_inputs(cfg_or_name, seed, num_layers=None):
         out.w_up.append(f64_to_bf16_bits(std * rng.standard_normal((I, H))))
         out.w_down.append(f64_to_bf16_bits(std * rng.standard_normal((H, I))))
     return out
+
+
+@dataclass
+class PmtpInputs:
+    """Weights of P-MTP verification and drafting (bf16 bits, torch Linear
+    layout): lm_head and embed [V][hidden], w_draft_gate and w_draft_up
+    [I_d][2 hidden], w_draft_down [hidden][I_d]; g_final None (ones)."""
+    vocab: int
+    draft_inner: int
+    lm_head: np.ndarray
+    embed: np.ndarray
+    w_draft_gate: np.ndarray
+    w_draft_up: np.ndarray
+    w_draft_down: np.ndarray
+    g_final: np.ndarray = None
+
+
+def make_pmtp_inputs(hidden, vocab, draft_inner, weight_std, seed):
+    """P-MTP weights drawn N(0, std^2) from their own stream (seed, 7), in the
+    order lm_head, embed, gate, up, down; they leave every other draw of the
+    workload unchanged."""
+    rng = np.random.default_rng([seed, 7])
+    w = lambda r, c: f64_to_bf16_bits(rng.standard_normal((r, c)) * weight_std)
+    return PmtpInputs(vocab=vocab, draft_inner=draft_inner, lm_head=w(vocab, hidden), embed=w(vocab, hidden),
+                      w_draft_gate=w(draft_inner, 2 * hidden), w_draft_up=w(draft_inner, 2 * hidden),
+                      w_draft_down=w(hidden, draft_inner))
