@@ -383,6 +383,7 @@ def bench_decode(args, torch, _lib):
         pm = make_pmtp_inputs(inp.hidden, c["vocab"], c["draft_inner"], c["weight_std"], args.seed)
         vd = VerifyDraft(step_obj, {k: dev(getattr(pm, k)) for k in ("lm_head", "embed", "w_draft_gate",
                                                                      "w_draft_up", "w_draft_down")})
+        pm_host = pm if not args.no_cpu_baseline else None   # the oracle's copy for the CPU leg
         del pm
         tokens_in = torch.from_numpy(np.random.default_rng(args.seed).integers(0, c["vocab"], size=step_obj.T)
                                      .astype(np.int32)).cuda()
@@ -445,6 +446,8 @@ def bench_decode(args, torch, _lib):
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_decode(inp, args.cpu_seconds, T)
+        if vd is not None:
+            cpu_pmtp(res["cpu_baseline"], inp, pm_host, tokens_in.cpu().numpy(), T)
     return res
 
 
@@ -469,6 +472,26 @@ def cpu_decode(inp, budget_s, T):
             "sample": f"first {n} of {inp.num_layers} layers of the same step (fp64 numpy, BLAS matmuls), "
                       f"scaled to the full step: {t:.2f} s/step",
             "cpu": model, "cpus_available": ncpu}
+
+
+def cpu_pmtp(cpu, inp, pm, tokens_in, T):
+    """Adds the oracle's verification and drafting of one step (fp64 LM head
+    over every position, then k - 1 draft advances per branch) to the
+    decode-step baseline.  The step's input hidden state stands in for its
+    output (same shape; the oracle's cost does not depend on the values)."""
+    from oracle.pmtp import draft, verify
+    f = lambda a: (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    W_lm, E = f(pm.lm_head), f(pm.embed)
+    Wg, Wu, Wd = f(pm.w_draft_gate), f(pm.w_draft_up), f(pm.w_draft_down)
+    t0 = time.perf_counter()
+    ver, n_acc, bonus, seed_row, _ = verify(inp.hidden_in, tokens_in, inp.num_new, None, W_lm)
+    draft(np.asarray(inp.hidden_in, np.float64)[seed_row], bonus, int(max(inp.num_new)) - 1, E, Wg, Wu, Wd,
+          None, W_lm, inp.rms_eps)
+    tp = time.perf_counter() - t0
+    t_step = T / cpu["value"] + tp
+    cpu["value"] = T / t_step
+    cpu["sample"] += f"; plus the oracle's P-MTP verification and drafting of the whole step ({tp:.2f} s)"
+    return cpu
 
 
 if __name__ == "__main__":

@@ -280,7 +280,7 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan,
  * position j - 1, and the branch accepts its longest verified prefix of
  * drafts, n_acc.  The argmax y* at the first unverified position is the
  * step's bonus token and the first token of the next step's window; the
- * lightweight residual MLP then drafts the rest of the window from that
+ * small residual MLP then drafts the rest of the window from that
  * position's hidden state: f <- f + SwiGLU(RMSNorm([f ; embed(token)]))
  * W_down^T, next token = argmax of the LM head on RMSNorm(f), as often as
  * the branch's window needs.

@@ -12,7 +12,7 @@ decoding and verification), with the readings recorded in the design notes:
   longest verified prefix s_1 .. s_n, and y*_n (the model's own token at the
   first unverified position) is the bonus token that opens the next window.
 * Drafting.  From the hidden state f at position n and token t = y*_n, the
-  lightweight residual MLP advances f <- f + SwiGLU(RMSNorm([f ; embed(t)]))
+  small residual MLP advances f <- f + SwiGLU(RMSNorm([f ; embed(t)]))
   W_down^T and the next drafted token is the LM head argmax on RMSNorm(f);
   repeated until the window (k tokens: the bonus token and k - 1 drafts) is
   full.
