@@ -295,6 +295,10 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan,
  *  w_draft_gate_up  gate/up of the draft MLP, [I_d][2 hidden] each, packed
  *                   with hpd_pack_gate_up
  *  w_draft_down     [hidden][I_d], packed with hpd_pack_weight_f16
+ *  window           tokens of the next window of every branch (the bonus
+ *                   token and window - 1 drafts), 0..HPD_MAX_K; 0 = the
+ *                   plan's largest k_b.  A branch that fed fewer tokens this
+ *                   step (one just started) still gets a full window.
  *
  * Argmax ties go to the smallest token id.  The LM head runs on the bf16
  * rounding of x = h * g_final; the positive per-token RMSNorm factor does not
@@ -307,6 +311,7 @@ typedef struct {
   const void *embed;
   const void *w_draft_gate_up;
   const void *w_draft_down;
+  int32_t window;
 } hpd_pmtp_desc;
 
 /* Bytes of device workspace hpd_verify_draft_step needs on top of
@@ -319,8 +324,9 @@ size_t hpd_pmtp_workspace_bytes(const hpd_model_desc *model, const hpd_pmtp_desc
  * verified    device int32 [T]: argmax token at each position (written)
  * n_acc       device int32 [num_branches]: accepted drafts, 0..k_b - 1
  * draft_out   device int32 [num_branches][HPD_MAX_K]: the next window of
- *             branch b in entries 0..k_b - 1 (entry 0 the bonus token);
- *             later entries unspecified
+ *             branch b in entries 0..W - 1 (entry 0 the bonus token; W =
+ *             pmtp->window, or the largest k_b if it is 0); later entries
+ *             unspecified
  * workspace   >= hpd_plan_workspace_bytes + hpd_pmtp_workspace_bytes,
  *             256-byte aligned, uploaded with hpd_plan_upload (it may be the
  *             decode step's workspace if it is large enough for both).
@@ -387,12 +393,15 @@ hpd_status hpd_attn_phase_isolation(int enable);
  *                       drafts), returning whole blocks past it; a root
  *                       cannot shrink below a live branch's fork_len.
  *  hpd_kv_seq_release   ends a sequence: a branch returns its blocks; a root
- *                       returns its blocks once its last branch is released.
+ *                       returns the blocks past every live branch's fork_len
+ *                       at once and the rest as the branches that see them
+ *                       are released (per-block reference counting).
  *  hpd_kv_seq_info      length, block count, parent (-1 for a root) and
  *                       fork_len of a live sequence.
  *  hpd_kv_seq_blocks    copies its block ids (capacity entries at most).
  *  hpd_kv_batch_tables  fills hpd_paged_kv tables for a batch: the block ids
- *                       of each page's root, then of each branch,
+ *                       of each page's root (live, or released with live
+ *                       branches), then of each (live) branch,
  *                       concatenated into blocks_out (capacity entries),
  *                       with page_block0_out / branch_block0_out; *entries is
  *                       the length needed (HPD_ERR_INVALID_ARGUMENT if above
@@ -412,6 +421,115 @@ hpd_status hpd_kv_batch_tables(const hpd_kv_pool *pool, int32_t num_pages, const
                                int32_t num_branches, const int32_t *branch_seq, int32_t *blocks_out,
                                int32_t capacity, int32_t *page_block0_out, int32_t *branch_block0_out,
                                int32_t *entries);
+
+/* ---- Host scheduler (section "Inference Workflow", Algorithm 1: FCFS
+ * scheduling with hierarchical parallel decoding).
+ *
+ * Requests.  A parent is a page: its layout branch decodes after a prefill of
+ * prompt_len rows (visual tokens and prompt, computed by the caller) that
+ * also gave its first token.  When a parent emits fork_token the scheduler
+ * spawns a child (a content branch) that sees the parent's rows before that
+ * token by reference and starts from child_token.  Request ids count up from
+ * 0 in order of submission or spawn and are also the arrival order.
+ *
+ * One engine iteration:
+ *  hpd_sched_schedule  sorts the waiting queue when forks dirtied it
+ *                      (children before parents; children by their parent's
+ *                      arrival, then by more live siblings first, then by
+ *                      their own arrival; parents by arrival), makes room in
+ *                      the K/V pool for every active request's next step
+ *                      (len + k rows), preempting the youngest active
+ *                      request while that fails (its unshared blocks are
+ *                      freed, its rows recomputed when it resumes, and it
+ *                      goes to the front of the queue), then admits from the
+ *                      queue's front: parents only while the pool's used
+ *                      blocks are <= kv_threshold * num_blocks and fewer than
+ *                      max_active requests are active; children regardless;
+ *                      a request whose K/V does not fit stops admission.
+ *                      It returns the step's batch.
+ *  (the caller)        computes the prefill rows the batch asks for, runs
+ *                      hpd_decode_step on the batch's plan (paged, with the
+ *                      batch's tables) and hpd_verify_draft_step with
+ *                      window = config window.
+ *  hpd_sched_commit    takes the verification results: each request keeps
+ *                      the rows of the tokens it fed up to its accepted
+ *                      drafts (len += n_acc + 1; the rest is rolled back),
+ *                      records its emitted tokens y*_0 .. y*_{n_acc} (eos ends
+ *                      it and is not recorded; so does reaching max_new
+ *                      recorded tokens), spawns a child per fork_token a
+ *                      parent emits, takes draft_out as its next window, and
+ *                      releases finished requests.  A page is output once
+ *                      its parent and every child of it have finished: the
+ *                      parent's tokens with each child's tokens right after
+ *                      the fork token that spawned the child.
+ *
+ * K/V.  The scheduler owns an hpd_kv_pool of num_blocks blocks of block_rows
+ * rows; the device K/V pools are the caller's (shared_k/v and priv_k/v of
+ * the step are the same pool tensors).  A page's rows (prompt + the
+ * parent's accepted tokens) form a root sequence; the parent branch reads
+ * them as its own rows (fork_len 0, past_len = its length) and writes its new
+ * rows after them; a child reads the page's first fork_len rows as the
+ * shared prefix and owns its rows.  Host memory only; not thread-safe. */
+typedef struct {
+  int32_t num_blocks;      /* K/V pool blocks (> 0)                          */
+  int32_t block_rows;      /* rows per block, a positive multiple of 64      */
+  double kv_threshold;     /* tau in [0, 1]                                   */
+  int32_t window;          /* K: tokens fed per step after the first, 1..HPD_MAX_K */
+  int32_t max_active;      /* N_max >= 1                                     */
+  int32_t fork_token, child_token, eos_token;
+} hpd_sched_config;
+
+/* The batch of one step.  Arrays are owned by the scheduler and valid until
+ * its next call.  num_branches = 0: nothing to run (commit with NULLs). */
+typedef struct {
+  int32_t num_pages, num_branches, num_tokens;
+  const int32_t *prefix_len;    /* [num_pages] P_p: the largest fork_len of
+                                   the page's children in the batch        */
+  const int32_t *branch_page;   /* [nb] pages in order of their parent's
+                                   arrival; a page's parent first, then its
+                                   children by arrival                     */
+  const int32_t *num_new;       /* [nb] tokens fed                          */
+  const int32_t *past_len;      /* [nb] rows before them                    */
+  const int32_t *fork_len;      /* [nb] parent 0, child its fork point       */
+  hpd_paged_kv paged;           /* the batch's block tables                 */
+  const int32_t *request;       /* [nb] request id                          */
+  const int32_t *tokens_in;     /* [num_tokens] tokens fed                  */
+  const int32_t *prefill_from;  /* [nb] rows prefill_from..prefill_to - 1 of
+                                   the branch's own rows (a parent: the
+                                   page's) must be computed before the step;
+                                   equal when none                          */
+  const int32_t *prefill_to;    /* [nb]                                     */
+  int32_t num_preempted;        /* requests preempted by this schedule      */
+  const int32_t *preempted;
+  int32_t num_admitted;         /* requests admitted by it, in order        */
+  const int32_t *admitted;
+} hpd_sched_batch;
+
+typedef struct hpd_sched hpd_sched;
+hpd_status hpd_sched_create(const hpd_sched_config *config, hpd_sched **out);
+void hpd_sched_destroy(hpd_sched *sched);
+/* A new page: prompt_len >= 1 prefill rows, its first token, at most
+ * max_new >= 1 recorded tokens per request (its children too). */
+hpd_status hpd_sched_submit(hpd_sched *sched, int32_t prompt_len, int32_t first_token, int32_t max_new,
+                            int32_t *request);
+hpd_status hpd_sched_schedule(hpd_sched *sched, hpd_sched_batch *out);
+/* verified [num_tokens], n_acc [num_branches] (0..num_new - 1), draft_out
+ * [num_branches][HPD_MAX_K] (entries 0..window - 1 read): HOST copies of
+ * hpd_verify_draft_step's outputs for the last scheduled batch.  Validated
+ * before anything changes. */
+hpd_status hpd_sched_commit(hpd_sched *sched, const int32_t *verified, const int32_t *n_acc,
+                            const int32_t *draft_out);
+/* The oldest finished page not yet taken: *page = its parent's id (-1 if
+ * none) and *len its tokens; they are copied and the page is dropped when
+ * capacity >= *len (tokens may be NULL with capacity 0 to ask the length). */
+hpd_status hpd_sched_next_output(hpd_sched *sched, int32_t *page, int32_t *tokens, int32_t capacity,
+                                 int32_t *len);
+/* Waiting and active requests, free pool blocks. */
+hpd_status hpd_sched_counts(const hpd_sched *sched, int32_t *waiting, int32_t *active, int32_t *free_blocks);
+/* state: 0 waiting, 1 active, 2 finished; len: rows of its own sequence;
+ * kept: of them, rows whose K/V is held; recorded: tokens recorded. */
+hpd_status hpd_sched_request(const hpd_sched *sched, int32_t request, int32_t *state, int32_t *len,
+                             int32_t *kept, int32_t *recorded);
 
 const char *hpd_status_string(hpd_status status);
 const char *hpd_last_error_message(void);

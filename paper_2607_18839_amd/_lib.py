@@ -83,7 +83,21 @@ HPD_WEIGHTS_TORCH, HPD_WEIGHTS_PACKED = 0, 1
 class hpd_pmtp_desc(ctypes.Structure):
     _fields_ = [("vocab", ctypes.c_int32), ("draft_inner", ctypes.c_int32), ("lm_head", ctypes.c_void_p),
                 ("g_final", ctypes.c_void_p), ("embed", ctypes.c_void_p), ("w_draft_gate_up", ctypes.c_void_p),
-                ("w_draft_down", ctypes.c_void_p)]
+                ("w_draft_down", ctypes.c_void_p), ("window", ctypes.c_int32)]
+
+
+class hpd_sched_config(ctypes.Structure):
+    _fields_ = [("num_blocks", ctypes.c_int32), ("block_rows", ctypes.c_int32), ("kv_threshold", ctypes.c_double),
+                ("window", ctypes.c_int32), ("max_active", ctypes.c_int32), ("fork_token", ctypes.c_int32),
+                ("child_token", ctypes.c_int32), ("eos_token", ctypes.c_int32)]
+
+
+class hpd_sched_batch(ctypes.Structure):
+    _fields_ = [("num_pages", ctypes.c_int32), ("num_branches", ctypes.c_int32), ("num_tokens", ctypes.c_int32),
+                ("prefix_len", c_i32p), ("branch_page", c_i32p), ("num_new", c_i32p), ("past_len", c_i32p),
+                ("fork_len", c_i32p), ("paged", hpd_paged_kv), ("request", c_i32p), ("tokens_in", c_i32p),
+                ("prefill_from", c_i32p), ("prefill_to", c_i32p), ("num_preempted", ctypes.c_int32),
+                ("preempted", c_i32p), ("num_admitted", ctypes.c_int32), ("admitted", c_i32p)]
 
 
 # Every symbol include/hpd.h declares, with its ctypes signature.
@@ -126,6 +140,14 @@ SIGNATURES = {
     "hpd_kv_seq_blocks": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, c_i32p, ctypes.c_int32]),
     "hpd_kv_batch_tables": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, c_i32p, ctypes.c_int32, c_i32p,
                                            c_i32p, ctypes.c_int32, c_i32p, c_i32p, c_i32p]),
+    "hpd_sched_create": (ctypes.c_int, [ctypes.POINTER(hpd_sched_config), ctypes.POINTER(ctypes.c_void_p)]),
+    "hpd_sched_destroy": (None, [ctypes.c_void_p]),
+    "hpd_sched_submit": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, c_i32p]),
+    "hpd_sched_schedule": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(hpd_sched_batch)]),
+    "hpd_sched_commit": (ctypes.c_int, [ctypes.c_void_p, c_i32p, c_i32p, c_i32p]),
+    "hpd_sched_next_output": (ctypes.c_int, [ctypes.c_void_p, c_i32p, c_i32p, ctypes.c_int32, c_i32p]),
+    "hpd_sched_counts": (ctypes.c_int, [ctypes.c_void_p, c_i32p, c_i32p, c_i32p]),
+    "hpd_sched_request": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, c_i32p, c_i32p, c_i32p, c_i32p]),
     "hpd_kernel_times_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int]),
     "hpd_kernel_kind_name": (ctypes.c_char_p, [ctypes.c_int]),
     "hpd_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -382,6 +404,87 @@ class KvPool:
                                            ctypes.byref(n)), "hpd_kv_batch_tables")
         return dict(block_rows=self.block_rows, num_blocks=self.num_blocks, blocks=blocks[:n.value],
                     page_block0=p0[:len(ps)], branch_block0=b0[:len(bs)])
+
+
+class Sched:
+    """hpd_sched: the host scheduler of the inference workflow (FCFS with
+    hierarchical parallel decoding) and the K/V block pool it owns."""
+
+    def __init__(self, num_blocks, block_rows, kv_threshold, window, max_active, fork_token, child_token,
+                 eos_token):
+        cfg = hpd_sched_config(num_blocks, block_rows, kv_threshold, window, max_active, fork_token, child_token,
+                               eos_token)
+        h = ctypes.c_void_p()
+        _check(load().hpd_sched_create(ctypes.byref(cfg), ctypes.byref(h)), "hpd_sched_create")
+        self.handle, self.window = h, int(window)
+        self.num_blocks, self.block_rows = int(num_blocks), int(block_rows)
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.hpd_sched_destroy(self.handle)
+            self.handle = None
+
+    def submit(self, prompt_len, first_token, max_new):
+        out = ctypes.c_int32()
+        _check(load().hpd_sched_submit(self.handle, prompt_len, first_token, max_new, ctypes.byref(out)),
+               "hpd_sched_submit")
+        return out.value
+
+    def schedule(self):
+        """The next step's batch as a dict of numpy copies (hpd_sched_batch)."""
+        b = hpd_sched_batch()
+        _check(load().hpd_sched_schedule(self.handle, ctypes.byref(b)), "hpd_sched_schedule")
+
+        def arr(p, n):
+            return np.ctypeslib.as_array(p, shape=(n,)).copy() if n > 0 else np.zeros(0, np.int32)
+
+        npg, nb, T = b.num_pages, b.num_branches, b.num_tokens
+        out = dict(num_pages=npg, num_branches=nb, num_tokens=T, prefix_len=arr(b.prefix_len, npg),
+                   branch_page=arr(b.branch_page, nb), num_new=arr(b.num_new, nb), past_len=arr(b.past_len, nb),
+                   fork_len=arr(b.fork_len, nb), request=arr(b.request, nb), tokens_in=arr(b.tokens_in, T),
+                   prefill_from=arr(b.prefill_from, nb), prefill_to=arr(b.prefill_to, nb),
+                   preempted=arr(b.preempted, b.num_preempted), admitted=arr(b.admitted, b.num_admitted))
+        out["paged"] = None if nb == 0 else dict(
+            block_rows=b.paged.block_rows, num_blocks=b.paged.num_blocks,
+            blocks=arr(b.paged.blocks, b.paged.num_entries), page_block0=arr(b.paged.page_block0, npg),
+            branch_block0=arr(b.paged.branch_block0, nb))
+        return out
+
+    def commit(self, verified, n_acc, draft_out):
+        """Host arrays: verified [T], n_acc [nb], draft_out [nb][HPD_MAX_K]."""
+        v, n = _i32(verified), _i32(n_acc)
+        d = None if draft_out is None else np.ascontiguousarray(draft_out, dtype=np.int32)
+        if d is not None and d.size and d.shape[-1] != HPD_MAX_K:
+            raise ValueError("draft_out must be [num_branches][HPD_MAX_K]")
+        _check(load().hpd_sched_commit(self.handle, _ptr(v, c_i32p) if v is not None and v.size else None,
+                                       _ptr(n, c_i32p) if n is not None and n.size else None,
+                                       _ptr(d, c_i32p) if d is not None and d.size else None), "hpd_sched_commit")
+
+    def next_output(self):
+        """(page id, tokens) of the oldest finished page, or None."""
+        lib = load()
+        page, n = ctypes.c_int32(), ctypes.c_int32()
+        _check(lib.hpd_sched_next_output(self.handle, ctypes.byref(page), None, 0, ctypes.byref(n)),
+               "hpd_sched_next_output")
+        if page.value < 0:
+            return None
+        if n.value == 0:   # an empty page was taken by the query itself
+            return page.value, np.zeros(0, np.int32)
+        buf = np.zeros(n.value, np.int32)
+        _check(lib.hpd_sched_next_output(self.handle, ctypes.byref(page), _ptr(buf, c_i32p), n.value,
+                                         ctypes.byref(n)), "hpd_sched_next_output")
+        return page.value, buf[:n.value]
+
+    def counts(self):
+        v = [ctypes.c_int32() for _ in range(3)]
+        _check(load().hpd_sched_counts(self.handle, *[ctypes.byref(x) for x in v]), "hpd_sched_counts")
+        return dict(waiting=v[0].value, active=v[1].value, free_blocks=v[2].value)
+
+    def request(self, rid):
+        v = [ctypes.c_int32() for _ in range(4)]
+        _check(load().hpd_sched_request(self.handle, rid, *[ctypes.byref(x) for x in v]), "hpd_sched_request")
+        return dict(state=("waiting", "active", "done")[v[0].value], len=v[1].value, kept=v[2].value,
+                    recorded=v[3].value)
 
 
 def hpd_pmtp_workspace_bytes(model, pmtp, plan):

@@ -21,7 +21,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 HIP_SOURCES = ["attn_kernels.hip", "gemm_kernels.hip", "decode.hip", "pmtp.hip", "timing.hip", "api.hip"]
-CXX_SOURCES = ["plan.cpp", "kv_pool.cpp"]
+CXX_SOURCES = ["plan.cpp", "kv_pool.cpp", "scheduler.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-I" + os.path.join(ROOT, "include"), "-I" + CSRC]
 # Packed fp32 VALU forms are disabled for all device code.  MFMA results

@@ -31,6 +31,21 @@ struct hpd_kv_pool {
   std::vector<int32_t> free_ids;
 
   int64_t blocks_for(int64_t rows) const { return (rows + block_rows - 1) / block_rows; }
+  // Returns the blocks of a released root that no live branch sees any more
+  // (a block is freed when its last reference goes, as with per-block
+  // reference counts).
+  void trim_released_root(int32_t id) {
+    int32_t need = 0;
+    for (const Seq &c : seqs)
+      if (c.live && c.parent == id) need = std::max(need, c.fork_len);
+    Seq &r = seqs[id];
+    const size_t keep = (size_t)blocks_for(need);
+    while (r.blocks.size() > keep) {
+      free_list.push_back(r.blocks.back());
+      r.blocks.pop_back();
+    }
+    r.len = std::min(r.len, need);
+  }
   void give_back(Seq &s) {
     for (auto it = s.blocks.rbegin(); it != s.blocks.rend(); ++it) free_list.push_back(*it);
     s.blocks.clear();
@@ -47,6 +62,11 @@ hpd_status err(hpd_status st, const std::string &msg) {
 
 bool live_seq(const hpd_kv_pool *p, int32_t s) {
   return p && s >= 0 && s < (int32_t)p->seqs.size() && p->seqs[s].live;
+}
+
+// Live, or a released root still holding blocks for its live branches.
+bool holding_seq(const hpd_kv_pool *p, int32_t s) {
+  return p && s >= 0 && s < (int32_t)p->seqs.size() && (p->seqs[s].live || p->seqs[s].holds);
 }
 
 }  // namespace
@@ -164,8 +184,11 @@ hpd_status hpd_kv_seq_release(hpd_kv_pool *pool, int32_t seq) {
     const int32_t parent = s.parent;
     retire(seq);
     if (--root.branches == 0 && !root.live) retire(parent);
+    else if (!root.live) pool->trim_released_root(parent);
   } else if (s.branches == 0) {
     retire(seq);
+  } else {
+    pool->trim_released_root(seq);
   }
   return HPD_OK;
 }
@@ -200,7 +223,8 @@ hpd_status hpd_kv_batch_tables(const hpd_kv_pool *pool, int32_t num_pages, const
   int64_t n = 0;
   for (int32_t i = 0; i < num_pages + num_branches; ++i) {
     const int32_t id = i < num_pages ? page_seq[i] : branch_seq[i - num_pages];
-    if (!live_seq(pool, id)) return err(HPD_ERR_INVALID_ARGUMENT, "hpd_kv_batch_tables: not a live sequence");
+    if (i < num_pages ? !holding_seq(pool, id) : !live_seq(pool, id))
+      return err(HPD_ERR_INVALID_ARGUMENT, "hpd_kv_batch_tables: not a live sequence");
     n += (int64_t)pool->seqs[id].blocks.size();
   }
   if (n > INT32_MAX) return err(HPD_ERR_INVALID_ARGUMENT, "hpd_kv_batch_tables: too many entries");

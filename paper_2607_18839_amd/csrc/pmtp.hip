@@ -46,7 +46,7 @@ PmtpLayout pmtp_layout(const hpd_model_desc &m, const hpd_pmtp_desc &d, const Pl
   L.H = m.hidden;
   L.V = d.vocab;
   L.Id = d.draft_inner;
-  L.kmax = *std::max_element(P.num_new.begin(), P.num_new.end());
+  L.kmax = d.window > 0 ? d.window : *std::max_element(P.num_new.begin(), P.num_new.end());
   L.ntile = d.vocab / kGemmTile;
   size_t off = align256(P.workspace_bytes);
   auto take = [&](size_t bytes) {
@@ -218,6 +218,7 @@ hpd_status validate(const hpd_model_desc *m, const hpd_pmtp_desc *d, const hpd_p
     return HPD_ERR_UNSUPPORTED;
   }
   if (!(m->rms_eps >= 0.f) || m->rms_eps > 1.f) { *err = "rms_eps out of range"; return HPD_ERR_INVALID_ARGUMENT; }
+  if (d->window < 0 || d->window > HPD_MAX_K) { *err = "window must be in 0..HPD_MAX_K"; return HPD_ERR_INVALID_ARGUMENT; }
   auto bad = [](const void *p) { return !p || ((uintptr_t)p & 15); };
   if (bad(d->lm_head) || bad(d->embed) || bad(d->w_draft_gate_up) || bad(d->w_draft_down) ||
       (d->g_final && ((uintptr_t)d->g_final & 15))) {
@@ -305,7 +306,7 @@ hpd_status hpd_verify_draft_step(const hpd_model_desc *model, const hpd_pmtp_des
                 tokens_in, hidden, L.H, verified, n_acc, draft_out, f, tok);
     e = hipGetLastError();
   }
-  // drafting: iterations 1 .. kmax - 1
+  // drafting: iterations 1 .. W - 1 (W = the window)
   for (int it = 1; it < L.kmax && e == hipSuccess; ++it) {
     hpd::launch(hpd::KK_DRAFT_MLP, hpd::draft_input_kernel, dim3(L.nbpad), dim3(256), stream, it, L.nb, L.ntile,
                 amax_d, (const __bf16 *)pmtp->embed, f, L.H, x_d, ss_d, tok, draft_out);

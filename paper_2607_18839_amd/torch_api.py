@@ -133,10 +133,12 @@ class VerifyDraft:
     'w_draft_up' [I_d][2 hidden], 'w_draft_down' [hidden][I_d] (bf16 device
     tensors, torch Linear layout) and optionally 'g_final' [hidden]; the
     projections are packed once here.  ``step`` is the DecodeStep whose plan
-    and workspace it shares (the workspace is enlarged if needed).
+    and workspace it shares (the workspace is enlarged if needed).  ``window``
+    is the next window's length per branch (hpd_pmtp_desc.window; 0 = the
+    largest k_b of the step).
     """
 
-    def __init__(self, step, pmtp, stream=None):
+    def __init__(self, step, pmtp, stream=None, window=0):
         self.step = step
         self.vocab, self.hidden = pmtp["lm_head"].shape
         self.draft_inner = pmtp["w_draft_gate"].shape[0]
@@ -147,7 +149,7 @@ class VerifyDraft:
         g = self._w["g_final"]
         self.desc = _lib.hpd_pmtp_desc(self.vocab, self.draft_inner, self._w["lm_head"].data_ptr(),
                                        None if g is None else g.data_ptr(), self._w["embed"].data_ptr(),
-                                       self._w["gate_up"].data_ptr(), self._w["down"].data_ptr())
+                                       self._w["gate_up"].data_ptr(), self._w["down"].data_ptr(), window)
         plan = step.attn.plan
         self.ws_bytes = step.plan_bytes + _lib.hpd_pmtp_workspace_bytes(step.model, self.desc, plan)
         if self.ws_bytes > step.ws_bytes:   # one workspace for both steps

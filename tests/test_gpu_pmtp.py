@@ -40,14 +40,14 @@ def _valid_argmax(tokens, logits, what):
     return float(np.mean(tokens == logits.argmax(axis=-1)))
 
 
-def _run(inp, pm, plant_seed):
+def _run(inp, pm, plant_seed, window=0):
     from paper_2607_18839_amd.torch_api import DecodeStep, VerifyDraft
     w = {k: [to_dev(a, "bf16") for a in getattr(inp, k)] for k in ("w_qkv", "w_o", "w_gate", "w_up", "w_down")}
     step = DecodeStep(inp.num_q_heads, inp.num_kv_heads, inp.prefix_len, inp.branch_page, inp.num_new,
                       inp.past_len, w, inp.hidden, inp.intermediate, inp.rms_eps, packed=True)
     pw = {k: to_dev(getattr(pm, k), "bf16") for k in ("lm_head", "embed", "w_draft_gate", "w_draft_up",
                                                        "w_draft_down")}
-    vd = VerifyDraft(step, pw)
+    vd = VerifyDraft(step, pw, window=window)
     sk = [to_dev(a, "bf16") for a in inp.shared_k]
     sv = [to_dev(a, "bf16") for a in inp.shared_v]
     pk = [to_dev(a, "bf16") for a in inp.priv_k]
@@ -76,8 +76,8 @@ def _run(inp, pm, plant_seed):
     return h64, tokens, np.array(planted), ver.cpu().numpy(), n_acc.cpu().numpy(), drafts.cpu().numpy()
 
 
-def _check(inp, pm, plant_seed):
-    h64, tokens, planted, ver, n_acc, drafts = _run(inp, pm, plant_seed)
+def _check(inp, pm, plant_seed, window=0):
+    h64, tokens, planted, ver, n_acc, drafts = _run(inp, pm, plant_seed, window)
     f64 = lambda a: (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
     W_lm, E = f64(pm.lm_head), f64(pm.embed)
     Wg, Wu, Wd = f64(pm.w_draft_gate), f64(pm.w_draft_up), f64(pm.w_draft_down)
@@ -90,13 +90,13 @@ def _check(inp, pm, plant_seed):
         assert drafts[b, 0] == ver[q + n_acc[b]], b
         if np.array_equal(ver[q:q + k], ver_o[q:q + k]):
             assert n_acc[b] == planted[b], b
-    kmax = int(inp.num_new.max())
+    W = window or int(inp.num_new.max())   # every branch gets a window of W tokens
     seed = q0 + n_acc
-    forced = drafts[:, 1:kmax].astype(np.int64)
-    _, step_logits = draft(h64[seed], drafts[:, 0].astype(np.int64), kmax - 1, E, Wg, Wu, Wd, None, W_lm,
+    forced = drafts[:, 1:W].astype(np.int64)
+    _, step_logits = draft(h64[seed], drafts[:, 0].astype(np.int64), W - 1, E, Wg, Wu, Wd, None, W_lm,
                            inp.rms_eps, forced=forced)
     for s, lg in enumerate(step_logits):
-        need = np.nonzero(inp.num_new > s + 1)[0]   # branches whose window uses draft s + 1
+        need = np.arange(nb)
         _valid_argmax(forced[need, s], lg[need], f"draft {s + 1}")
     print(f"verified tokens equal to the oracle argmax: {agree:.3f}; n_acc {n_acc.tolist()}")
     return agree
@@ -108,6 +108,15 @@ def test_verify_draft_small(seed):
     inp = small_inputs(seed)
     pm = make_pmtp_inputs(inp.hidden, 2048, 256, 0.05, seed)
     assert _check(inp, pm, seed) > 0.9
+
+
+def test_verify_draft_window_longer_than_the_step():
+    """window = 7 > every k_b: each branch, including those that fed one
+    token, gets the bonus token and 6 drafts."""
+    announce("pmtp small window 7")
+    inp = small_inputs(2)
+    pm = make_pmtp_inputs(inp.hidden, 1024, 128, 0.05, 2)
+    assert _check(inp, pm, 2, window=7) > 0.9
 
 
 def test_verify_draft_c4_full_vocab():

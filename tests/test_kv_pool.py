@@ -57,13 +57,13 @@ def test_fork_is_zero_copy_and_keeps_the_prefix_alive():
         pool.new(kids[0], 0)               # branches of branches are not sequences here
     with pytest.raises(_lib.HpdError):
         pool.new(root, 201)                # beyond the root's length
-    pool.release(root)                     # kept while branches live
+    pool.release(root)                     # kept while branches see it
     assert pool.free_blocks() == 6
     with pytest.raises(_lib.HpdError):
         pool.new(root, 0)
     pool.release(kids[0])
-    pool.release(kids[2])
-    assert pool.free_blocks() == 10
+    pool.release(kids[2])                  # the 2 private blocks each, and the root
+    assert pool.free_blocks() == 13        # blocks past the last fork (64 rows: 1 kept)
     pool.release(kids[1])                  # last branch: the prefix blocks return too
     assert pool.free_blocks() == 16
     r2 = pool.new()
@@ -127,8 +127,9 @@ def test_random_operations_match_a_reference_model():
                 info = pool.info(s)
                 assert info["len"] == m["len"] and info["num_blocks"] == -(-m["len"] // B)
                 held += pool.blocks(s).tolist()
-            elif m["parent"] == -1 and alive_kids:
-                held += [None] * -(-m["len"] // B)
+            elif m["parent"] == -1 and alive_kids:   # released root: the blocks its branches see
+                fmax = max(k["fork"] for k in model.values() if k["live"] and k["parent"] == s)
+                held += [None] * -(-fmax // B)
         assert len(held) + pool.free_blocks() == NB
         ids = [b for b in held if b is not None]
         assert len(set(ids)) == len(ids) and all(0 <= b < NB for b in ids)
