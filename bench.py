@@ -1,6 +1,6 @@
 """Benchmark of the branch-parallel decode step on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4|c3|c3f|c5|c2|c1]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4|c3|c3f|c5|c2|c1|engine]
 
 A step is one pass of the whole hot path over one batch of seeded synthetic
 input already resident in HBM.  The default workload is c4, the full decode
@@ -90,6 +90,8 @@ def main():
     _lib.load()
     if args.workload == "c4":
         res = bench_decode(args, torch, _lib)
+    elif args.workload == "engine":
+        res = bench_engine(args, torch, _lib)
     else:
         res = bench_attention(args, torch, _lib)
     print(json.dumps(res))
@@ -472,6 +474,99 @@ def cpu_decode(inp, budget_s, T):
             "sample": f"first {n} of {inp.num_layers} layers of the same step (fp64 numpy, BLAS matmuls), "
                       f"scaled to the full step: {t:.2f} s/step",
             "cpu": model, "cpus_available": ncpu}
+
+
+def bench_engine(args, torch, _lib):
+    """The continuous-batching loop (host scheduler -> embedding lookup ->
+    paged decode step -> P-MTP verification and drafting -> commit) on the
+    c4 decoder with the 151,936-token LM head, over a closed-loop stream of
+    16 pages in flight (a finished page is replaced by a new one; prompt
+    U[1024, 4096] rows) whose layout branches fork U{4..32} content
+    branches each (fork tokens planted at the bonus token, each step with
+    probability 1/2, until the page has its count); every request records
+    at most 64 tokens.  Prefill rows are a synthetic fill.  Timed: K
+    iterations after W, each ending with the host reading the verified
+    tokens (the scheduler needs them)."""
+    from paper_2607_18839_amd.engine import Engine
+    from workloads import get_config, make_decode_inputs, make_pmtp_inputs
+    inp = make_decode_inputs("c4", args.seed, num_layers=args.layers)
+    c = get_config("c4")["pmtp"]
+    pm = make_pmtp_inputs(inp.hidden, c["vocab"], c["draft_inner"], c["weight_std"], args.seed)
+
+    def dev(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+    w = {k: [dev(a) for a in getattr(inp, k)] for k in ("w_qkv", "w_o", "w_gate", "w_up", "w_down")}
+    pw = {k: dev(getattr(pm, k)) for k in ("lm_head", "embed", "w_draft_gate", "w_draft_up", "w_draft_down")}
+    FORK, CHILD, EOS = c["vocab"] - 3, c["vocab"] - 2, c["vocab"] - 1
+    cfg = dict(num_blocks=4096, block_rows=64, kv_threshold=0.9, window=4, max_active=16, fork_token=FORK,
+               child_token=CHILD, eos_token=EOS)
+    eng = Engine(w, pw, inp.hidden, inp.intermediate, inp.num_q_heads, inp.num_kv_heads, cfg, rms_eps=inp.rms_eps)
+    del w, pw
+    rng = np.random.default_rng([args.seed, 11])
+    want_children, spawned = {}, {}
+
+    def new_page():
+        pid = eng.submit(int(rng.integers(1024, 4097)), int(rng.integers(0, c["vocab"] - 3)), 64)
+        want_children[pid], spawned[pid] = int(rng.integers(4, 33)), 0
+
+    for _ in range(16):
+        new_page()
+
+    def plant(batch):
+        q = 0
+        for b, k in enumerate(batch["num_new"]):
+            r = int(batch["request"][b])
+            if batch["fork_len"][b] == 0 and spawned.get(r, 0) < want_children.get(r, 0) and rng.random() < 0.5:
+                batch["verified"][q + batch["n_acc"][b]] = FORK
+                batch["draft_out"][b, 0] = FORK
+                spawned[r] += 1
+            q += k
+
+    eng.on_results = plant
+
+    def step():   # one iteration; a finished page is replaced by a new one (16 pages in flight)
+        b = eng.step()
+        for _ in eng.outputs():
+            new_page()
+        return b
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    eng.host_s = dict(schedule=0.0, plan=0.0, commit=0.0)
+    tokens = branches = emitted = idle = pages_done = 0
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        n0 = len(want_children)
+        b = step()
+        pages_done += len(want_children) - n0
+        if b["num_branches"] == 0:
+            idle += 1
+            continue
+        tokens += b["num_tokens"]
+        branches += b["num_branches"]
+        emitted += int(np.sum(b["n_acc"]) + b["num_branches"])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    K = args.steps
+    cnt = eng.sched.counts()
+    return {
+        "metric": "branch-tokens/s per decode step", "value": tokens / wall, "unit": "branch-tokens/s",
+        "n_gpus": 1, "steps": K, "warmup": args.warmup, "ms_per_step": wall / K * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "timing": "wall clock of K engine iterations (host scheduling, plan, upload, GPU step, result read-back)",
+        "data": "synthetic (seeded N(0,0.02) bf16 weights; prefill rows a seeded N(0,1) fill; planted fork tokens)",
+        "config": {"workload": "engine: Algorithm 1 continuous batching, c4 decoder (18 layers) + P-MTP "
+                               "(151,936-token vocab, window 4), 16 pages in flight, prompt U[1024, 4096], "
+                               "U{4..32} forks per page, <= 64 tokens per request",
+                   "sched": {k: v for k, v in cfg.items() if not k.endswith("token")}},
+        "engine": {"mean_tokens_per_step": tokens / max(K - idle, 1),
+                   "mean_branches_per_step": branches / max(K - idle, 1), "idle_steps": idle,
+                   "emitted_tokens_per_s": emitted / wall,
+                   "host_ms_per_step": {k: v / K * 1e3 for k, v in eng.host_s.items()},
+                   "after": cnt, "children_spawned": int(sum(spawned.values())), "pages_finished": pages_done},
+    }
 
 
 def cpu_pmtp(cpu, inp, pm, tokens_in, T):

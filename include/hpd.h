@@ -314,6 +314,14 @@ typedef struct {
   int32_t window;
 } hpd_pmtp_desc;
 
+/* The input of a decode step from the tokens it feeds: out[t][:] = the
+ * embedding row of tokens[t] as fp32.  embed [vocab][hidden] bf16 (8-byte
+ * aligned), tokens device int32 [T], out device float [T][hidden] (16-byte
+ * aligned); hidden a positive multiple of 4.  An id outside 0..vocab-1
+ * gives a zero row. */
+hpd_status hpd_embed_tokens(const void *embed, int32_t vocab, int32_t hidden, const int32_t *tokens, int32_t T,
+                            float *out, void *stream);
+
 /* Bytes of device workspace hpd_verify_draft_step needs on top of
  * hpd_plan_workspace_bytes. */
 size_t hpd_pmtp_workspace_bytes(const hpd_model_desc *model, const hpd_pmtp_desc *pmtp, const hpd_plan *plan);
@@ -347,7 +355,7 @@ hpd_status hpd_verify_draft_step(const hpd_model_desc *model, const hpd_pmtp_des
  * eager launches: do not enable it while capturing a graph.  keep_pairs = 1
  * keeps the pairs assigned after the read (re-read after re-running the same
  * launches); keep_pairs = 0 releases them. */
-#define HPD_NUM_KERNEL_KINDS 12
+#define HPD_NUM_KERNEL_KINDS 13
 typedef struct {
   int64_t count[HPD_NUM_KERNEL_KINDS];
   double total_ms[HPD_NUM_KERNEL_KINDS];
@@ -358,7 +366,7 @@ hpd_status hpd_kernel_times_read(hpd_kernel_times *out, int keep_pairs);
 /* Kind k: 0 shared_prefix, 1 private, 2 merge, 3 gemm_qkv, 4 gemm_o,
  * 5 gemm_gate_up, 6 gemm_down, 7 norm_input, 8 lm_head, 9 verify,
  * 10 draft_mlp (the draft MLP's two projections and its input),
- * 11 draft_token.  With bf16 inputs kind 0 is
+ * 11 draft_token, 12 embed.  With bf16 inputs kind 0 is
  * one launch that runs the shared-prefix and the private work items (kind 1
  * is then never launched) unless phase isolation is on. */
 const char *hpd_kernel_kind_name(int kind);

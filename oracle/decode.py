@@ -59,7 +59,9 @@ def silu(u):
 
 
 def decode_step(inp, num_layers=None):
-    """Run the step on ``workloads.DecodeInputs``.
+    """Run the step on ``workloads.DecodeInputs`` (an optional ``fork_len``
+    attribute gives per-branch fork points, section "Layout-Coordinated
+    Parallel Decoding": a branch sees its page's prefix up to its fork).
 
     Returns (h_out [T][hidden] fp64, new_k, new_v) where new_k[l] and
     new_v[l] are uint16 arrays [T][Hkv][D] with the bf16 bits the step writes
@@ -68,12 +70,13 @@ def decode_step(inp, num_layers=None):
     """
     Lyr = inp.num_layers if num_layers is None else num_layers
     Hq, Hkv, D = inp.num_q_heads, inp.num_kv_heads, inp.head_dim
-    plan = canonical_plan(inp.prefix_len, inp.branch_page, inp.num_new, inp.past_len)
+    fork = getattr(inp, "fork_len", None)   # per-branch fork points; None = the whole prefix
+    plan = canonical_plan(inp.prefix_len, inp.branch_page, inp.num_new, inp.past_len, fork)
     T = plan["T"]
     dest = (plan["priv_row"][plan["token_branch"]] +
             np.asarray(inp.past_len, np.int64)[plan["token_branch"]] + plan["token_j"])
     st = dict(prefix_len=inp.prefix_len, branch_page=inp.branch_page,
-              num_new=inp.num_new, past_len=inp.past_len)
+              num_new=inp.num_new, past_len=inp.past_len, fork_len=fork)
     h = np.asarray(inp.hidden_in, dtype=np.float64).copy()
     new_k, new_v = [], []
     for l in range(Lyr):

@@ -129,6 +129,8 @@ SIGNATURES = {
                                              ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                              ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                              ctypes.c_void_p]),
+    "hpd_embed_tokens": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                        ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]),
     "hpd_kv_pool_create": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_void_p)]),
     "hpd_kv_pool_destroy": (None, [ctypes.c_void_p]),
     "hpd_kv_pool_free_blocks": (ctypes.c_int32, [ctypes.c_void_p]),
@@ -311,7 +313,7 @@ def hpd_decode_step(model, plan, hidden_in, hidden_out, shared_k, shared_v, priv
                                   stream), "hpd_decode_step")
 
 
-HPD_NUM_KERNEL_KINDS = 12
+HPD_NUM_KERNEL_KINDS = 13
 
 
 class hpd_kernel_times(ctypes.Structure):
@@ -496,3 +498,7 @@ def hpd_verify_draft_step(model, pmtp, plan, hidden, tokens_in, verified, n_acc,
     _check(load().hpd_verify_draft_step(ctypes.byref(model), ctypes.byref(pmtp), plan.handle, hidden, tokens_in,
                                         verified, n_acc, draft_out, workspace, workspace_bytes, stream),
            "hpd_verify_draft_step")
+
+
+def hpd_embed_tokens(embed, vocab, hidden, tokens, T, out, stream=None):
+    _check(load().hpd_embed_tokens(embed, vocab, hidden, tokens, T, out, stream), "hpd_embed_tokens")

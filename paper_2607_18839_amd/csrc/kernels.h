@@ -28,7 +28,7 @@ PlanDev plan_dev(const Plan &P, void *workspace);
 
 // Kernel kinds of the optional benchmark timing (hpd_kernel_timing).
 enum KernelKind { KK_SHARED = 0, KK_PRIVATE, KK_MERGE, KK_GEMM_QKV, KK_GEMM_O, KK_GEMM_GATE_UP,
-                  KK_GEMM_DOWN, KK_NORM, KK_LM_HEAD, KK_VERIFY, KK_DRAFT_MLP, KK_DRAFT_TOKEN };
+                  KK_GEMM_DOWN, KK_NORM, KK_LM_HEAD, KK_VERIFY, KK_DRAFT_MLP, KK_DRAFT_TOKEN, KK_EMBED };
 // Element offset of (row, col) of a [rows][cols] 16-bit matrix in the packed
 // layout (tiles of 32 rows x 64 columns, 2048 elements each, ordered by row
 // tile then column tile; inside a tile, element e of 16-byte piece (j, l) is

@@ -200,6 +200,23 @@ __global__ __launch_bounds__(256) void draft_input_kernel(int it, int nb, int nt
   }
 }
 
+// Embedding rows of the tokens a step feeds, as fp32 (one workgroup per token).
+__global__ __launch_bounds__(256) void embed_kernel(const __bf16 *embed, int V, int H, const int32_t *tokens,
+                                                    float *out) {
+  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  const int t = blockIdx.x, tok = tokens[t];
+  const bool ok = tok >= 0 && tok < V;
+  for (int c = 4 * threadIdx.x; c < H; c += 1024) {
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    if (ok) {
+      const bf16x4 e = *(const bf16x4 *)(embed + (int64_t)tok * H + c);
+      v = f32x4{(float)e[0], (float)e[1], (float)e[2], (float)e[3]};
+    }
+    *(f32x4 *)(out + (int64_t)t * H + c) = v;
+  }
+}
+
 // The last drafted token of each branch.
 __global__ __launch_bounds__(256) void draft_token_kernel(int it, int ntile, const uint64_t *amax,
                                                           int32_t *draft_out) {
@@ -232,6 +249,24 @@ hpd_status validate(const hpd_model_desc *m, const hpd_pmtp_desc *d, const hpd_p
 }  // namespace hpd
 
 extern "C" {
+
+hpd_status hpd_embed_tokens(const void *embed, int32_t vocab, int32_t hidden, const int32_t *tokens, int32_t T,
+                            float *out, void *stream) {
+  if (!embed || !tokens || !out || vocab < 1 || hidden < 4 || hidden % 4 || T < 0 || ((uintptr_t)embed & 7) ||
+      ((uintptr_t)out & 15)) {
+    hpd::set_last_error("hpd_embed_tokens: NULL or misaligned pointer, or bad sizes");
+    return HPD_ERR_INVALID_ARGUMENT;
+  }
+  if (T == 0) return HPD_OK;
+  hpd::launch(hpd::KK_EMBED, hpd::embed_kernel, dim3(T), dim3(256), (hipStream_t)stream, (const __bf16 *)embed,
+              (int)vocab, (int)hidden, tokens, out);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    hpd::set_last_error(std::string("hpd_embed_tokens: ") + hipGetErrorString(e));
+    return HPD_ERR_HIP;
+  }
+  return HPD_OK;
+}
 
 size_t hpd_pmtp_workspace_bytes(const hpd_model_desc *model, const hpd_pmtp_desc *pmtp, const hpd_plan *plan) {
   std::string err;
