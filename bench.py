@@ -499,7 +499,7 @@ def bench_engine(args, torch, _lib):
     w = {k: [dev(a) for a in getattr(inp, k)] for k in ("w_qkv", "w_o", "w_gate", "w_up", "w_down")}
     pw = {k: dev(getattr(pm, k)) for k in ("lm_head", "embed", "w_draft_gate", "w_draft_up", "w_draft_down")}
     FORK, CHILD, EOS = c["vocab"] - 3, c["vocab"] - 2, c["vocab"] - 1
-    cfg = dict(num_blocks=4096, block_rows=64, kv_threshold=0.9, window=4, max_active=16, fork_token=FORK,
+    cfg = dict(num_blocks=4096, block_rows=64, kv_threshold=0.9, window=4, max_active=64, fork_token=FORK,
                child_token=CHILD, eos_token=EOS)
     eng = Engine(w, pw, inp.hidden, inp.intermediate, inp.num_q_heads, inp.num_kv_heads, cfg, rms_eps=inp.rms_eps)
     del w, pw

@@ -76,10 +76,10 @@ hipError_t launch_norm_input(const float *h_in, float *h, int T, int Tpad, int H
 hipError_t launch_pack_weight(const __bf16 *w, const __bf16 *w2, int rows, int cols, bool gate_up, bool to_f16,
                               __bf16 *out, hipStream_t stream);
 // f16: fp16 GEMM (bf16 weights converted to fp16 in registers, fp16
-// activations); epi: kEpi*.
+// activations); epi: kEpiQKV, kEpiResidual or kEpiSwiGLU.
 hipError_t launch_gemm(const GemmArgs &g, bool f16, int epi, int kind, hipStream_t stream);
-// LM head with the argmax epilogue (bf16, packed operands) for Tpad <= 160:
-// 128 rows per workgroup against every token tile; n_slices = N / 128.
+// LM head with the argmax epilogue (bf16, packed operands): 128 rows per
+// workgroup against a group of up to 5 token tiles; n_slices = N / 128.
 hipError_t launch_lm_argmax(const GemmArgs &g, int kind, hipStream_t stream);
 
 // Row groups per workgroup for an N x K projection over Tpad tokens, from a

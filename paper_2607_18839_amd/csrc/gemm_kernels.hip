@@ -78,9 +78,7 @@ __device__ __forceinline__ void load_early(const GemmArgs &g, int t, EpilogueIn 
 
 template <int EPI>
 __device__ __forceinline__ void load_late(const GemmArgs &g, int t, int tile, int half, EpilogueIn &in) {
-  if constexpr (EPI == kEpiArgmax) {
-    // nothing: the argmax needs no norm factor (a positive per-token scale)
-  } else if constexpr (EPI == kEpiResidual) {
+  if constexpr (EPI == kEpiResidual) {
     const float *hr = g.h + (int64_t)min(t, g.T - 1) * g.N + tile * kGemmTile + 4 * half;
 #pragma unroll
     for (int i = 0; i < 4; ++i) in.h[i] = *(const f32x4 *)(hr + 8 * i);
@@ -479,22 +477,25 @@ __global__ __launch_bounds__(256) void gemm_packed_kernel(GemmArgs g) {
   epilogue<EPI>(g, acc, ein, t, tile, half);
 }
 
-// LM head with the argmax epilogue for up to 5 token tiles (T <= 160): a
-// workgroup of 4 waves owns 128 vocabulary rows (32 per wave) against every
-// token tile at once, so its weight rows are streamed once however many
-// tokens there are (the generic kernel re-reads them once per token tile).
-// Per K step the waves copy their own 4 KB weight tile and, 1 KB each, the
-// step's token tiles into an LDS ring of 4 steps (direct global -> LDS
-// copies, 3 steps ahead; a wave issues 4 + NTT copies per step), then read
-// their fragments from LDS.
+// LM head with the argmax epilogue: a workgroup of 4 waves owns 128
+// vocabulary rows (32 per wave) against a group of up to 5 token tiles at
+// once, so its weight rows are streamed once per group (the generic kernel
+// re-reads them once per token tile).  With more than 5 token tiles the
+// groups of one weight slice are consecutive workgroups of one XCD, so the
+// later groups find the slice in that XCD's L2.  Per K step the waves copy
+// their own 4 KB weight tile and, 1 KB each, the group's token tiles into an
+// LDS ring of 4 steps (direct global -> LDS copies, 3 steps ahead; a wave
+// issues 4 + NTT copies per step: a group's padding tiles re-read the last
+// token tile, so the count is fixed), then read their fragments from LDS.
 template <int NTT>
-__global__ __launch_bounds__(256) void lm_argmax_kernel(GemmArgs g) {
+__global__ __launch_bounds__(256) void lm_argmax_kernel(GemmArgs g, int groups) {
   constexpr int SB = 4, kA = 4 * 4096, kB = NTT * 4096, kStage = kA + kB;
   static_assert(SB * kStage <= 160 * 1024, "LDS");
   __shared__ __attribute__((aligned(16))) unsigned char lds[SB * kStage];
   const int per_xcd = gridDim.x / 8;
-  const int slice = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (slice >= g.n_slices) return;
+  const int item = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (item >= g.n_slices * groups) return;
+  const int slice = item / groups, tt0 = (item % groups) * NTT;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int frow = lane & 31, half = lane >> 5;
   const int tile = slice * 4 + wave, ksteps = g.K / kGemmKStep;
@@ -505,7 +506,8 @@ __global__ __launch_bounds__(256) void lm_argmax_kernel(GemmArgs g) {
     for (int j = 0; j < 4; ++j) dma16(asrc + (int64_t)step * 2048 + 512 * j, st + wave * 4096 + 1024 * j);
 #pragma unroll
     for (int i = 0; i < NTT; ++i) {
-      const int q = wave + 4 * i, tt = q >> 2, j = q & 3;   // token tile tt, piece j
+      const int q = wave + 4 * i, j = q & 3;                    // group tile q / 4, piece j
+      const int tt = min(tt0 + (q >> 2), g.n_ttiles - 1);       // token tile (padding: the last one)
       dma16(g.x + ((int64_t)tt * ksteps + step) * 2048 + 512 * j + lane * 8, st + kA + 1024 * q);
     }
   };
@@ -541,7 +543,8 @@ __global__ __launch_bounds__(256) void lm_argmax_kernel(GemmArgs g) {
   }
   EpilogueIn none;
 #pragma unroll
-  for (int tt = 0; tt < NTT; ++tt) epilogue<kEpiArgmax>(g, acc[tt], none, tt * kGemmTile + frow, tile, half);
+  for (int tt = 0; tt < NTT; ++tt)
+    if (tt0 + tt < g.n_ttiles) epilogue<kEpiArgmax>(g, acc[tt], none, (tt0 + tt) * kGemmTile + frow, tile, half);
 }
 
 // Packs W[rows][cols] (bf16) into the packed layout: one thread per 16-byte
@@ -642,16 +645,17 @@ hipError_t launch_pack_weight(const __bf16 *w, const __bf16 *w2, int rows, int c
 
 hipError_t launch_lm_argmax(const GemmArgs &g, int kind, hipStream_t stream) {
   const int ntt = g.Tpad / kGemmTile;
-  if (ntt < 1 || ntt > 5 || g.Tpad % kGemmTile || g.N % (4 * kGemmTile) || g.K % kGemmKStep || !g.amax ||
-      !g.a_packed || !g.act_packed || g.n_slices != g.N / (4 * kGemmTile))
+  if (ntt < 1 || g.n_ttiles != ntt || g.Tpad % kGemmTile || g.N % (4 * kGemmTile) || g.K % kGemmKStep ||
+      !g.amax || !g.a_packed || !g.act_packed || g.n_slices != g.N / (4 * kGemmTile))
     return hipErrorInvalidValue;
-  const dim3 grid((g.n_slices + 7) / 8 * 8), block(256);
-  switch (ntt) {
-    case 1: launch(kind, lm_argmax_kernel<1>, grid, block, stream, g); break;
-    case 2: launch(kind, lm_argmax_kernel<2>, grid, block, stream, g); break;
-    case 3: launch(kind, lm_argmax_kernel<3>, grid, block, stream, g); break;
-    case 4: launch(kind, lm_argmax_kernel<4>, grid, block, stream, g); break;
-    default: launch(kind, lm_argmax_kernel<5>, grid, block, stream, g); break;
+  const int groups = (ntt + 4) / 5, per = (ntt + groups - 1) / groups;   // per <= 5 token tiles per group
+  const dim3 grid(((int64_t)g.n_slices * groups + 7) / 8 * 8), block(256);
+  switch (per) {
+    case 1: launch(kind, lm_argmax_kernel<1>, grid, block, stream, g, groups); break;
+    case 2: launch(kind, lm_argmax_kernel<2>, grid, block, stream, g, groups); break;
+    case 3: launch(kind, lm_argmax_kernel<3>, grid, block, stream, g, groups); break;
+    case 4: launch(kind, lm_argmax_kernel<4>, grid, block, stream, g, groups); break;
+    default: launch(kind, lm_argmax_kernel<5>, grid, block, stream, g, groups); break;
   }
   return hipGetLastError();
 }
@@ -662,16 +666,14 @@ hipError_t launch_gemm(const GemmArgs &g, bool f16, int epi, int kind, hipStream
       g.n_ttiles * kGemmTile != g.Tpad || g.T < 1 || g.T > g.Tpad || g.N != g.n_slices * kGemmTile * g.rg ||
       (epi == kEpiSwiGLU && (g.N != 2 * g.I || !f16)) || (epi == kEpiQKV && f16))
     return hipErrorInvalidValue;
-  if (epi != kEpiArgmax &&
+  if (epi == kEpiArgmax ||   // the LM head has its own kernel (launch_lm_argmax)
       (epi == kEpiResidual ? (!g.h || (g.x_out && !g.ss_out)) : (!g.ss_in || g.n_ss < 4 || g.n_ss % 4 != 0)))
     return hipErrorInvalidValue;
   const int nwg = g.n_slices * g.n_ttiles;
   const dim3 grid((nwg + 7) / 8 * 8);
-  if (epi == kEpiArgmax && (!g.amax || f16 || !g.a_packed)) return hipErrorInvalidValue;
   if (g.a_packed) {
     if (!g.act_packed) return hipErrorInvalidValue;
-    if (epi == kEpiArgmax) launch_packed<false, kEpiArgmax>(g, kind, grid, stream);
-    else if (epi == kEpiSwiGLU) launch_packed<true, kEpiSwiGLU>(g, kind, grid, stream);
+    if (epi == kEpiSwiGLU) launch_packed<true, kEpiSwiGLU>(g, kind, grid, stream);
     else if (epi == kEpiQKV) launch_packed<false, kEpiQKV>(g, kind, grid, stream);
     else if (f16) launch_packed<true, kEpiResidual>(g, kind, grid, stream);
     else launch_packed<false, kEpiResidual>(g, kind, grid, stream);

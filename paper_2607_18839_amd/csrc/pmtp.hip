@@ -316,20 +316,15 @@ hpd_status hpd_verify_draft_step(const hpd_model_desc *model, const hpd_pmtp_des
     g.w0 = (const __bf16 *)pmtp->lm_head;
     g.K = L.H;
     g.N = L.V;
-    g.rg = hpd::choose_gemm_rg(L.V, L.H, Tpad);
-    g.n_slices = L.V / (hpd::kGemmTile * g.rg);
+    g.rg = 4;
+    g.n_slices = L.V / (4 * hpd::kGemmTile);
     g.n_ttiles = Tpad / hpd::kGemmTile;
     g.x = x;
     g.T = T;
     g.Tpad = Tpad;
     g.amax = amax;
     g.a_packed = g.act_packed = true;
-    if (Tpad <= 5 * hpd::kGemmTile) {   // every token tile per workgroup
-      g.rg = 4;
-      g.n_slices = L.V / (4 * hpd::kGemmTile);
-      return hpd::launch_lm_argmax(g, hpd::KK_LM_HEAD, stream);
-    }
-    return hpd::launch_gemm(g, false, hpd::kEpiArgmax, hpd::KK_LM_HEAD, stream);
+    return hpd::launch_lm_argmax(g, hpd::KK_LM_HEAD, stream);
   };
 
   // verification: x = bf16(h * g_final) (the norm factor does not move the argmax)

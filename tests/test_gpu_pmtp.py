@@ -119,6 +119,21 @@ def test_verify_draft_window_longer_than_the_step():
     assert _check(inp, pm, 2, window=7) > 0.9
 
 
+def test_verify_draft_many_tokens():
+    """T = 1 + 48 * 4 = 193 tokens (7 token tiles): the LM head runs two
+    token-tile groups per weight slice, the second with a padding tile."""
+    announce("pmtp 193 tokens")
+    from workloads import get_config, make_decode_inputs
+    cfg = get_config("c4", num_q_heads=4, num_kv_heads=2, num_pages=1, prefix=("fixed", 200),
+                     layout=dict(k=1, past=("fixed", 30)), content_count=("fixed", 48), content_k=4,
+                     content_past=("lognormal", 20.0, 1.0, 0, 80),
+                     model=dict(num_layers=1, hidden=256, intermediate=384, weight_std=0.05, rms_eps=1e-6))
+    inp = make_decode_inputs(cfg, 3)
+    assert int(inp.num_new.sum()) == 193
+    pm = make_pmtp_inputs(inp.hidden, 2048, 128, 0.05, 3)
+    assert _check(inp, pm, 3) > 0.9
+
+
 def test_verify_draft_c4_full_vocab():
     """c4 (18 layers, 33 branches) with the full 151,936-token vocabulary."""
     announce("pmtp c4 full vocab")
