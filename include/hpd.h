@@ -338,7 +338,7 @@ size_t hpd_pmtp_workspace_bytes(const hpd_model_desc *model, const hpd_pmtp_desc
  * workspace   >= hpd_plan_workspace_bytes + hpd_pmtp_workspace_bytes,
  *             256-byte aligned, uploaded with hpd_plan_upload (it may be the
  *             decode step's workspace if it is large enough for both).
- * The plan must be HPD_BF16. */
+ * The plan must be HPD_BF16 and the model's hidden a multiple of 256. */
 hpd_status hpd_verify_draft_step(const hpd_model_desc *model, const hpd_pmtp_desc *pmtp, const hpd_plan *plan,
                                  const float *hidden, const int32_t *tokens_in, int32_t *verified,
                                  int32_t *n_acc, int32_t *draft_out, void *workspace, size_t workspace_bytes,

@@ -79,7 +79,8 @@ hipError_t launch_pack_weight(const __bf16 *w, const __bf16 *w2, int rows, int c
 // activations); epi: kEpiQKV, kEpiResidual or kEpiSwiGLU.
 hipError_t launch_gemm(const GemmArgs &g, bool f16, int epi, int kind, hipStream_t stream);
 // LM head with the argmax epilogue (bf16, packed operands): 128 rows per
-// workgroup against a group of up to 5 token tiles; n_slices = N / 128.
+// workgroup against a group of up to 5 token tiles; n_slices = N / 128,
+// K a multiple of 256.
 hipError_t launch_lm_argmax(const GemmArgs &g, int kind, hipStream_t stream);
 
 // Row groups per workgroup for an N x K projection over Tpad tokens, from a

@@ -482,15 +482,16 @@ __global__ __launch_bounds__(256) void gemm_packed_kernel(GemmArgs g) {
 // once, so its weight rows are streamed once per group (the generic kernel
 // re-reads them once per token tile).  With more than 5 token tiles the
 // groups of one weight slice are consecutive workgroups of one XCD, so the
-// later groups find the slice in that XCD's L2.  Per K step the waves copy
-// their own 4 KB weight tile and, 1 KB each, the group's token tiles into an
-// LDS ring of 4 steps (direct global -> LDS copies, 3 steps ahead; a wave
-// issues 4 + NTT copies per step: a group's padding tiles re-read the last
-// token tile, so the count is fixed), then read their fragments from LDS.
+// later groups find the slice in that XCD's L2.  A wave's own weight tile
+// (4 KB per K step, the packed layout: 4 whole 1 KB loads) goes straight into
+// a register ring of 4 steps; the group's token tiles, which all 4 waves
+// multiply, go through an LDS ring of 4 steps (direct global -> LDS copies,
+// 1 KB per wave and tile).  Both are issued 3 steps ahead; a wave issues 4 +
+// NTT loads per step (a group's padding tiles re-read the last token tile,
+// so the count is fixed).  Requires K a multiple of 256 (4 steps of 64).
 template <int NTT>
 __global__ __launch_bounds__(256) void lm_argmax_kernel(GemmArgs g, int groups) {
-  constexpr int SB = 4, kA = 4 * 4096, kB = NTT * 4096, kStage = kA + kB;
-  static_assert(SB * kStage <= 160 * 1024, "LDS");
+  constexpr int SB = 4, kStage = NTT * 4096;
   __shared__ __attribute__((aligned(16))) unsigned char lds[SB * kStage];
   const int per_xcd = gridDim.x / 8;
   const int item = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
@@ -500,15 +501,16 @@ __global__ __launch_bounds__(256) void lm_argmax_kernel(GemmArgs g, int groups) 
   const int frow = lane & 31, half = lane >> 5;
   const int tile = slice * 4 + wave, ksteps = g.K / kGemmKStep;
   const __bf16 *asrc = g.w0 + (int64_t)tile * ksteps * 2048 + lane * 8;
-  auto issue = [&](int step) {
-    unsigned char *st = lds + (step % SB) * kStage;
+  u32x4 a[4][4];   // weight fragments of step s in a[s % 4]
+  auto issue = [&](int step, u32x4 (&slot)[4]) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) dma16(asrc + (int64_t)step * 2048 + 512 * j, st + wave * 4096 + 1024 * j);
+    for (int j = 0; j < 4; ++j) slot[j] = *(const u32x4 *)(asrc + (int64_t)step * 2048 + 512 * j);
+    unsigned char *st = lds + (step % SB) * kStage;
 #pragma unroll
     for (int i = 0; i < NTT; ++i) {
       const int q = wave + 4 * i, j = q & 3;                    // group tile q / 4, piece j
       const int tt = min(tt0 + (q >> 2), g.n_ttiles - 1);       // token tile (padding: the last one)
-      dma16(g.x + ((int64_t)tt * ksteps + step) * 2048 + 512 * j + lane * 8, st + kA + 1024 * q);
+      dma16(g.x + ((int64_t)tt * ksteps + step) * 2048 + 512 * j + lane * 8, st + 1024 * q);
     }
   };
   f32x16 acc[NTT];
@@ -516,30 +518,35 @@ __global__ __launch_bounds__(256) void lm_argmax_kernel(GemmArgs g, int groups) 
   for (int tt = 0; tt < NTT; ++tt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[tt][r] = 0.f;
-  for (int s = 0; s < SB - 1 && s < ksteps; ++s) issue(s);
-  for (int c = 0; c < ksteps; ++c) {
-    // step c landed (this wave's copies; the steps after it may stay in
-    // flight), and visible to every wave; the slot of step c - 1 is free
-    const int pending = min(SB - 2, ksteps - 1 - c);
+  auto step = [&](int c, u32x4 (&cur)[4], u32x4 (&next)[4]) {
+    // step c landed (this wave's loads; the steps after it may stay in
+    // flight), the token tiles visible to every wave; the slot of c - 1 is free
+    const int pending = min(2, ksteps - 1 - c);
     if (pending >= 2) wait_vm<2 * (4 + NTT)>();
     else if (pending == 1) wait_vm<4 + NTT>();
     else wait_vm<0>();
     ring_barrier();
-    if (c + SB - 1 < ksteps) issue(c + SB - 1);
+    if (c + 3 < ksteps) issue(c + 3, next);
     const unsigned char *st = lds + (c % SB) * kStage;
-    u32x4 a[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) a[j] = *(const u32x4 *)(st + wave * 4096 + 1024 * j + 16 * lane);
 #pragma unroll
     for (int tt = 0; tt < NTT; ++tt) {
       u32x4 b[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = *(const u32x4 *)(st + kA + 1024 * (4 * tt + j) + 16 * lane);
+      for (int j = 0; j < 4; ++j) b[j] = *(const u32x4 *)(st + 1024 * (4 * tt + j) + 16 * lane);
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        acc[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[j]),
+        acc[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, cur[j]),
                                                           __builtin_bit_cast(bf16x8, b[j]), acc[tt], 0, 0, 0);
     }
+  };
+  issue(0, a[0]);
+  issue(1, a[1]);
+  issue(2, a[2]);
+  for (int c = 0; c < ksteps; c += 4) {   // the ring slot of each step is a compile-time index
+    step(c, a[0], a[3]);
+    step(c + 1, a[1], a[0]);
+    step(c + 2, a[2], a[1]);
+    step(c + 3, a[3], a[2]);
   }
   EpilogueIn none;
 #pragma unroll
@@ -645,7 +652,7 @@ hipError_t launch_pack_weight(const __bf16 *w, const __bf16 *w2, int rows, int c
 
 hipError_t launch_lm_argmax(const GemmArgs &g, int kind, hipStream_t stream) {
   const int ntt = g.Tpad / kGemmTile;
-  if (ntt < 1 || g.n_ttiles != ntt || g.Tpad % kGemmTile || g.N % (4 * kGemmTile) || g.K % kGemmKStep ||
+  if (ntt < 1 || g.n_ttiles != ntt || g.Tpad % kGemmTile || g.N % (4 * kGemmTile) || g.K % (4 * kGemmKStep) ||
       !g.amax || !g.a_packed || !g.act_packed || g.n_slices != g.N / (4 * kGemmTile))
     return hipErrorInvalidValue;
   const int groups = (ntt + 4) / 5, per = (ntt + groups - 1) / groups;   // per <= 5 token tiles per group

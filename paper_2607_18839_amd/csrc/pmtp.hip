@@ -229,7 +229,7 @@ __global__ __launch_bounds__(256) void draft_token_kernel(int it, int ntile, con
 hpd_status validate(const hpd_model_desc *m, const hpd_pmtp_desc *d, const hpd_plan *plan, std::string *err) {
   if (!m || !d || !plan) { *err = "NULL model, pmtp or plan"; return HPD_ERR_INVALID_ARGUMENT; }
   if (plan->p.attn.dtype != HPD_BF16) { *err = "the plan must be HPD_BF16"; return HPD_ERR_UNSUPPORTED; }
-  if (m->hidden < 128 || m->hidden % 128) { *err = "hidden must be a positive multiple of 128"; return HPD_ERR_UNSUPPORTED; }
+  if (m->hidden < 256 || m->hidden % 256) { *err = "hidden must be a positive multiple of 256"; return HPD_ERR_UNSUPPORTED; }
   if (d->vocab < 128 || d->vocab % 128 || d->draft_inner < 128 || d->draft_inner % 128) {
     *err = "vocab and draft_inner must be positive multiples of 128";
     return HPD_ERR_UNSUPPORTED;
