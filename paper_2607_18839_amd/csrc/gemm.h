@@ -11,7 +11,7 @@ namespace hpd {
 
 constexpr int kGemmTile = 32;             // weight rows and tokens of one wave's output tile
 constexpr int kGemmKStep = 64;            // K per pipeline step (4 MFMAs of 16)
-constexpr int kEpiQKV = 0, kEpiResidual = 1, kEpiSwiGLU = 2, kEpiArgmax = 3;
+constexpr int kEpiQKV = 0, kEpiResidual = 1, kEpiSwiGLU = 2;
 
 // One projection Y[t][n] = sum_k X[t][k] W[n][k] over the full K range.  A
 // workgroup of 4 waves owns the output tile of 32 rg weight rows x 32
@@ -47,8 +47,8 @@ struct GemmArgs {
   __bf16 *x_out; bool x_out_f16;            // [Tpad][N]; rows < T written
   const __bf16 *gamma;                      // [N] bf16, NULL = ones
   float *ss_out;                            // [Tpad][N / 32]
-  // argmax epilogue (LM head): per token and 32-row tile the largest logit
-  // as an ordered key (argmax_key), amax[t][N / 32]
+  // LM head (launch_lm_argmax): per token and 128-row slice the largest
+  // logit as an ordered key (argmax_key), amax[t][N / 128]
   uint64_t *amax;
   // layouts: a_packed: w0 is packed (packed_offset; SwiGLU: the interleaved
   // gate/up pair, w1 unused); act_packed: x, x_out and m_out are packed.
@@ -78,9 +78,9 @@ hipError_t launch_pack_weight(const __bf16 *w, const __bf16 *w2, int rows, int c
 // f16: fp16 GEMM (bf16 weights converted to fp16 in registers, fp16
 // activations); epi: kEpiQKV, kEpiResidual or kEpiSwiGLU.
 hipError_t launch_gemm(const GemmArgs &g, bool f16, int epi, int kind, hipStream_t stream);
-// LM head with the argmax epilogue (bf16, packed operands): 128 rows per
+// LM head with an argmax epilogue (bf16, packed operands): 128 rows per
 // workgroup against a group of up to 5 token tiles; n_slices = N / 128,
-// K a multiple of 256.
+// K a multiple of 256; writes amax[Tpad][n_slices].
 hipError_t launch_lm_argmax(const GemmArgs &g, int kind, hipStream_t stream);
 
 // Row groups per workgroup for an N x K projection over Tpad tokens, from a

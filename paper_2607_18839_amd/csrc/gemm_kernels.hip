@@ -109,21 +109,7 @@ __device__ __forceinline__ void load_late(const GemmArgs &g, int t, int tile, in
 template <int EPI>
 __device__ __forceinline__ void epilogue(const GemmArgs &g, const f32x16 &acc, EpilogueIn &in, int t, int tile,
                                          int half) {
-  if constexpr (EPI == kEpiArgmax) {
-    // the tile's largest logit for token t (rows 8 (r / 4) + 4 half + r % 4
-    // of this lane, the other 16 in lane ^ 32), ties to the smaller row
-    uint64_t best = 0;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const uint64_t k = argmax_key(acc[r], tile * kGemmTile + 8 * (r >> 2) + 4 * half + (r & 3));
-      best = k > best ? k : best;
-    }
-    const uint64_t other = ((uint64_t)(uint32_t)__shfl_xor((int)(best >> 32), 32) << 32) |
-                           (uint32_t)__shfl_xor((int)(uint32_t)best, 32);
-    best = other > best ? other : best;
-    if (half == 0) g.amax[(int64_t)t * (g.N / kGemmTile) + tile] = best;
-    return;
-  } else if constexpr (EPI == kEpiResidual) {
+  if constexpr (EPI == kEpiResidual) {
     // h += Y; x_out = h * gamma (the next norm's input, unnormalised) and the
     // sum of squares of h over this 32-column tile
     if (t >= g.T) return;
@@ -477,7 +463,7 @@ __global__ __launch_bounds__(256) void gemm_packed_kernel(GemmArgs g) {
   epilogue<EPI>(g, acc, ein, t, tile, half);
 }
 
-// LM head with the argmax epilogue: a workgroup of 4 waves owns 128
+// LM head with an argmax epilogue: a workgroup of 4 waves owns 128
 // vocabulary rows (32 per wave) against a group of up to 5 token tiles at
 // once, so its weight rows are streamed once per group (the generic kernel
 // re-reads them once per token tile).  With more than 5 token tiles the
@@ -548,10 +534,34 @@ __global__ __launch_bounds__(256) void lm_argmax_kernel(GemmArgs g, int groups) 
     step(c + 2, a[2], a[1]);
     step(c + 3, a[3], a[2]);
   }
-  EpilogueIn none;
+  // argmax epilogue: per token, the largest logit of the slice's 128 rows as
+  // an ordered key (ties to the smaller row).  A lane holds rows
+  // 8 (r / 4) + 4 half + r % 4 of its wave's tile for token frow; lanes l and
+  // l ^ 32 combine, then the 4 waves through LDS (the ring is free once every
+  // wave is past its last step).
+  __syncthreads();
+  uint64_t *red = (uint64_t *)lds;   // [NTT][4 waves][32 tokens]
 #pragma unroll
-  for (int tt = 0; tt < NTT; ++tt)
-    if (tt0 + tt < g.n_ttiles) epilogue<kEpiArgmax>(g, acc[tt], none, (tt0 + tt) * kGemmTile + frow, tile, half);
+  for (int tt = 0; tt < NTT; ++tt) {
+    uint64_t best = 0;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const uint64_t k = argmax_key(acc[tt][r], tile * kGemmTile + 8 * (r >> 2) + 4 * half + (r & 3));
+      best = k > best ? k : best;
+    }
+    const uint64_t other = ((uint64_t)(uint32_t)__shfl_xor((int)(best >> 32), 32) << 32) |
+                           (uint32_t)__shfl_xor((int)(uint32_t)best, 32);
+    best = other > best ? other : best;
+    if (half == 0) red[(tt * 4 + wave) * 32 + frow] = best;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < NTT * 32; i += 256) {
+    const int tt = i >> 5, tok = i & 31;
+    if (tt0 + tt >= g.n_ttiles) continue;
+    const uint64_t *v = red + tt * 128 + tok;
+    const uint64_t m01 = v[0] > v[32] ? v[0] : v[32], m23 = v[64] > v[96] ? v[64] : v[96];
+    g.amax[(int64_t)((tt0 + tt) * kGemmTile + tok) * g.n_slices + slice] = m01 > m23 ? m01 : m23;
+  }
 }
 
 // Packs W[rows][cols] (bf16) into the packed layout: one thread per 16-byte
@@ -673,7 +683,7 @@ hipError_t launch_gemm(const GemmArgs &g, bool f16, int epi, int kind, hipStream
       g.n_ttiles * kGemmTile != g.Tpad || g.T < 1 || g.T > g.Tpad || g.N != g.n_slices * kGemmTile * g.rg ||
       (epi == kEpiSwiGLU && (g.N != 2 * g.I || !f16)) || (epi == kEpiQKV && f16))
     return hipErrorInvalidValue;
-  if (epi == kEpiArgmax ||   // the LM head has its own kernel (launch_lm_argmax)
+  if (epi < kEpiQKV || epi > kEpiSwiGLU ||
       (epi == kEpiResidual ? (!g.h || (g.x_out && !g.ss_out)) : (!g.ss_in || g.n_ss < 4 || g.n_ss % 4 != 0)))
     return hipErrorInvalidValue;
   const int nwg = g.n_slices * g.n_ttiles;

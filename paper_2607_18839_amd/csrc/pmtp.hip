@@ -3,9 +3,9 @@
 // speculative decoding and verification).
 //
 // Per call: the final-norm input of the T decoder outputs, the LM head with an
-// argmax epilogue (per token and 32-row tile the largest logit as an ordered
-// key), then one workgroup per branch reduces the keys to y* at each of its
-// positions, verifies its drafts, writes n_acc and the bonus token and seeds
+// argmax epilogue (per token and 128-row slice the largest logit as an
+// ordered key), then one workgroup per branch reduces the keys to y* at each
+// of its positions (one wave per position), verifies its drafts, writes n_acc and the bonus token and seeds
 // the draft state f = h at the last verified position.  Each draft iteration:
 // the draft input [f ; embed(token)] with its sums of squares, the draft
 // MLP's gate/up (SwiGLU epilogue, RMSNorm folded) and down projection
@@ -47,7 +47,7 @@ PmtpLayout pmtp_layout(const hpd_model_desc &m, const hpd_pmtp_desc &d, const Pl
   L.V = d.vocab;
   L.Id = d.draft_inner;
   L.kmax = d.window > 0 ? d.window : *std::max_element(P.num_new.begin(), P.num_new.end());
-  L.ntile = d.vocab / kGemmTile;
+  L.ntile = d.vocab / (4 * kGemmTile);   // argmax keys per token: one per 128-row slice
   size_t off = align256(P.workspace_bytes);
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -69,18 +69,17 @@ PmtpLayout pmtp_layout(const hpd_model_desc &m, const hpd_pmtp_desc &d, const Pl
   return L;
 }
 
-// Largest key of keys[0..n) over the workgroup's share of this wave (a
-// workgroup of 256 threads strides over the keys): each thread's loads are
-// issued 8 at a time into independent registers (one round trip per 8, not
-// per load), then the wave's lanes are reduced.
-__device__ uint64_t wave_max_key(const uint64_t *keys, int n) {
-  constexpr int U = 8;
+// Largest of keys[0..n), reduced over the 64 lanes of the calling wave:
+// thread t of the STRIDE threads that share the work issues its loads U at a
+// time into independent registers (one round trip per U loads, not per load).
+template <int STRIDE, int U>
+__device__ uint64_t wave_max_key(const uint64_t *keys, int n, int t) {
   uint64_t best = 0;
-  for (int i0 = threadIdx.x; i0 < n; i0 += 256 * U) {
+  for (int i0 = t; i0 < n; i0 += STRIDE * U) {
     uint64_t v[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int i = i0 + 256 * u;
+      const int i = i0 + STRIDE * u;
       v[u] = i < n ? keys[i] : 0;
     }
 #pragma unroll
@@ -98,7 +97,7 @@ __device__ uint64_t wave_max_key(const uint64_t *keys, int n) {
 // Largest key of keys[0..n) over the workgroup (256 threads); every thread
 // gets the result.
 __device__ uint64_t wg_max_key(const uint64_t *keys, int n, uint64_t *sh) {
-  const uint64_t best = wave_max_key(keys, n);
+  const uint64_t best = wave_max_key<256, 8>(keys, n, threadIdx.x);
   __syncthreads();   // sh is free (previous readers are done)
   if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = best;
   __syncthreads();
@@ -111,7 +110,6 @@ __global__ __launch_bounds__(256) void verify_kernel(PlanDev dev, int nb, int nt
                                                      const int32_t *tokens_in, const float *hidden, int H,
                                                      int32_t *verified, int32_t *n_acc, int32_t *draft_out,
                                                      float *f, int32_t *cur_tok) {
-  __shared__ uint64_t sh[4];
   __shared__ int ystar[HPD_MAX_K];
   __shared__ int acc_n;
   const int b = blockIdx.x;
@@ -122,19 +120,14 @@ __global__ __launch_bounds__(256) void verify_kernel(PlanDev dev, int nb, int nt
     return;
   }
   const int q0 = dev.branch_q_row[b], k = dev.branch_new[b];
-  // per-wave maxima of every position first (no barrier between positions),
-  // then one barrier and the workgroup maximum per position
-  __shared__ uint64_t wmax[HPD_MAX_K][4];
-  for (int j = 0; j < k; ++j) {
-    const uint64_t w = wave_max_key(amax + (int64_t)(q0 + j) * ntile, ntile);
-    if ((threadIdx.x & 63) == 0) wmax[j][threadIdx.x >> 6] = w;
-  }
-  __syncthreads();
-  if (threadIdx.x < k) {
-    const int j = threadIdx.x;
-    const uint64_t key = max(max(wmax[j][0], wmax[j][1]), max(wmax[j][2], wmax[j][3]));
-    ystar[j] = argmax_id(key);
-    verified[q0 + j] = ystar[j];
+  // one wave per position (all of a position's keys loaded at once)
+  const int lane = threadIdx.x & 63;
+  for (int j = threadIdx.x >> 6; j < k; j += 4) {
+    const uint64_t key = wave_max_key<64, 24>(amax + (int64_t)(q0 + j) * ntile, ntile, lane);
+    if (lane == 0) {
+      ystar[j] = argmax_id(key);
+      verified[q0 + j] = ystar[j];
+    }
   }
   __syncthreads();
   if (threadIdx.x == 0) {
