@@ -342,9 +342,21 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 // weights packed once by hpd_pack_weight / hpd_pack_gate_up, activations
 // written packed by their producers).  A wave's fragments for one step are
 // then 4 whole contiguous 1 KB pieces per operand, loaded straight into a
-// register ring of kPackedRing steps (3 ahead of the MFMAs); no LDS is used
-// until the K groups are added.
+// register ring of kPackedRing steps (kPackedRing - 1 ahead of the MFMAs);
+// no LDS is used until the K groups are added.  Measured on the c4 step:
+// rings of 6 and 8 steps are slower than 4 (gate/up 9.0 -> 15.7 us at 6,
+// down 8.3 -> 16.6 us at 8): past 256 VGPRs the ring spills into
+// accumulator registers and a SIMD holds one wave instead of two.
 constexpr int kPackedRing = 4;
+
+// f(integral_constant<int, rem>) for the runtime value rem in 1..N.
+template <int N, typename F>
+__device__ __forceinline__ void with_rem(int rem, F &&f) {
+  if constexpr (N >= 1) {
+    if (rem == N) f(std::integral_constant<int, N>{});
+    else with_rem<N - 1>(rem, f);
+  }
+}
 
 template <int RG, bool F16, int EPI>
 __global__ __launch_bounds__(256) void gemm_packed_kernel(GemmArgs g) {
@@ -406,13 +418,6 @@ __global__ __launch_bounds__(256) void gemm_packed_kernel(GemmArgs g) {
       compute(u % S);
     }
   };
-  using I1 = std::integral_constant<int, 1>;
-  using I2 = std::integral_constant<int, 2>;
-  using I3 = std::integral_constant<int, 3>;
-  using I4 = std::integral_constant<int, 4>;
-  using I5 = std::integral_constant<int, 5>;
-  using I6 = std::integral_constant<int, 6>;
-  static_assert(S == 4, "the tail cases below cover REM = 1 .. 2 S - 2");
   // unconditional (a step index past the end repeats the last step, unused),
   // so that no load sits under a runtime condition
 #pragma unroll
@@ -427,21 +432,9 @@ __global__ __launch_bounds__(256) void gemm_packed_kernel(GemmArgs g) {
       }
     }
     const int base = n_main * S;
-    switch (nsteps - base) {   // S - 1 .. 2 S - 2
-      case 3: tail(base, I3{}); break;
-      case 4: tail(base, I4{}); break;
-      case 5: tail(base, I5{}); break;
-      default: tail(base, I6{}); break;
-    }
+    with_rem<2 * S - 2>(nsteps - base, [&](auto rem) { tail(base, rem); });   // S - 1 .. 2 S - 2
   } else {
-    switch (nsteps) {   // 1 .. 2 S - 2
-      case 1: tail(0, I1{}); break;
-      case 2: tail(0, I2{}); break;
-      case 3: tail(0, I3{}); break;
-      case 4: tail(0, I4{}); break;
-      case 5: tail(0, I5{}); break;
-      default: tail(0, I6{}); break;
-    }
+    with_rem<2 * S - 2>(nsteps, [&](auto rem) { tail(0, rem); });            // 1 .. 2 S - 2
   }
 
   // the epilogue's own loads overlap the K-group hand-over
