@@ -30,7 +30,9 @@ def pool_rows(batch, b, lo, hi):
 
 def synthetic_prefill(seed=0):
     """A prefill stand-in: writes seeded N(0, 1) bf16 K/V into the rows the
-    batch asks for (same values for the same request and row)."""
+    batch asks for (a new page's prompt rows, a resumed request's dropped
+    rows).  The values stand in for what a prefill would compute; they do
+    not reproduce the rows a request had before it was preempted."""
     def fill(engine, batch):
         for b in range(batch["num_branches"]):
             lo, hi = int(batch["prefill_from"][b]), int(batch["prefill_to"][b])

@@ -74,9 +74,17 @@ def _oracle_inputs(eng, inp, pm, batch):
     return ns, pr[new_mask]
 
 
-def test_engine_steps_match_the_oracle_with_planted_forks():
+def _engine(inp, pm, num_blocks, max_active):
     from paper_2607_18839_amd.engine import Engine
-    announce("engine: 2 pages, planted forks, oracle every step")
+    w = {k: [to_dev(a, "bf16") for a in getattr(inp, k)] for k in ("w_qkv", "w_o", "w_gate", "w_up", "w_down")}
+    pw = {k: to_dev(getattr(pm, k), "bf16") for k in ("lm_head", "embed", "w_draft_gate", "w_draft_up",
+                                                       "w_draft_down")}
+    return Engine(w, pw, inp.hidden, inp.intermediate, inp.num_q_heads, inp.num_kv_heads,
+                  dict(num_blocks=num_blocks, block_rows=64, kv_threshold=1.0, window=3, max_active=max_active,
+                       fork_token=FORK, child_token=CHILD, eos_token=EOS), rms_eps=inp.rms_eps)
+
+
+def _inputs():
     inp = small_inputs(0)
     pm = make_pmtp_inputs(inp.hidden, 1024, 128, 0.05, 0)
     # the embedding rows are the step's hidden input: give them the decode
@@ -84,17 +92,12 @@ def test_engine_steps_match_the_oracle_with_planted_forks():
     # (at 0.05 the bf16 roundings of the layer updates dominate the output)
     from workloads.gen import f64_to_bf16_bits
     pm.embed = f64_to_bf16_bits(np.random.default_rng([0, 21]).standard_normal(pm.embed.shape))
-    w = {k: [to_dev(a, "bf16") for a in getattr(inp, k)] for k in ("w_qkv", "w_o", "w_gate", "w_up", "w_down")}
-    pw = {k: to_dev(getattr(pm, k), "bf16") for k in ("lm_head", "embed", "w_draft_gate", "w_draft_up",
-                                                       "w_draft_down")}
-    eng = Engine(w, pw, inp.hidden, inp.intermediate, inp.num_q_heads, inp.num_kv_heads,
-                 dict(num_blocks=48, block_rows=64, kv_threshold=1.0, window=3, max_active=4, fork_token=FORK,
-                      child_token=CHILD, eos_token=EOS), rms_eps=inp.rms_eps)
-    eng.submit(150, 11, 14)
-    eng.submit(90, 12, 14)
+    return inp, pm
+
+
+def _checker(eng, inp, pm, seen, plant_at):
+    """The per-step hook: every check against the oracle, then the planted forks."""
     W_lm = (pm.lm_head.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
-    seen = dict(children=0, forks=0, prefill=0, worst=(0.0, 0.0))
-    plant_at = {1: 0, 3: 1, 4: 0}   # step -> page index whose parent forks at its bonus token
 
     def check(batch):
         T = batch["num_tokens"]
@@ -136,8 +139,25 @@ def test_engine_steps_match_the_oracle_with_planted_forks():
                     batch["draft_out"][b, 0] = FORK
                     seen["forks"] += 1
                 q += k
+        # a request admitted after a preemption resumes with its dropped rows to refill
+        out = seen.setdefault("out", set())
+        out.update(int(r) for r in batch["preempted"])
+        for b, r in enumerate(batch["request"]):
+            if int(r) in out and int(r) in set(int(a) for a in batch["admitted"]):
+                seen["resumed"] += 1
+                out.discard(int(r))
+        seen["preempted"] += len(batch["preempted"])
+    return check
 
-    eng.on_results = check
+
+def test_engine_steps_match_the_oracle_with_planted_forks():
+    announce("engine: 2 pages, planted forks, oracle every step")
+    inp, pm = _inputs()
+    eng = _engine(inp, pm, num_blocks=48, max_active=4)
+    eng.submit(150, 11, 14)
+    eng.submit(90, 12, 14)
+    seen = dict(children=0, forks=0, prefill=0, worst=(0.0, 0.0), preempted=0, resumed=0)
+    eng.on_results = _checker(eng, inp, pm, seen, {1: 0, 3: 1, 4: 0})   # step -> page whose parent forks
     pages = []
     for _ in range(40):
         b = eng.step()
@@ -149,3 +169,28 @@ def test_engine_steps_match_the_oracle_with_planted_forks():
     assert seen["forks"] >= 2 and seen["children"] >= 1 and seen["prefill"] >= 2
     assert sorted(p for p, _ in pages) == [0, 1]
     assert eng.sched.counts() == dict(waiting=0, active=0, free_blocks=48)
+
+
+def test_engine_preempts_and_resumes_in_a_tight_pool():
+    """8 blocks of 64 rows for three pages (prompts 100, 80 and 60 rows, up
+    to 60 tokens each, a fork planted on the first page): growing requests
+    preempt the youngest, whose dropped rows are refilled when it resumes;
+    every step still matches the oracle and every page is output."""
+    announce("engine: tight pool, preemption and resume, oracle every step")
+    inp, pm = _inputs()
+    eng = _engine(inp, pm, num_blocks=8, max_active=8)
+    for prompt, tok in ((100, 11), (80, 12), (60, 13)):
+        eng.submit(prompt, tok, 60)
+    seen = dict(children=0, forks=0, prefill=0, worst=(0.0, 0.0), preempted=0, resumed=0)
+    eng.on_results = _checker(eng, inp, pm, seen, {2: 0})
+    pages = []
+    for _ in range(400):
+        b = eng.step()
+        pages += eng.outputs()
+        if b["num_branches"] == 0 and len(pages) == 3:
+            break
+    print(f"engine (tight pool): {eng.steps} steps, preempted {seen['preempted']}, resumed {seen['resumed']}, "
+          f"worst max abs {seen['worst'][0]:.2e}")
+    assert seen["preempted"] >= 1 and seen["resumed"] >= 1 and seen["forks"] >= 1
+    assert sorted(p for p, _ in pages) == [0, 1, 2]
+    assert eng.sched.counts() == dict(waiting=0, active=0, free_blocks=8)
