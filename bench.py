@@ -88,7 +88,7 @@ def main():
         sys.exit(3)
     from paper_2607_18839_amd import _lib
     _lib.load()
-    if args.workload == "c4":
+    if args.workload in ("c4", "c4q"):
         res = bench_decode(args, torch, _lib)
     elif args.workload == "engine":
         res = bench_engine(args, torch, _lib)
@@ -355,11 +355,14 @@ def gemm_work(T, Hq, Hkv, D, H, I):
 def bench_decode(args, torch, _lib):
     from paper_2607_18839_amd.torch_api import DecodeStep
     from workloads import make_decode_inputs
-    inp = make_decode_inputs("c4", args.seed, num_layers=args.layers)
+    inp = make_decode_inputs(args.workload, args.seed, num_layers=args.layers)
 
     def dev(a):
         return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
     w = {k: [dev(a) for a in getattr(inp, k)] for k in ("w_qkv", "w_o", "w_gate", "w_up", "w_down")}
+    for k in ("q_norm", "k_norm"):   # c4q: Qwen3-style head gains
+        if getattr(inp, k, None) is not None:
+            w[k] = [dev(a) for a in getattr(inp, k)]
     sk = [dev(a) for a in inp.shared_k]
     sv = [dev(a) for a in inp.shared_v]
     pk = [dev(a) for a in inp.priv_k]
@@ -372,7 +375,7 @@ def bench_decode(args, torch, _lib):
         pk, pv = [_to_pool(torch, t, pr_rows, n_pool) for t in pk], [_to_pool(torch, t, pr_rows, n_pool) for t in pv]
     step_obj = DecodeStep(inp.num_q_heads, inp.num_kv_heads, inp.prefix_len, inp.branch_page, inp.num_new,
                           inp.past_len, w, inp.hidden, inp.intermediate, inp.rms_eps,
-                          packed=args.weights == "packed", paged=pg and pg[0])
+                          packed=args.weights == "packed", paged=pg and pg[0], rope_theta=inp.rope_theta)
     del w   # the packed copies are held by step_obj; the torch-layout tensors are not read again
     h_in = torch.from_numpy(inp.hidden_in).cuda()
     h_out = torch.empty_like(h_in)
@@ -434,8 +437,10 @@ def bench_decode(args, torch, _lib):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "timing": "HIP graph replay (one step per graph)",
         "data": "synthetic (seeded N(0,1) KV and hidden, N(0,0.02) bf16 weights)",
-        "config": {"workload": "c4: full decode step, 18-layer synthetic decoder, 1 page, "
-                               "1 layout (k=1) + 32 content (k=4) branches, 4096-token shared prefix",
+        "config": {"workload": f"{args.workload}: full decode step, 18-layer synthetic decoder, 1 page, "
+                               "1 layout (k=1) + 32 content (k=4) branches, 4096-token shared prefix"
+                               + (", Qwen3-style per-head QK norm and rotary embedding (base 1e6)"
+                                  if args.workload == "c4q" else ""),
                    "layers": inp.num_layers, "hidden": H, "intermediate": I, "heads": [Hq, Hkv, D],
                    "branch_tokens": T, "branches": int(len(inp.num_new)), "prefix_len": int(inp.prefix_len[0]),
                    "private_rows": int((inp.past_len + inp.num_new).sum()),

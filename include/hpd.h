@@ -201,6 +201,19 @@ typedef struct {
   const void *const *g_attn_norm; /* [L] -> [hidden] bf16 RMSNorm gain; NULL = ones */
   const void *const *g_mlp_norm;  /* [L] -> [hidden] bf16 RMSNorm gain; NULL = ones */
   int32_t weight_format;        /* hpd_weight_format; 0 = HPD_WEIGHTS_TORCH      */
+  /* Qwen3-style attention inputs (optional; NULL / 0 = off, the plain stack
+   * above).  The "Overview" section names Qwen3-0.6B as the decoder's base;
+   * its attention normalises each head's q and k and rotates them by
+   * position.  q_norm, k_norm: [L] -> [64] bf16 gains of an RMSNorm (epsilon
+   * rms_eps) over each head's 64 q (k) values after the projection.
+   * rope_theta > 0: rotary position embedding after the norm, dims i and
+   * i + 32 of a head rotated by the angle pos * rope_theta^(-i / 32)
+   * (x_i, x_{i+32}) -> (x_i cos - x_{i+32} sin, x_{i+32} cos + x_i sin), pos
+   * = F_b + L_b + j, the token's position in its branch's sequence.  The
+   * shared and past K rows are taken as already normalised and rotated. */
+  const void *const *q_norm;
+  const void *const *k_norm;
+  float rope_theta;
 } hpd_model_desc;
 
 /* Layout of the projection weights of an hpd_model_desc.
@@ -355,7 +368,7 @@ hpd_status hpd_verify_draft_step(const hpd_model_desc *model, const hpd_pmtp_des
  * eager launches: do not enable it while capturing a graph.  keep_pairs = 1
  * keeps the pairs assigned after the read (re-read after re-running the same
  * launches); keep_pairs = 0 releases them. */
-#define HPD_NUM_KERNEL_KINDS 13
+#define HPD_NUM_KERNEL_KINDS 14
 typedef struct {
   int64_t count[HPD_NUM_KERNEL_KINDS];
   double total_ms[HPD_NUM_KERNEL_KINDS];
@@ -366,7 +379,7 @@ hpd_status hpd_kernel_times_read(hpd_kernel_times *out, int keep_pairs);
 /* Kind k: 0 shared_prefix, 1 private, 2 merge, 3 gemm_qkv, 4 gemm_o,
  * 5 gemm_gate_up, 6 gemm_down, 7 norm_input, 8 lm_head, 9 verify,
  * 10 draft_mlp (the draft MLP's two projections and its input),
- * 11 draft_token, 12 embed.  With bf16 inputs kind 0 is
+ * 11 draft_token, 12 embed, 13 qk_norm_rope.  With bf16 inputs kind 0 is
  * one launch that runs the shared-prefix and the private work items (kind 1
  * is then never launched) unless phase isolation is on. */
 const char *hpd_kernel_kind_name(int kind);

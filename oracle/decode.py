@@ -17,6 +17,12 @@ draft over the active pool).  For each layer l, with residual stream h
   x = RMSNorm(h)
   h = h + (silu(x W_gate^T) * (x W_up^T)) W_down^T,  silu(u) = u / (1 + e^-u)
 
+Optionally (a Qwen3-style decoder, the base the "Overview" section names):
+right after the projection, q and k are RMS-normalised per head with their
+own gains, then rotated by position (rotary embedding): dims i and i + 32 of
+a head turn by the angle pos * theta^(-i / 32), pos = F_b + L_b + j the
+token's position in its branch's sequence.
+
 The step returns h after the last layer (no final norm, no LM head) and the
 bf16 bits of the K/V rows it wrote.  Everything else is fp64.
 """
@@ -54,6 +60,34 @@ def rms_norm(y, eps, gamma=None):
     return r if gamma is None else r * gamma
 
 
+def rope(x, pos, theta):
+    """Rotary position embedding of the last axis (2 * half values) at
+    positions pos (one per entry of the first axis): dims i and i + half turn
+    by the angle pos * theta^(-i / half)."""
+    half = x.shape[-1] // 2
+    ang = np.asarray(pos, np.float64)[:, None] * float(theta) ** (-np.arange(half) / half)[None, :]
+    shape = (ang.shape[0],) + (1,) * (x.ndim - 2) + (half,)
+    c, s = np.cos(ang).reshape(shape), np.sin(ang).reshape(shape)
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+def qwen3_qk(inp, l, q, k, visible):
+    """Qwen3-style attention inputs of layer l (identity when the inputs carry
+    no q_norm / k_norm / rope_theta): per-head RMSNorm of q and k with their
+    gains, then the rotary embedding at position visible - 1."""
+    qn, kn = getattr(inp, "q_norm", None), getattr(inp, "k_norm", None)
+    theta = float(getattr(inp, "rope_theta", 0.0) or 0.0)
+    if qn is not None:
+        q = rms_norm(q, inp.rms_eps, _bits_value(qn[l]))
+    if kn is not None:
+        k = rms_norm(k, inp.rms_eps, _bits_value(kn[l]))
+    if theta > 0:
+        pos = np.asarray(visible, np.float64) - 1
+        q, k = rope(q, pos, theta), rope(k, pos, theta)
+    return q, k
+
+
 def silu(u):
     return u / (1.0 + np.exp(-u))
 
@@ -88,7 +122,8 @@ def decode_step(inp, num_layers=None):
         x = rms_norm(h, inp.rms_eps)
         qkv = x @ Wqkv.T
         q = qkv[:, :Hq * D].reshape(T, Hq, D)
-        k_new = _bf16_value(qkv[:, Hq * D:(Hq + Hkv) * D].reshape(T, Hkv, D))
+        q, k_raw = qwen3_qk(inp, l, q, qkv[:, Hq * D:(Hq + Hkv) * D].reshape(T, Hkv, D), plan["visible"])
+        k_new = _bf16_value(k_raw)
         v_new = _bf16_value(qkv[:, (Hq + Hkv) * D:].reshape(T, Hkv, D))
         pk = _bits_value(inp.priv_k[l]).copy()
         pv = _bits_value(inp.priv_v[l]).copy()

@@ -74,7 +74,8 @@ class hpd_model_desc(ctypes.Structure):
     _fields_ = [("num_layers", ctypes.c_int32), ("hidden", ctypes.c_int32),
                 ("intermediate", ctypes.c_int32), ("rms_eps", ctypes.c_float),
                 ("w_qkv", PP), ("w_o", PP), ("w_gate", PP), ("w_up", PP), ("w_down", PP),
-                ("g_attn_norm", PP), ("g_mlp_norm", PP), ("weight_format", ctypes.c_int32)]
+                ("g_attn_norm", PP), ("g_mlp_norm", PP), ("weight_format", ctypes.c_int32),
+                ("q_norm", PP), ("k_norm", PP), ("rope_theta", ctypes.c_float)]
 
 
 HPD_WEIGHTS_TORCH, HPD_WEIGHTS_PACKED = 0, 1
@@ -276,11 +277,13 @@ def _ptr_array(ptrs):
 
 
 def model_desc(num_layers, hidden, intermediate, rms_eps, w_qkv, w_o, w_gate, w_up, w_down,
-               g_attn_norm=None, g_mlp_norm=None, weight_format=HPD_WEIGHTS_TORCH):
+               g_attn_norm=None, g_mlp_norm=None, weight_format=HPD_WEIGHTS_TORCH, q_norm=None, k_norm=None,
+               rope_theta=0.0):
     """hpd_model_desc from lists of device pointers; keeps the arrays alive."""
-    keep = [_ptr_array(x) for x in (w_qkv, w_o, w_gate, w_up, w_down, g_attn_norm, g_mlp_norm)]
+    keep = [_ptr_array(x) for x in (w_qkv, w_o, w_gate, w_up, w_down, g_attn_norm, g_mlp_norm, q_norm, k_norm)]
     cast = [None if k is None else ctypes.cast(k, PP) for k in keep]
-    d = hpd_model_desc(num_layers, hidden, intermediate, rms_eps, *cast, weight_format)
+    d = hpd_model_desc(num_layers, hidden, intermediate, rms_eps, *cast[:7], weight_format, *cast[7:],
+                       float(rope_theta))
     d._keep = keep
     return d
 
@@ -313,7 +316,7 @@ def hpd_decode_step(model, plan, hidden_in, hidden_out, shared_k, shared_v, priv
                                   stream), "hpd_decode_step")
 
 
-HPD_NUM_KERNEL_KINDS = 13
+HPD_NUM_KERNEL_KINDS = 14
 
 
 class hpd_kernel_times(ctypes.Structure):

@@ -1102,6 +1102,7 @@ PlanDev plan_dev(const Plan &P, void *workspace) {
   d.token_slots = (const int32_t *)(ws + P.off_token_slots);
   d.token_fork = (const int32_t *)(ws + P.off_token_fork);
   d.token_dest = (const int32_t *)(ws + P.off_token_dest);
+  d.token_vis = (const int32_t *)(ws + P.off_token_vis);
   d.counters = (int32_t *)(ws + P.off_counters);
   d.part_o = (float *)(ws + P.off_part_o);
   d.part_lse = (float *)(ws + P.off_part_lse);

@@ -9,7 +9,8 @@
 //   0 h = hidden_in; x = h * gamma_attn[0] (bf16), sums of squares
 // and per layer:
 //   1 QKV GEMM -> q (bf16) and the new K/V rows (bf16), written into the
-//     layer's private cache at row priv_row + L + j
+//     layer's private cache at row priv_row + L + j (optionally followed by
+//     the Qwen3-style QK norm and rotary embedding of q and the new k rows)
 //   2 branch attention (one launch for the shared-prefix and private work
 //     items, then the merge) -> a (bf16)
 //   3 O GEMM: h += a W_o^T; x = h * gamma_mlp (fp16), sums of squares
@@ -73,6 +74,55 @@ DecodeLayout decode_layout(const hpd_model_desc &m, const Plan &P) {
   return L;
 }
 
+// Qwen3-style q / k after the QKV projection (hpd_model_desc q_norm, k_norm,
+// rope_theta): per (token, head) an RMSNorm over the head's 64 values with
+// its gain, then the rotary position embedding at the token's position in
+// its branch's sequence (visible keys - 1).  q is rewritten in place, k in
+// the cache row the projection appended.  One wave per (token, head); lane i
+// (and i + 32, which computes the same values) owns dims i and i + 32.  The
+// angle and its sine and cosine are taken in fp64 (positions reach the
+// thousands), the rest in fp32; results are rounded to bf16 once.
+__global__ __launch_bounds__(256) void qk_norm_rope_kernel(PlanDev dev, __bf16 *q, __bf16 *k_cache, int T, int Hq,
+                                                           int Hkv, const __bf16 *gq, const __bf16 *gk, float eps,
+                                                           float theta) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, nh = Hq + Hkv;
+  const int64_t item = (int64_t)blockIdx.x * 4 + wave;   // (token, head)
+  if (item >= (int64_t)T * nh) return;
+  const int t = (int)(item / nh), hh = (int)(item % nh);
+  __bf16 *row;
+  const __bf16 *g;
+  if (hh < Hq) {
+    row = q + ((int64_t)t * Hq + hh) * HPD_HEAD_DIM;
+    g = gq;
+  } else {
+    row = k_cache + ((int64_t)dev.token_dest[t] * Hkv + (hh - Hq)) * HPD_HEAD_DIM;
+    g = gk;
+  }
+  const int i = lane & 31;
+  float x0 = (float)row[i], x1 = (float)row[i + 32];
+  if (g) {
+    float ss = fmaf(x0, x0, x1 * x1);
+#pragma unroll
+    for (int off = 16; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
+    const float r = 1.0f / sqrtf(ss * (1.0f / HPD_HEAD_DIM) + eps);
+    x0 = x0 * r * (float)g[i];
+    x1 = x1 * r * (float)g[i + 32];
+  }
+  if (theta > 0.f) {
+    const double ang = (double)(dev.token_vis[t] - 1) * pow((double)theta, -(double)i / 32.0);
+    double s, c;
+    sincos(ang, &s, &c);
+    const float cf = (float)c, sf = (float)s;
+    const float y0 = x0 * cf - x1 * sf, y1 = x1 * cf + x0 * sf;
+    x0 = y0;
+    x1 = y1;
+  }
+  if (lane < 32) {
+    row[i] = (__bf16)x0;
+    row[i + 32] = (__bf16)x1;
+  }
+}
+
 hpd_status validate(const hpd_model_desc *m, const hpd_plan *plan, std::string *err) {
   if (!m || !plan) { *err = "NULL model or plan"; return HPD_ERR_INVALID_ARGUMENT; }
   const Plan &P = plan->p;
@@ -96,8 +146,17 @@ hpd_status validate(const hpd_model_desc *m, const hpd_plan *plan, std::string *
     *err = "NULL weight array";
     return HPD_ERR_INVALID_ARGUMENT;
   }
+  if (!(m->rope_theta >= 0.f) || m->rope_theta > 3.0e38f) {
+    *err = "rope_theta must be finite and >= 0";
+    return HPD_ERR_INVALID_ARGUMENT;
+  }
   auto misaligned = [](const void *p) { return ((uintptr_t)p & 15) != 0; };
   for (int l = 0; l < m->num_layers; ++l) {
+    if ((m->q_norm && (!m->q_norm[l] || misaligned(m->q_norm[l]))) ||
+        (m->k_norm && (!m->k_norm[l] || misaligned(m->k_norm[l])))) {
+      *err = "NULL or misaligned q_norm / k_norm gain of layer " + std::to_string(l);
+      return HPD_ERR_INVALID_ARGUMENT;
+    }
     if (!m->w_qkv[l] || !m->w_o[l] || !m->w_gate[l] || (!packed && !m->w_up[l]) || !m->w_down[l]) {
       *err = "NULL weight of layer " + std::to_string(l);
       return HPD_ERR_INVALID_ARGUMENT;
@@ -188,6 +247,8 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
     return g;
   };
 
+  const bool qwen3 = m.q_norm || m.k_norm || m.rope_theta > 0.f;
+  const int Hq = P.attn.num_q_heads, Hkv = P.attn.num_kv_heads;
   hipError_t e = hpd::launch_norm_input(hidden_in, h, L.T, L.Tpad, L.H, gamma(m.g_attn_norm, 0), x, ss, attn,
                                          L.nq, packed, stream);
   for (int l = 0; l < m.num_layers && e == hipSuccess; ++l) {
@@ -202,6 +263,13 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
     g.dest = dev.token_dest;
     e = hpd::launch_gemm(g, false, hpd::kEpiQKV, hpd::KK_GEMM_QKV, stream);
     if (e != hipSuccess) break;
+    if (qwen3) {   // 1b: QK norm and rotary embedding of q and the new k rows
+      const int64_t items = (int64_t)L.T * (Hq + Hkv);
+      hpd::launch(hpd::KK_QK_ROPE, hpd::qk_norm_rope_kernel, dim3((unsigned)((items + 3) / 4)), dim3(256), stream,
+                  dev, q, (__bf16 *)priv_k[l], L.T, Hq, Hkv, gamma(m.q_norm, l), gamma(m.k_norm, l), m.rms_eps,
+                  m.rope_theta);
+      if ((e = hipGetLastError()) != hipSuccess) break;
+    }
     // 2: attention over the shared prefix and the private rows
     e = hpd::launch_branch_attention(P, q, shared_k ? shared_k[l] : nullptr, shared_v ? shared_v[l] : nullptr,
                                      priv_k[l], priv_v[l], attn, nullptr, workspace, stream, packed);

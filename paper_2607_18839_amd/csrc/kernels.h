@@ -19,6 +19,7 @@ struct PlanDev {
   const int32_t *token_slots;
   const int32_t *token_fork;
   const int32_t *token_dest;
+  const int32_t *token_vis;   // [T] visible keys of token t (its position + 1)
   int32_t *counters;
   float *part_o;
   float *part_lse;
@@ -28,7 +29,7 @@ PlanDev plan_dev(const Plan &P, void *workspace);
 
 // Kernel kinds of the optional benchmark timing (hpd_kernel_timing).
 enum KernelKind { KK_SHARED = 0, KK_PRIVATE, KK_MERGE, KK_GEMM_QKV, KK_GEMM_O, KK_GEMM_GATE_UP,
-                  KK_GEMM_DOWN, KK_NORM, KK_LM_HEAD, KK_VERIFY, KK_DRAFT_MLP, KK_DRAFT_TOKEN, KK_EMBED };
+                  KK_GEMM_DOWN, KK_NORM, KK_LM_HEAD, KK_VERIFY, KK_DRAFT_MLP, KK_DRAFT_TOKEN, KK_EMBED, KK_QK_ROPE };
 // Element offset of (row, col) of a [rows][cols] 16-bit matrix in the packed
 // layout (tiles of 32 rows x 64 columns, 2048 elements each, ordered by row
 // tile then column tile; inside a tile, element e of 16-byte piece (j, l) is

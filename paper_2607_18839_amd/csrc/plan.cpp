@@ -326,6 +326,8 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   off = align256(off + P.token_fork.size() * sizeof(int32_t));
   P.off_token_dest = off;
   off = align256(off + P.token_dest.size() * sizeof(int32_t));
+  P.off_token_vis = off;
+  off = align256(off + P.visible.size() * sizeof(int32_t));
   P.off_counters = off;   // zeroed by the upload; every user resets what it uses
   off = align256(off + kNumCounters * sizeof(int32_t));
   P.table_bytes = off;
@@ -348,6 +350,7 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   put(P.off_token_slots, P.token_slots);
   put(P.off_token_fork, P.token_fork);
   put(P.off_token_dest, P.token_dest);
+  put(P.off_token_vis, P.visible);
 
   *out = std::move(P);
   return HPD_OK;

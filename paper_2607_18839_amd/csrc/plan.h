@@ -64,6 +64,7 @@ struct Plan {
   std::vector<int32_t> token_slots;                   // [T][2]: first slot, count
   std::vector<int32_t> token_fork;                    // [T] visible prefix per token
   std::vector<int32_t> token_dest;                    // [T] private row of token t: priv_row + L + j
+  // (visible[t] - 1 is token t's position in its branch's sequence)
   int64_t num_slots = 0;                              // partial rows = num_slots * Hq
   int32_t split_keys = 0;                             // prefix keys per shared work item
   // One page without fork offsets: its shared items are (kv head, split, row
@@ -77,7 +78,7 @@ struct Plan {
   // device workspace layout (byte offsets, 256-aligned)
   size_t off_shared_tiles = 0, off_priv_tiles = 0, off_branch_q_row = 0, off_branch_new = 0;
   size_t off_shared_items = 0, off_private_items = 0, off_token_slots = 0,
-         off_token_fork = 0, off_token_dest = 0, off_counters = 0, off_part_o = 0, off_part_lse = 0, table_bytes = 0,
+         off_token_fork = 0, off_token_dest = 0, off_token_vis = 0, off_counters = 0, off_part_o = 0, off_part_lse = 0, table_bytes = 0,
          workspace_bytes = 0;
   std::vector<unsigned char> table_image;             // host copy of [0, table_bytes)
 

@@ -32,7 +32,7 @@ int64_t g_dropped = 0;
 
 const char *kKindNames[HPD_NUM_KERNEL_KINDS] = {
     "shared_prefix", "private", "merge", "gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down",
-    "norm_input", "lm_head", "verify", "draft_mlp", "draft_token", "embed"};
+    "norm_input", "lm_head", "verify", "draft_mlp", "draft_token", "embed", "qk_norm_rope"};
 
 }  // namespace
 

@@ -78,8 +78,9 @@ class DecodeStep:
     """One decode step of the decoder stack for a fixed batch shape.
 
     ``weights`` maps 'w_qkv', 'w_o', 'w_gate', 'w_up', 'w_down' (and
-    optionally 'g_attn_norm', 'g_mlp_norm') to lists of per-layer bf16 device
-    tensors in torch Linear layout.  The tensors must stay alive while the
+    optionally 'g_attn_norm', 'g_mlp_norm', and the Qwen3-style 'q_norm',
+    'k_norm' head gains) to lists of per-layer bf16 device tensors in torch
+    Linear layout; ``rope_theta`` > 0 turns on the rotary embedding.  The tensors must stay alive while the
     step is used.  packed=True packs the projection weights once here
     (HPD_WEIGHTS_PACKED, a device copy of the weights) and the step reads
     the packed copies.
@@ -87,7 +88,7 @@ class DecodeStep:
 
     def __init__(self, num_q_heads, num_kv_heads, prefix_len, branch_page, num_new, past_len,
                  weights, hidden, intermediate, rms_eps=1e-6, prefix_row=None, priv_row=None,
-                 device="cuda", stream=None, packed=False, fork_len=None, paged=None):
+                 device="cuda", stream=None, packed=False, fork_len=None, paged=None, rope_theta=0.0):
         self.attn = BranchAttention(num_q_heads, num_kv_heads, prefix_len, branch_page, num_new, past_len,
                                     dtype=torch.bfloat16, prefix_row=prefix_row, priv_row=priv_row,
                                     device=device, stream=stream, fork_len=fork_len, paged=paged)
@@ -107,7 +108,8 @@ class DecodeStep:
         ptrs = {k: [t.data_ptr() for t in v] for k, v in weights.items()}
         self.model = _lib.model_desc(self.num_layers, hidden, intermediate, rms_eps, ptrs["w_qkv"], ptrs["w_o"],
                                      ptrs["w_gate"], ptrs["w_up"], ptrs["w_down"], ptrs.get("g_attn_norm"),
-                                     ptrs.get("g_mlp_norm"), weight_format=fmt)
+                                     ptrs.get("g_mlp_norm"), weight_format=fmt, q_norm=ptrs.get("q_norm"),
+                                     k_norm=ptrs.get("k_norm"), rope_theta=rope_theta)
         self.plan_bytes = self.attn.ws_bytes
         self.ws_bytes = self.plan_bytes + _lib.hpd_decode_workspace_bytes(self.model, self.attn.plan)
         # one workspace holding the plan tables (uploaded) and the step's scratch

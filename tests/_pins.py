@@ -334,7 +334,10 @@ def _textbook_decoder(inp, branch_sel=None):
             x = torch.nn.functional.rms_norm(h, (H,), eps=inp.rms_eps)
             qkv = x @ val(inp.w_qkv[l]).T
             q = qkv[:, :Hq * D].reshape(k, Hq, D)
-            kn = qkv[:, Hq * D:(Hq + Hkv) * D].reshape(k, Hkv, D).to(torch.float32).to(torch.bfloat16).to(torch.float64)
+            kr = qkv[:, Hq * D:(Hq + Hkv) * D].reshape(k, Hkv, D)
+            if getattr(inp, "rope_theta", 0.0) or getattr(inp, "q_norm", None) is not None:
+                q, kr = _qwen3_library(inp, l, q, kr, [P + L + j for j in range(k)])
+            kn = kr.to(torch.float32).to(torch.bfloat16).to(torch.float64)
             vn = qkv[:, (Hq + Hkv) * D:].reshape(k, Hkv, D).to(torch.float32).to(torch.bfloat16).to(torch.float64)
             sk = val(inp.shared_k[l])[pstart[p]:pstart[p] + P]
             sv = val(inp.shared_v[l])[pstart[p]:pstart[p] + P]
@@ -356,13 +359,35 @@ def _textbook_decoder(inp, branch_sel=None):
     return np.concatenate(outs)
 
 
-def small_decode_inputs(seed=3, layers=2):
+def _qwen3_library(inp, l, q, k, pos):
+    """Qwen3-style q / k of one branch with library routines: torch's rms_norm
+    over each head with the gain, then transformers' Qwen3RotaryEmbedding and
+    apply_rotary_pos_emb at positions pos (fp32 angles there)."""
+    from transformers import Qwen3Config
+    from transformers.models.qwen3.modeling_qwen3 import Qwen3RotaryEmbedding, apply_rotary_pos_emb
+    D = q.shape[-1]
+    val = lambda b: torch.from_numpy(np.asarray(b, np.int32) << 16).view(torch.float32).to(torch.float64)
+    if getattr(inp, "q_norm", None) is not None:
+        q = torch.nn.functional.rms_norm(q, (D,), weight=val(inp.q_norm[l]), eps=inp.rms_eps)
+    if getattr(inp, "k_norm", None) is not None:
+        k = torch.nn.functional.rms_norm(k, (D,), weight=val(inp.k_norm[l]), eps=inp.rms_eps)
+    if getattr(inp, "rope_theta", 0.0):
+        cfg = Qwen3Config(head_dim=D, hidden_size=inp.hidden, num_attention_heads=q.shape[1],
+                          num_key_value_heads=k.shape[1], max_position_embeddings=4096, rope_theta=inp.rope_theta)
+        cos, sin = Qwen3RotaryEmbedding(cfg)(torch.zeros(1, len(pos), D), torch.tensor(pos)[None])
+        qo, ko = apply_rotary_pos_emb(q.permute(1, 0, 2)[None], k.permute(1, 0, 2)[None], cos.double(), sin.double())
+        q, k = qo[0].permute(1, 0, 2), ko[0].permute(1, 0, 2)
+    return q, k
+
+
+def small_decode_inputs(seed=3, layers=2, qwen3=None):
+    model = dict(num_layers=layers, hidden=32, intermediate=48, weight_std=0.2, rms_eps=1e-6)
+    if qwen3:
+        model["qwen3"] = qwen3
     cfg = get_config("c4", num_q_heads=4, num_kv_heads=2, head_dim=8, num_pages=1,
                      prefix=("fixed", 11), layout=dict(k=1, past=("fixed", 5)),
                      content_count=("fixed", 2), content_k=3,
-                     content_past=("list", [0, 4]),
-                     model=dict(num_layers=layers, hidden=32, intermediate=48,
-                                weight_std=0.2, rms_eps=1e-6))
+                     content_past=("list", [0, 4]), model=model)
     return make_decode_inputs(cfg, seed)
 
 
@@ -392,8 +417,20 @@ def pin_decode_kv_written(att=None, plan=None, dec=None):
     return float(np.count_nonzero(kbits != nk[0]) + np.count_nonzero(vbits != nv[0]))
 
 
+def pin_decode_qwen3_library(att=None, plan=None, dec=None):
+    """The step with per-head QK norm and rotary embedding against the
+    branch-by-branch decoder built from torch's rms_norm / SDPA and
+    transformers' Qwen3 rotary routines (base 10^2, so positions 11..20 turn
+    every frequency by a visible angle)."""
+    inp = small_decode_inputs(qwen3=dict(rope_theta=100.0, qk_norm=True))
+    h, _, _ = dec.decode_step(inp)
+    return float(np.abs(h - _textbook_decoder(inp)).max())
+
+
 ATTN_PINS = [pin_hand_cases, pin_brute_force, pin_split_merge, pin_sdpa_k1, pin_sdpa_bottom_right,
              pin_rows_sum_to_one, pin_visible_count, pin_isolation, pin_causal_prefix, pin_equivariance]
 PLAN_PINS = [pin_plan_walk]
-DECODE_PINS = [pin_decode_textbook, pin_decode_kv_written]
-TOLERANCE = {pin_decode_textbook: 1e-10, pin_plan_walk: 0.0, pin_decode_kv_written: 0.0}
+DECODE_PINS = [pin_decode_textbook, pin_decode_kv_written, pin_decode_qwen3_library]
+# the Qwen3 pin: transformers takes the rotary angles in fp32 (about 1e-7 relative)
+TOLERANCE = {pin_decode_textbook: 1e-10, pin_plan_walk: 0.0, pin_decode_kv_written: 0.0,
+             pin_decode_qwen3_library: 1e-5}

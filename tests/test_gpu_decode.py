@@ -23,8 +23,12 @@ def run_decode(inp, canary=True, packed=False):
     """Runs hpd_decode_step on the inputs; returns (h_out, priv_k list, priv_v list) as numpy."""
     from paper_2607_18839_amd.torch_api import DecodeStep
     w = {k: [to_dev(a, "bf16") for a in getattr(inp, k)] for k in ("w_qkv", "w_o", "w_gate", "w_up", "w_down")}
+    for k in ("q_norm", "k_norm"):   # Qwen3-style inputs, when the workload has them
+        if getattr(inp, k, None) is not None:
+            w[k] = [to_dev(a, "bf16") for a in getattr(inp, k)]
     step = DecodeStep(inp.num_q_heads, inp.num_kv_heads, inp.prefix_len, inp.branch_page, inp.num_new,
-                      inp.past_len, w, inp.hidden, inp.intermediate, inp.rms_eps, packed=packed)
+                      inp.past_len, w, inp.hidden, inp.intermediate, inp.rms_eps, packed=packed,
+                      fork_len=getattr(inp, "fork_len", None), rope_theta=getattr(inp, "rope_theta", 0.0))
     sk = [to_dev(a, "bf16") for a in inp.shared_k]
     sv = [to_dev(a, "bf16") for a in inp.shared_v]
     pk_np = [a.copy() for a in inp.priv_k]
@@ -128,3 +132,41 @@ def test_decode_deterministic_and_hidden_alias():
     h3, pk3, _ = run_decode(inp, packed=True)
     h4, pk4, _ = run_decode(inp, packed=True)
     assert np.array_equal(h3, h4) and all(np.array_equal(a, b) for a, b in zip(pk3, pk4))
+
+
+def qwen3_inputs(seed, layers=2, theta=1e4):
+    cfg = get_config("c4", num_q_heads=4, num_kv_heads=2, num_pages=1, prefix=("fixed", 300),
+                     layout=dict(k=1, past=("fixed", 70)), content_count=("fixed", 5), content_k=4,
+                     content_past=("lognormal", 40.0, 1.0, 0, 200),
+                     model=dict(num_layers=layers, hidden=256, intermediate=384, weight_std=0.05, rms_eps=1e-6,
+                                qwen3=dict(rope_theta=theta, qk_norm=True)))
+    return make_decode_inputs(cfg, seed)
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_qwen3_small_stack(seed):
+    """Per-head QK norm and rotary embedding (base 10^4) on the small stack,
+    with random fork points for the content branches on the second seed."""
+    announce(f"decode qwen3 small seed {seed}")
+    inp = qwen3_inputs(seed)
+    if seed == 1:
+        rng = np.random.default_rng(9)
+        P = int(inp.prefix_len[0])
+        inp.fork_len = np.array([P] + [int(rng.integers(100, P + 1)) for _ in inp.num_new[1:]], np.int64)
+    h, pk, pv = run_decode(inp, packed=True)
+    ref, nk, nv = decode_step(inp)
+    mx, rl = errors(h, ref)
+    print(f"qwen3 small seed {seed}: max abs {mx:.3e} rel L2 {rl:.3e}")
+    assert mx <= BF16_MAX_ABS and rl <= BF16_REL_L2, (mx, rl)
+    _check_cache(inp, pk, pv, nk, nv)
+
+
+def test_qwen3_c4q_full_step():
+    """c4q: the 18-layer c4 step with QK norm and rotary embedding (base 10^6)."""
+    announce("decode c4q")
+    inp = make_decode_inputs("c4q", 0)
+    h, pk, pv = run_decode(inp, packed=True)
+    ref, nk, nv = decode_step(inp)
+    mx, rl = errors(h, ref)
+    print(f"c4q: max abs {mx:.3e} rel L2 {rl:.3e}")
+    assert mx <= BF16_MAX_ABS and rl <= BF16_REL_L2, (mx, rl)

@@ -166,3 +166,67 @@ def test_pmtp_lm_input_rounding_is_bf16():
     got = lm_logits(h, g, eye)
     want = bf16_bits_to_f64(f64_to_bf16_bits(h * g))
     assert np.array_equal(got, want)
+
+
+# ---------------------------------------------------------------- Qwen3-style attention inputs
+
+def test_qk_norm_matches_transformers_qwen3_rmsnorm():
+    """The per-head q / k norm against transformers' Qwen3RMSNorm (library;
+    it normalises in fp32, hence the tolerance)."""
+    import torch
+    from transformers.models.qwen3.modeling_qwen3 import Qwen3RMSNorm
+    from oracle.decode import rms_norm
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((7, 3, 64)) * 2.0
+    g = 1 + 0.1 * rng.standard_normal(64)
+    m = Qwen3RMSNorm(64, eps=1e-6).double()
+    with torch.no_grad():
+        m.weight.copy_(torch.from_numpy(g))
+        want = m(torch.from_numpy(x)).numpy()
+    assert np.abs(rms_norm(x, 1e-6, g) - want).max() < 1e-5
+
+
+def test_rope_matches_transformers_qwen3_rotary_embedding():
+    """The rotary embedding against transformers' Qwen3RotaryEmbedding and
+    apply_rotary_pos_emb (library; fp32 angles there, hence the tolerance)."""
+    import torch
+    from transformers import Qwen3Config
+    from transformers.models.qwen3.modeling_qwen3 import Qwen3RotaryEmbedding, apply_rotary_pos_emb
+    from oracle.decode import rope
+    cfg = Qwen3Config(head_dim=64, hidden_size=1024, num_attention_heads=16, num_key_value_heads=2,
+                      max_position_embeddings=8192, rope_theta=1e6)
+    pos = np.array([0, 1, 5, 100, 2047])
+    cos, sin = Qwen3RotaryEmbedding(cfg)(torch.zeros(1, len(pos), 64), torch.from_numpy(pos)[None])
+    rng = np.random.default_rng(6)
+    q, k = rng.standard_normal((5, 3, 64)), rng.standard_normal((5, 2, 64))
+    qo, ko = apply_rotary_pos_emb(torch.from_numpy(q).permute(1, 0, 2)[None].float(),
+                                  torch.from_numpy(k).permute(1, 0, 2)[None].float(), cos, sin)
+    assert np.abs(qo[0].permute(1, 0, 2).double().numpy() - rope(q, pos, 1e6)).max() < 1e-4
+    assert np.abs(ko[0].permute(1, 0, 2).double().numpy() - rope(k, pos, 1e6)).max() < 1e-4
+
+
+def test_rope_scores_depend_only_on_the_position_difference():
+    """<rope(q, m), rope(k, n)> = <rope(q, m - n), k> per head (closed form of
+    a rotation), rope(x, 0) = x, and norms are kept."""
+    from oracle.decode import rope
+    rng = np.random.default_rng(7)
+    q, k = rng.standard_normal((1, 64)), rng.standard_normal((1, 64))
+    for m, n in ((5, 3), (4000, 17), (123, 123), (0, 900)):
+        lhs = np.sum(rope(q, [m], 1e6) * rope(k, [n], 1e6))
+        rhs = np.sum(rope(q, [m - n], 1e6) * k)
+        assert abs(lhs - rhs) < 1e-9 * (1 + abs(rhs))
+    x = rng.standard_normal((3, 2, 64))
+    assert np.allclose(rope(x, [0, 0, 0], 1e4), x, rtol=0, atol=0)
+    y = rope(x, [1, 70, 3000], 1e4)
+    assert np.allclose(np.linalg.norm(y, axis=-1), np.linalg.norm(x, axis=-1), rtol=1e-12)
+
+
+def test_qwen3_options_off_leave_the_step_unchanged():
+    """rope_theta = 0 and no gains: the step equals the plain one bit for bit."""
+    from oracle.decode import decode_step
+    from tests.test_gpu_decode import small_inputs
+    inp = small_inputs(0, layers=1)
+    h0, k0, _ = decode_step(inp)
+    inp.rope_theta = 0.0
+    h1, k1, _ = decode_step(inp)
+    assert np.array_equal(h0, h1) and all(np.array_equal(a, b) for a, b in zip(k0, k1))

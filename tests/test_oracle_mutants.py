@@ -63,8 +63,11 @@ MUTANTS = [
     ("decode", "h = h + a.reshape(T, Hq * D) @ Wo.T", "h = a.reshape(T, Hq * D) @ Wo.T"),  # lost residual
     ("decode", "return u / (1.0 + np.exp(-u))", "return u / (1.0 + np.exp(u))"),      # silu sign
     ("decode", "np.mean(y * y, axis=-1, keepdims=True) + eps", "np.mean(y * y, axis=0, keepdims=True) + eps"),
-    ("decode", "k_new = _bf16_value(qkv[:, Hq * D:(Hq + Hkv) * D].reshape(T, Hkv, D))",
-               "k_new = qkv[:, Hq * D:(Hq + Hkv) * D].reshape(T, Hkv, D)"),     # cache not bf16
+    ("decode", "k_new = _bf16_value(k_raw)", "k_new = k_raw"),                    # cache not bf16
+    ("decode", "return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)",
+               "return np.concatenate([x1 * c + x2 * s, x2 * c - x1 * s], axis=-1)"),   # rotation sign
+    ("decode", "float(theta) ** (-np.arange(half) / half)", "float(theta) ** (-np.arange(half) / (2 * half))"),
+    ("decode", "pos = np.asarray(visible, np.float64) - 1", "pos = np.asarray(visible, np.float64)"),  # off by one
     ("decode", "v_new = _bf16_value(qkv[:, (Hq + Hkv) * D:].reshape(T, Hkv, D))",
                "v_new = _bf16_value(qkv[:, Hq * D:(Hq + Hkv) * D].reshape(T, Hkv, D))"),  # v := k
     ("decode", "(silu(x @ Wg.T) * (x @ Wu.T)) @ Wd.T", "(silu(x @ Wu.T) * (x @ Wg.T)) @ Wd.T"),  # gate/up swapped

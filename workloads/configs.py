@@ -65,6 +65,17 @@ CONFIGS = {
         # parser; readings in the design notes)
         pmtp=dict(vocab=151936, draft_inner=1024, weight_std=0.02),
     ),
+    # c4 with Qwen3-style attention: per-head q / k RMSNorm (gains 1 + 0.1 N(0, 1))
+    # and rotary position embedding, base 10^6 (the Qwen3 family's)
+    "c4q": dict(
+        name="c4q", dtype="bf16", num_q_heads=16, num_kv_heads=2, head_dim=64,
+        num_pages=1, prefix=("fixed", 4096),
+        layout=dict(k=1, past=("fixed", 512)),
+        content_count=("fixed", 32), content_k=4,
+        content_past=("lognormal", 128.0, 1.0, 8, 1024),
+        model=dict(num_layers=18, hidden=1024, intermediate=3072,
+                   weight_std=0.02, rms_eps=1e-6, qwen3=dict(rope_theta=1e6, qk_norm=True)),
+    ),
     # c3 with per-branch fork offsets (tree-shaped prefix): a content branch
     # sees the page's prefix only up to its fork point F_b, drawn uniform in
     # [1024, P] (1024 = the visual-token part every branch sees); the layout

@@ -249,6 +249,11 @@ class DecodeInputs:
     w_gate: list = field(default_factory=list)
     w_up: list = field(default_factory=list)
     w_down: list = field(default_factory=list)
+    # Qwen3-style attention (model "qwen3" in the config): per-layer [64] bf16
+    # gains of the per-head q / k RMSNorm and the rotary base; None / 0 = off
+    q_norm: list = None
+    k_norm: list = None
+    rope_theta: float = 0.0
 
     @property
     def num_tokens(self):
@@ -295,6 +300,14 @@ def make_decode_inputs(cfg_or_name, seed, num_layers=None):
         out.w_gate.append(f64_to_bf16_bits(std * rng.standard_normal((I, H))))
         out.w_up.append(f64_to_bf16_bits(std * rng.standard_normal((I, H))))
         out.w_down.append(f64_to_bf16_bits(std * rng.standard_normal((H, I))))
+    qw = m.get("qwen3")
+    if qw:   # own stream (seed, 13): every draw above is unchanged
+        out.rope_theta = float(qw["rope_theta"])
+        if qw.get("qk_norm"):
+            r2 = np.random.default_rng([seed, 13])
+            gain = lambda: f64_to_bf16_bits(1.0 + 0.1 * r2.standard_normal(D))
+            out.q_norm = [gain() for _ in range(Lyr)]
+            out.k_norm = [gain() for _ in range(Lyr)]
     return out
 
 
