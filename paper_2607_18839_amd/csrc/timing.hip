@@ -14,6 +14,9 @@
 #include "kernels.h"
 
 namespace hpd {
+
+void set_last_error(const std::string &msg);
+
 namespace {
 
 struct Pair {
@@ -65,12 +68,21 @@ hpd_status hpd_attn_phase_isolation(int enable) {
 hpd_status hpd_kernel_timing(int enable, int max_launches) {
   std::lock_guard<std::mutex> lk(hpd::g_mu);
   if (enable) {
-    if (max_launches < 1) return HPD_ERR_INVALID_ARGUMENT;
-    for (auto &p : hpd::g_pool) { hipEventDestroy(p.start); hipEventDestroy(p.stop); }
+    if (max_launches < 1) {
+      hpd::set_last_error("hpd_kernel_timing: max_launches must be >= 1");
+      return HPD_ERR_INVALID_ARGUMENT;
+    }
+    for (auto &p : hpd::g_pool) {   // events of a previous enable (a failed one may have left NULLs)
+      if (p.start) (void)hipEventDestroy(p.start);
+      if (p.stop) (void)hipEventDestroy(p.stop);
+    }
     hpd::g_pool.assign(max_launches, hpd::Pair{});
     for (auto &p : hpd::g_pool) {
-      if (hipEventCreate(&p.start) != hipSuccess || hipEventCreate(&p.stop) != hipSuccess)
+      if (hipEventCreate(&p.start) != hipSuccess || hipEventCreate(&p.stop) != hipSuccess) {
+        hpd::g_enabled = false;
+        hpd::set_last_error("hpd_kernel_timing: hipEventCreate failed");
         return HPD_ERR_HIP;
+      }
     }
     hpd::g_used = 0;
     hpd::g_enabled = true;
