@@ -126,7 +126,6 @@ hpd_status build_batch(hpd_sched *s) {
     s->prefill_from.push_back(r.kept);
     s->prefill_to.push_back(r.len);
     s->branch_seq.push_back(r.seq);
-    r.kept = r.len;   // the caller computes the prefill rows before the step
   }
   s->page_block0.assign(s->pages.size(), 0);
   s->branch_block0.assign(order.size(), 0);
@@ -136,9 +135,13 @@ hpd_status build_batch(hpd_sched *s) {
                                       s->page_block0.data(), s->branch_block0.data(), &n);
   if (st != HPD_OK && n == 0) return st;
   s->blocks.assign((size_t)std::max(n, 1), 0);
-  return hpd_kv_batch_tables(s->pool, (int32_t)s->pages.size(), s->page_seq.data(), (int32_t)order.size(),
-                             s->branch_seq.data(), s->blocks.data(), n, s->page_block0.data(),
-                             s->branch_block0.data(), &n);
+  st = hpd_kv_batch_tables(s->pool, (int32_t)s->pages.size(), s->page_seq.data(), (int32_t)order.size(),
+                           s->branch_seq.data(), s->blocks.data(), n, s->page_block0.data(), s->branch_block0.data(),
+                           &n);
+  if (st != HPD_OK) return st;
+  s->blocks.resize((size_t)n);
+  for (int32_t id : order) s->reqs[id].kept = s->reqs[id].len;   // the caller computes the prefill rows first
+  return HPD_OK;
 }
 
 void fill_out(const hpd_sched *s, hpd_sched_batch *out) {

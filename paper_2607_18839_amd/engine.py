@@ -106,10 +106,12 @@ class Engine:
             self._buf[name] = t
         return t[:n]
 
-    def step(self, stream=None):
-        """One iteration; returns the batch with the step's results (host
-        arrays under 'verified', 'n_acc', 'draft_out', 'hidden_out'), or the
-        empty batch when nothing was active."""
+    def step(self):
+        """One iteration on torch's current stream (the prefill, the library
+        launches and the read-back of the results share it); returns the
+        batch with the step's results (host arrays under 'verified', 'n_acc',
+        'draft_out', 'hidden_out'), or the empty batch when nothing was
+        active."""
         t0 = time.perf_counter()
         batch = self.sched.schedule()
         t1 = time.perf_counter()
@@ -128,7 +130,7 @@ class Engine:
         if self.workspace.numel() < need:
             self.workspace = torch.empty(need * 3 // 2 + 4096, dtype=torch.uint8, device=self.device)
         ws, ws_bytes = self.workspace.data_ptr(), self.workspace.numel()
-        s = _stream(stream)
+        s = _stream(None)
         _lib.hpd_plan_upload(plan, ws, ws_bytes, s)
         self.host_s["plan"] += time.perf_counter() - t2
         tok = self._buffer("tokens", T, torch.int32)
