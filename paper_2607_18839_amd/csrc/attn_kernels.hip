@@ -382,6 +382,15 @@ template <typename T> struct WaveAttn {
     }
     u32x2t vr[16];   // [b][st][hh]
     ds_read_tr16_tile<0>(vr, vt + voff[0], vt + voff[1]);
+    // matrix core first: the next tile's scores need only the K reads, and
+    // run while the VALU does this tile's softmax
+    if (kt_next) {
+      for (int r = 0; r < 16; ++r) { s_next[0][r] = 0.f; s_next[1][r] = 0.f; }
+#pragma unroll
+      for (int st = 0; st < 4; ++st)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) mma(s_next[kb], ka[kb][st], qf[st]);
+    }
     // softmax of this tile (VALU)
     if (masked) {
 #pragma unroll
@@ -422,15 +431,8 @@ template <typename T> struct WaveAttn {
     Frag<T> pf[4];
 #pragma unroll
     for (int st = 0; st < 4; ++st) from_f32(pf[st], p + 8 * st);
-    lds_wait_tr(vr);   // also completes the K reads (lgkmcnt(0))
-    // matrix core: next tile's scores, this tile's PV and row sums
-    if (kt_next) {
-      for (int r = 0; r < 16; ++r) { s_next[0][r] = 0.f; s_next[1][r] = 0.f; }
-#pragma unroll
-      for (int st = 0; st < 4; ++st)
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) mma(s_next[kb], ka[kb][st], qf[st]);
-    }
+    lds_wait_tr(vr);   // (lgkmcnt(0))
+    // matrix core: this tile's PV and row sums
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
