@@ -143,20 +143,21 @@ def qwen3_inputs(seed, layers=2, theta=1e4):
     return make_decode_inputs(cfg, seed)
 
 
-@pytest.mark.parametrize("seed", [0, 1])
-def test_qwen3_small_stack(seed):
+@pytest.mark.parametrize("seed,packed", [(0, True), (1, True), (0, False)], ids=["packed0", "packed1", "torch0"])
+def test_qwen3_small_stack(seed, packed):
     """Per-head QK norm and rotary embedding (base 10^4) on the small stack,
-    with random fork points for the content branches on the second seed."""
-    announce(f"decode qwen3 small seed {seed}")
+    with random fork points for the content branches on the second seed,
+    with packed and with torch-layout weights."""
+    announce(f"decode qwen3 small seed {seed} packed {packed}")
     inp = qwen3_inputs(seed)
     if seed == 1:
         rng = np.random.default_rng(9)
         P = int(inp.prefix_len[0])
         inp.fork_len = np.array([P] + [int(rng.integers(100, P + 1)) for _ in inp.num_new[1:]], np.int64)
-    h, pk, pv = run_decode(inp, packed=True)
+    h, pk, pv = run_decode(inp, packed=packed)
     ref, nk, nv = decode_step(inp)
     mx, rl = errors(h, ref)
-    print(f"qwen3 small seed {seed}: max abs {mx:.3e} rel L2 {rl:.3e}")
+    print(f"qwen3 small seed {seed} packed {packed}: max abs {mx:.3e} rel L2 {rl:.3e}")
     assert mx <= BF16_MAX_ABS and rl <= BF16_REL_L2, (mx, rl)
     _check_cache(inp, pk, pv, nk, nv)
 
