@@ -150,10 +150,12 @@ def _kernel_pass(torch, _lib, step, K, W, queue_cycles=20_000_000):
             if not k.startswith("_") and c}
 
 
-def _phase_pass(torch, _lib, step, K, W, work, queue_cycles=2_000_000):
+def _phase_pass(torch, _lib, step, K, W, work, queue_cycles=2_000_000, measured=False):
     """Per-kernel durations with the attention phases in launches of their own
     (hpd_attn_phase_isolation): the shared-prefix items alone (MFMA-bound) and
-    the private items alone (HBM-bound), next to the co-scheduled launch."""
+    the private items alone (HBM-bound), next to the co-scheduled launch.
+    measured: also the rocprofv3-measured HBM bytes of each phase launch
+    (profiles/traffic_c4.md, taken on the c4 step) and the rate they give."""
     _lib.hpd_attn_phase_isolation(True)
     try:
         kern = _kernel_pass(torch, _lib, step, K, W, queue_cycles)
@@ -169,6 +171,12 @@ def _phase_pass(torch, _lib, step, K, W, work, queue_cycles=2_000_000):
         out["private_algorithmic_bytes"] = work["private_bytes"]
         out["private_gbs"] = work["private_bytes"] / pr / 1e3
         out["private_hbm_frac"] = work["private_bytes"] / pr / 1e3 / HBM_PEAK_GBS
+    if measured:
+        for phase, us in (("shared_phase", sh), ("private_phase", pr)):
+            tb = _traffic(phase)
+            if us and tb:
+                out[phase + "_measured_bytes"] = tb
+                out[phase + "_measured_gbs"] = tb / us / 1e3
     return out
 
 
@@ -423,7 +431,8 @@ def bench_decode(args, torch, _lib):
             k.update(bound="hbm", bytes=lb, gbs=lb / us / 1e3, frac=lb / us / 1e3 / HBM_PEAK_GBS)
         k["total_us_per_step"] = us * k["launches"] / min(args.steps, 10)
     dom = max(kern, key=lambda n: kern[n]["total_us_per_step"])
-    kern["phases_isolated"] = _phase_pass(torch, _lib, step, min(args.steps, 10), args.warmup, aw)
+    kern["phases_isolated"] = _phase_pass(torch, _lib, step, min(args.steps, 10), args.warmup, aw,
+                                          measured=args.workload == "c4" and not args.paged)
     d = kern[dom]
     if d.get("bound") == "mfma":
         roof = {"bound": "mfma", "kernel": dom, "achieved": d["tflops"], "peak": BF16_PEAK_TFLOPS,
