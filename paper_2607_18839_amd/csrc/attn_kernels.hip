@@ -357,9 +357,11 @@ template <typename T> struct WaveAttn {
 
   // One software-pipelined step of the ring kernel: the LDS reads of the
   // next tile's K (kt_next, or none) and of this tile's V^T are issued first,
-  // the softmax of this tile's raw scores s_cur runs while they are in flight,
-  // then the next tile's QK^T MFMAs (into s_next) and this tile's PV and
-  // row-sum MFMAs are issued together.  FSUM: the row sums are instead taken
+  // then the next tile's QK^T MFMAs (into s_next), which need only the K
+  // reads and run while the VALU does the softmax of this tile's raw scores
+  // s_cur, then this tile's PV and row-sum MFMAs.  (Measured: giving the
+  // two waves of a SIMD opposite orders, QK^T last on one of them, is
+  // slower.)  FSUM: the row sums are instead taken
   // in fp32 on the VALU into l (this lane's half of the keys), which keeps
   // the exported log-sum-exp exact to fp32 rounding when a row sees only a
   // few keys (the matrix-core sum adds bf16-rounded probabilities).
