@@ -171,3 +171,22 @@ def test_qwen3_c4q_full_step():
     mx, rl = errors(h, ref)
     print(f"c4q: max abs {mx:.3e} rel L2 {rl:.3e}")
     assert mx <= BF16_MAX_ABS and rl <= BF16_REL_L2, (mx, rl)
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_small_stack_multipage(seed):
+    """Three pages of ragged prefixes and branch counts (the planner's general
+    work lists, not the single-page computed items), packed weights."""
+    announce(f"decode small multipage seed {seed}")
+    cfg = get_config("c4", num_q_heads=4, num_kv_heads=2, num_pages=3, prefix=("uniform", 64, 300),
+                     layout=dict(k=1, past=("uniform", 0, 90)), content_count=("uniform", 2, 5), content_k=4,
+                     content_past=("lognormal", 40.0, 1.0, 0, 200),
+                     model=dict(num_layers=2, hidden=256, intermediate=384, weight_std=0.05, rms_eps=1e-6))
+    inp = make_decode_inputs(cfg, seed)
+    assert len(inp.prefix_len) == 3
+    h, pk, pv = run_decode(inp, packed=True)
+    ref, nk, nv = decode_step(inp)
+    mx, rl = errors(h, ref)
+    print(f"multipage seed {seed}: T {len(h)} max abs {mx:.3e} rel L2 {rl:.3e}")
+    assert mx <= BF16_MAX_ABS and rl <= BF16_REL_L2, (mx, rl)
+    _check_cache(inp, pk, pv, nk, nv)
