@@ -250,3 +250,51 @@ def test_fork_work_lists_cover_visible_keys_once(name, st, Hq, Hkv):
     for t in range(T):
         assert np.all(cov[t] == 1), t
     assert np.all(slot_writes == 1)
+
+
+def test_embed_and_pmtp_entry_points_validate_before_launching(lib):
+    """hpd_embed_tokens and hpd_verify_draft_step reject bad arguments on the
+    host, before any launch (fake device addresses are never touched)."""
+    fake = 4096
+    assert lib.hpd_embed_tokens(None, 1024, 256, fake, 4, fake, None) == 1
+    assert lib.hpd_embed_tokens(fake, 1024, 250, fake, 4, fake, None) == 1          # hidden % 4
+    assert lib.hpd_embed_tokens(fake + 2, 1024, 256, fake, 4, fake, None) == 1     # 8-byte alignment
+    assert lib.hpd_embed_tokens(fake, 1024, 256, fake, 4, fake + 4, None) == 1     # out 16-byte aligned
+    assert b"hpd_embed_tokens" in lib.hpd_last_error_message()
+    st = tiny_structures()[1]
+    plan = _plan(st, 4, 2)
+    one = [fake]
+    model = _lib.model_desc(1, 256, 384, 1e-6, one, one, one, one, one, weight_format=1)
+    ok = dict(vocab=1024, draft_inner=128, lm_head=fake, g_final=None, embed=fake, w_draft_gate_up=fake,
+              w_draft_down=fake, window=0)
+    cases = [(dict(window=HPD_MAX_K + 1), "window"), (dict(window=-1), "window"),
+             (dict(vocab=1000), "multiples of 128"), (dict(lm_head=fake + 8), "misaligned"),
+             (dict(embed=None), "misaligned")]
+    for over, needle in cases:
+        d = dict(ok, **over)
+        desc = _lib.hpd_pmtp_desc(d["vocab"], d["draft_inner"], d["lm_head"], d["g_final"], d["embed"],
+                                  d["w_draft_gate_up"], d["w_draft_down"], d["window"])
+        with pytest.raises(_lib.HpdError) as e:
+            _lib.hpd_verify_draft_step(model, desc, plan, fake, fake, fake, fake, fake, fake, 1 << 30)
+        assert needle in str(e.value), (over, str(e.value))
+    small = _lib.model_desc(1, 128, 384, 1e-6, one, one, one, one, one, weight_format=1)   # hidden % 256
+    desc = _lib.hpd_pmtp_desc(1024, 128, fake, None, fake, fake, fake, 0)
+    with pytest.raises(_lib.HpdError) as e:
+        _lib.hpd_verify_draft_step(small, desc, plan, fake, fake, fake, fake, fake, fake, 1 << 30)
+    assert "multiple of 256" in str(e.value)
+
+
+def test_qwen3_options_are_validated():
+    st = tiny_structures()[1]
+    plan = _plan(st, 4, 2)
+    fake = 4096
+    one = [fake]
+    for kw, needle in ((dict(rope_theta=-1.0), "rope_theta"), (dict(rope_theta=float("nan")), "rope_theta"),
+                       (dict(q_norm=[None]), "q_norm"), (dict(k_norm=[fake + 2]), "k_norm")):
+        model = _lib.model_desc(1, 256, 384, 1e-6, one, one, one, one, one, weight_format=1, **kw)
+        with pytest.raises(_lib.HpdError) as e:
+            _lib.hpd_decode_step(model, plan, fake, fake, one, one, one, one, 4096, 1 << 30)
+        assert needle in str(e.value), (kw, str(e.value))
+
+
+HPD_MAX_K = _lib.HPD_MAX_K
