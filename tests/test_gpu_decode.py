@@ -173,6 +173,28 @@ def test_qwen3_c4q_full_step():
     assert mx <= BF16_MAX_ABS and rl <= BF16_REL_L2, (mx, rl)
 
 
+@pytest.mark.parametrize("packed", [False, True], ids=["torch", "packed"])
+def test_many_token_tiles(packed):
+    """322 tokens (two pages of 40 content branches, k = 4): 11 token tiles,
+    the last holding 2 tokens.  Each projection's token tiles start their K
+    walks at different steps, and with more tiles than K steps per wave
+    (QKV 2, down 3, gate/up 8 at hidden 512, intermediate 768) several tiles
+    share a start; the whole step is checked against the oracle."""
+    announce(f"decode 322 tokens, 11 token tiles, packed {packed}")
+    cfg = get_config("c4", num_q_heads=4, num_kv_heads=2, num_pages=2, prefix=("fixed", 200),
+                     layout=dict(k=1, past=("fixed", 40)), content_count=("fixed", 40), content_k=4,
+                     content_past=("lognormal", 30.0, 1.0, 0, 150),
+                     model=dict(num_layers=2, hidden=512, intermediate=768, weight_std=0.05, rms_eps=1e-6))
+    inp = make_decode_inputs(cfg, 3)
+    h, pk, pv = run_decode(inp, packed=packed)
+    assert len(h) == 322
+    ref, nk, nv = decode_step(inp)
+    mx, rl = errors(h, ref)
+    print(f"322 tokens, packed {packed}: max abs {mx:.3e} rel L2 {rl:.3e}")
+    assert mx <= BF16_MAX_ABS and rl <= BF16_REL_L2, (mx, rl)
+    _check_cache(inp, pk, pv, nk, nv)
+
+
 @pytest.mark.parametrize("seed", [0, 1])
 def test_small_stack_multipage(seed):
     """Three pages of ragged prefixes and branch counts (the planner's general
