@@ -29,6 +29,15 @@ GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 TOL = 1e-12
 
 
+def _worse(err, *vals):
+    """The largest of the errors; NaN counts as an infinite error (Python's
+    max would silently drop it)."""
+    for v in vals:
+        v = float(v)
+        err = float("inf") if math.isnan(v) else max(err, v)
+    return err
+
+
 def _st(batch):
     return dict(prefix_len=batch.prefix_len, branch_page=batch.branch_page,
                 num_new=batch.num_new, past_len=batch.past_len, fork_len=batch.fork_len)
@@ -54,18 +63,43 @@ def tiny_structures():
     return S
 
 
+def fork_structures():
+    """Tiny structures with per-branch fork points F_b < P_p (a branch sees its
+    page's prefix only up to its fork position, section "Layout-Coordinated
+    Parallel Decoding", paragraph "Dynamic Branch Forking and Efficient Context
+    Isolation"): F_b in {0, 1, a middle value, P_p} on one page, the same mix
+    over three pages (one of them empty), and one branch whose fork cuts the
+    prefix while k > 1."""
+    S = []
+    S.append(dict(prefix_len=np.array([7], np.int32), branch_page=np.array([0, 0, 0, 0], np.int32),
+                  num_new=np.array([1, 3, 2, 2], np.int32), past_len=np.array([2, 0, 3, 1], np.int32),
+                  fork_len=np.array([7, 0, 1, 4], np.int32)))
+    S.append(dict(prefix_len=np.array([5, 0, 9], np.int32), branch_page=np.array([0, 0, 1, 2, 2, 2], np.int32),
+                  num_new=np.array([2, 1, 1, 3, 1, 2], np.int32), past_len=np.array([0, 3, 2, 1, 4, 0], np.int32),
+                  fork_len=np.array([5, 2, 0, 0, 9, 3], np.int32)))
+    S.append(dict(prefix_len=np.array([6], np.int32), branch_page=np.array([0], np.int32),
+                  num_new=np.array([4], np.int32), past_len=np.array([2], np.int32),
+                  fork_len=np.array([3], np.int32)))
+    return S
+
+
 def tiny_batches(dtype="f32"):
     out = []
-    for i, st in enumerate(tiny_structures()):
+    for i, st in enumerate(tiny_structures() + fork_structures()):
         for Hq, Hkv, D in [(4, 2, 8), (2, 1, 3), (6, 3, 4)]:
             out.append(attn_batch_from_structure(st, Hq, Hkv, D, dtype, seed=100 + i))
     return out
 
 
+def _fork_list(b):
+    return None if b.fork_len is None else [int(f) for f in b.fork_len]
+
+
 # ------------------------------------------------------------------ pins
 
 def pin_hand_cases(att, plan=None, dec=None):
-    cases = json.load(open(os.path.join(GOLDEN, "hand_cases.json")))["cases"]
+    with open(os.path.join(GOLDEN, "hand_cases.json")) as f:
+        cases = json.load(f)["cases"]
     ns = {"e": math.e, "log": math.log, "exp": math.exp, "__builtins__": {}}
     err = 0.0
     for c in cases:
@@ -76,7 +110,7 @@ def pin_hand_cases(att, plan=None, dec=None):
                                st, c["Hq"], c["Hkv"])
         eO = np.vectorize(lambda s: eval(s, ns))(np.array(c["expected_O"], dtype=object)).astype(np.float64)
         eL = np.vectorize(lambda s: eval(s, ns))(np.array(c["expected_lse"], dtype=object)).astype(np.float64)
-        err = max(err, float(np.abs(O - eO).max()), float(np.abs(lse - eL).max()))
+        err = _worse(err, float(np.abs(O - eO).max()), float(np.abs(lse - eL).max()))
     return err
 
 
@@ -88,8 +122,9 @@ def pin_brute_force(att, plan=None, dec=None):
         bO, bL = brute_attention(b.f64("q").tolist(), b.f64("shared_k").tolist(), b.f64("shared_v").tolist(),
                                  b.f64("priv_k").tolist(), b.f64("priv_v").tolist(), b.prefix_len.tolist(),
                                  b.branch_page.tolist(), b.num_new.tolist(), b.past_len.tolist(),
-                                 b.num_q_heads, b.num_kv_heads, 1.0 / math.sqrt(D))
-        err = max(err, float(np.abs(O - np.array(bO)).max()), float(np.abs(lse - np.array(bL)).max()))
+                                 b.num_q_heads, b.num_kv_heads, 1.0 / math.sqrt(D),
+                                 fork_len=_fork_list(b))
+        err = _worse(err, float(np.abs(O - np.array(bO)).max()), float(np.abs(lse - np.array(bL)).max()))
     return err
 
 
@@ -101,17 +136,18 @@ def pin_split_merge(att, plan=None, dec=None):
         s = _run(att, b, keys="shared")
         p = _run(att, b, keys="private")
         Om, lm = att.lse_merge([s, p])
-        err = max(err, float(np.abs(O - Om).max()), float(np.abs(lse - lm).max()))
+        err = _worse(err, float(np.abs(O - Om).max()), float(np.abs(lse - lm).max()))
         # merging with an empty partial (lse = -inf) is the identity
         empty = (np.full_like(O, 7.0), np.full_like(lse, -np.inf))
         Oe, le = att.lse_merge([(O, lse), empty])
-        err = max(err, float(np.abs(O - Oe).max()), float(np.abs(lse - le).max()))
+        err = _worse(err, float(np.abs(O - Oe).max()), float(np.abs(lse - le).max()))
     return err
 
 
 def _sdpa_single_branch(b, mask_bottom_right):
-    """torch fp64 SDPA over [prefix ; private] for a one-branch batch."""
-    P, L, k = int(b.prefix_len[0]), int(b.past_len[0]), int(b.num_new[0])
+    """torch fp64 SDPA over [prefix up to the fork ; private] for a one-branch batch."""
+    P = int(b.prefix_len[0]) if b.fork_len is None else int(b.fork_len[0])
+    L, k = int(b.past_len[0]), int(b.num_new[0])
     G = b.num_q_heads // b.num_kv_heads
     q = torch.from_numpy(b.f64("q")).permute(1, 0, 2)[None]            # [1, Hq, k, D]
     K = torch.from_numpy(np.concatenate([b.f64("shared_k")[:P], b.f64("priv_k")[:L + k]]))
@@ -136,7 +172,7 @@ def pin_sdpa_k1(att, plan=None, dec=None):
                   past_len=np.array([L]))
         b = attn_batch_from_structure(st, Hq, Hkv, D, "f32", seed)
         O, _ = _run(att, b)
-        err = max(err, float(np.abs(O - _sdpa_single_branch(b, False)).max()))
+        err = _worse(err, float(np.abs(O - _sdpa_single_branch(b, False)).max()))
     return err
 
 
@@ -148,7 +184,24 @@ def pin_sdpa_bottom_right(att, plan=None, dec=None):
                   past_len=np.array([L]))
         b = attn_batch_from_structure(st, Hq, Hkv, D, "f32", seed)
         O, _ = _run(att, b)
-        err = max(err, float(np.abs(O - _sdpa_single_branch(b, True)).max()))
+        err = _worse(err, float(np.abs(O - _sdpa_single_branch(b, True)).max()))
+    return err
+
+
+def pin_sdpa_fork(att, plan=None, dec=None):
+    """1 branch whose fork point cuts its page's prefix (F < P): SDPA over the
+    first F prefix rows and the private rows, bottom-right mask.  The prefix
+    rows past the fork get large keys, so seeing any of them moves O."""
+    err = 0.0
+    for (P, F, L, k, Hq, Hkv, D, seed) in [(12, 5, 3, 3, 4, 2, 8, 8), (9, 0, 2, 2, 2, 1, 4, 9),
+                                           (10, 1, 0, 4, 6, 3, 8, 10), (7, 7, 1, 2, 4, 2, 8, 11)]:
+        st = dict(prefix_len=np.array([P]), branch_page=np.array([0]), num_new=np.array([k]),
+                  past_len=np.array([L]), fork_len=np.array([F]))
+        b = attn_batch_from_structure(st, Hq, Hkv, D, "f32", seed)
+        b.shared_k = b.shared_k.copy()
+        b.shared_k[F:] *= 4.0
+        O, _ = _run(att, b)
+        err = _worse(err, float(np.abs(O - _sdpa_single_branch(b, True)).max()))
     return err
 
 
@@ -157,7 +210,7 @@ def pin_rows_sum_to_one(att, plan=None, dec=None):
     for b in tiny_batches():
         _, _, ws = _run(att, b, return_weights=True)
         for w in ws:
-            err = max(err, float(np.abs(w.sum(axis=2) - 1.0).max()))
+            err = _worse(err, float(np.abs(w.sum(axis=2) - 1.0).max()))
             if (w < 0).any():
                 return float("inf")
     return err
@@ -168,7 +221,7 @@ def pin_visible_count(att, plan=None, dec=None):
     (1, i) in shared/private position codes, O recovers the exact visible
     count F_b + L_b + j + 1 (1 / O[0] = count) and which rows were seen."""
     err = 0.0
-    for st in tiny_structures():
+    for st in tiny_structures() + fork_structures():
         Hq, Hkv, D = 4, 2, 3
         b = attn_batch_from_structure(st, Hq, Hkv, D, "f32", seed=7)
         q = np.zeros_like(b.f64("q"))
@@ -185,13 +238,13 @@ def pin_visible_count(att, plan=None, dec=None):
         t, prow, pstart = 0, 0, np.concatenate([[0], np.cumsum(st["prefix_len"])])
         for bi in range(len(st["num_new"])):
             p, k, L = int(st["branch_page"][bi]), int(st["num_new"][bi]), int(st["past_len"][bi])
-            F = int(st["prefix_len"][p])
+            F = int(st["prefix_len"][p]) if "fork_len" not in st else int(st["fork_len"][bi])
             for j in range(k):
                 n = F + L + j + 1
                 srow_sum = sum(range(int(pstart[p]) + 1, int(pstart[p]) + F + 1))
                 prow_sum = sum(range(prow + 1, prow + L + j + 2))
                 exp_row = np.array([1.0, srow_sum / n, prow_sum / n])
-                err = max(err, float(np.abs(O[t] - exp_row[None]).max()),
+                err = _worse(err, float(np.abs(O[t] - exp_row[None]).max()),
                           float(np.abs(lse[t] - math.log(n)).max()))
                 t += 1
             prow += L + k
@@ -216,7 +269,7 @@ def pin_isolation(att, plan=None, dec=None):
             t1 = t0 + int(b.num_new[victim])
             keep = np.ones(O.shape[0], bool)
             keep[t0:t1] = False
-            err = max(err, float(np.abs(O[keep] - O2[keep]).max()) if keep.any() else 0.0)
+            err = _worse(err, float(np.abs(O[keep] - O2[keep]).max()) if keep.any() else 0.0)
             if not np.abs(O[t0:t1] - O2[t0:t1]).max() > 1e-6:   # the victim itself must change
                 return float("inf")
     return err
@@ -235,11 +288,12 @@ def pin_causal_prefix(att, plan=None, dec=None):
             k, L = int(b.num_new[bi]), int(b.past_len[bi])
             for j in range(k):
                 st = dict(prefix_len=b.prefix_len, branch_page=np.array([b.branch_page[bi]]),
-                          num_new=np.array([j + 1]), past_len=np.array([L]))
+                          num_new=np.array([j + 1]), past_len=np.array([L]),
+                          fork_len=None if b.fork_len is None else np.array([b.fork_len[bi]]))
                 O1, l1 = att.attention(q[t0:t0 + j + 1], b.f64("shared_k"), b.f64("shared_v"),
                                        pk[r0:r0 + L + j + 1], pv[r0:r0 + L + j + 1], st,
                                        b.num_q_heads, b.num_kv_heads)
-                err = max(err, float(np.abs(O1[j] - O[t0 + j]).max()),
+                err = _worse(err, float(np.abs(O1[j] - O[t0 + j]).max()),
                           float(np.abs(l1[j] - lse[t0 + j]).max()))
             t0 += k
             r0 += L + k
@@ -263,21 +317,24 @@ def pin_equivariance(att, plan=None, dec=None):
             pvs.append(pv[r_start[i]:r_start[i + 1]])
             Os.append(O[t_start[i]:t_start[i + 1]])
         st = dict(prefix_len=b.prefix_len, branch_page=b.branch_page[order],
-                  num_new=b.num_new[order], past_len=b.past_len[order])
+                  num_new=b.num_new[order], past_len=b.past_len[order],
+                  fork_len=None if b.fork_len is None else b.fork_len[order])
         O2, _ = att.attention(np.concatenate(qs), b.f64("shared_k"), b.f64("shared_v"),
                               np.concatenate(pks), np.concatenate(pvs), st,
                               b.num_q_heads, b.num_kv_heads)
-        err = max(err, float(np.abs(O2 - np.concatenate(Os)).max()))
+        err = _worse(err, float(np.abs(O2 - np.concatenate(Os)).max()))
     return err
 
 
 def pin_plan_walk(att=None, plan=None, dec=None):
     """canonical_plan vs a running-counter walk over the branches."""
     err = 0
-    for st in tiny_structures() + [dict(prefix_len=np.array([4, 4]), branch_page=np.array([1, 1]),
-                                        num_new=np.array([2, 3]), past_len=np.array([0, 9]))]:
-        pl = plan.canonical_plan(st["prefix_len"], st["branch_page"], st["num_new"], st["past_len"])
-        q_row, priv_row, vis = [], [], []
+    for st in tiny_structures() + fork_structures() + [
+            dict(prefix_len=np.array([4, 4]), branch_page=np.array([1, 1]),
+                 num_new=np.array([2, 3]), past_len=np.array([0, 9]))]:
+        fork = st.get("fork_len")
+        pl = plan.canonical_plan(st["prefix_len"], st["branch_page"], st["num_new"], st["past_len"], fork)
+        q_row, priv_row, vis, forks = [], [], [], []
         tq, tr = 0, 0
         page_T = [0] * len(st["prefix_len"])
         for bi in range(len(st["num_new"])):
@@ -285,8 +342,10 @@ def pin_plan_walk(att=None, plan=None, dec=None):
             priv_row.append(tr)
             p = int(st["branch_page"][bi])
             page_T[p] += int(st["num_new"][bi])
+            F = int(st["prefix_len"][p]) if fork is None else int(fork[bi])
+            forks.append(F)
             for j in range(int(st["num_new"][bi])):
-                vis.append(int(st["prefix_len"][p]) + int(st["past_len"][bi]) + j + 1)
+                vis.append(F + int(st["past_len"][bi]) + j + 1)
             tq += int(st["num_new"][bi])
             tr += int(st["past_len"][bi]) + int(st["num_new"][bi])
         page_q, acc = [], 0
@@ -298,7 +357,8 @@ def pin_plan_walk(att=None, plan=None, dec=None):
             pre.append(acc)
             acc += int(v)
         for got, want in [(pl["q_row"], q_row), (pl["priv_row"], priv_row), (pl["visible"], vis),
-                          (pl["page_T"], page_T), (pl["page_q_row"], page_q), (pl["prefix_row"], pre)]:
+                          (pl["page_T"], page_T), (pl["page_q_row"], page_q), (pl["prefix_row"], pre),
+                          (pl["fork"], forks)]:
             if list(map(int, got)) != list(want):
                 err += 1
     return float(err)
@@ -328,7 +388,10 @@ def _textbook_decoder(inp, branch_sel=None):
     rstart = np.concatenate([[0], np.cumsum(inp.past_len + inp.num_new)])
     for bi in sel:
         p, k, L = int(inp.branch_page[bi]), int(inp.num_new[bi]), int(inp.past_len[bi])
-        P = int(inp.prefix_len[p])
+        # the branch sees its page's prefix up to its fork point, and its
+        # tokens sit at positions F + L + j of its own sequence
+        fork = getattr(inp, "fork_len", None)
+        P = int(inp.prefix_len[p]) if fork is None else int(fork[bi])
         h = torch.from_numpy(inp.hidden_in[tstart[bi]:tstart[bi] + k].astype(np.float64))
         for l in range(inp.num_layers):
             x = torch.nn.functional.rms_norm(h, (H,), eps=inp.rms_eps)
@@ -380,7 +443,7 @@ def _qwen3_library(inp, l, q, k, pos):
     return q, k
 
 
-def small_decode_inputs(seed=3, layers=2, qwen3=None):
+def small_decode_inputs(seed=3, layers=2, qwen3=None, fork=None):
     model = dict(num_layers=layers, hidden=32, intermediate=48, weight_std=0.2, rms_eps=1e-6)
     if qwen3:
         model["qwen3"] = qwen3
@@ -388,7 +451,10 @@ def small_decode_inputs(seed=3, layers=2, qwen3=None):
                      prefix=("fixed", 11), layout=dict(k=1, past=("fixed", 5)),
                      content_count=("fixed", 2), content_k=3,
                      content_past=("list", [0, 4]), model=model)
-    return make_decode_inputs(cfg, seed)
+    inp = make_decode_inputs(cfg, seed)
+    if fork is not None:
+        inp.fork_len = np.asarray(fork, np.int64)
+    return inp
 
 
 def pin_decode_textbook(att=None, plan=None, dec=None):
@@ -427,10 +493,31 @@ def pin_decode_qwen3_library(att=None, plan=None, dec=None):
     return float(np.abs(h - _textbook_decoder(inp)).max())
 
 
+def pin_decode_textbook_fork(att=None, plan=None, dec=None):
+    """Fork points 11 (the whole 11-row prefix), 0 and 6 for the layout branch
+    and the two content branches: each branch's textbook decode reads only its
+    first F_b prefix rows."""
+    inp = small_decode_inputs(fork=[11, 0, 6])
+    h, _, _ = dec.decode_step(inp)
+    return float(np.abs(h - _textbook_decoder(inp)).max())
+
+
+def pin_decode_qwen3_fork(att=None, plan=None, dec=None):
+    """The Qwen3-style step with fork points: the rotary position of token j of
+    branch b is F_b + L_b + j (its place in its own sequence), checked against
+    transformers' rotary routines at those positions."""
+    inp = small_decode_inputs(qwen3=dict(rope_theta=100.0, qk_norm=True), fork=[11, 1, 6])
+    h, _, _ = dec.decode_step(inp)
+    return float(np.abs(h - _textbook_decoder(inp)).max())
+
+
 ATTN_PINS = [pin_hand_cases, pin_brute_force, pin_split_merge, pin_sdpa_k1, pin_sdpa_bottom_right,
-             pin_rows_sum_to_one, pin_visible_count, pin_isolation, pin_causal_prefix, pin_equivariance]
+             pin_sdpa_fork, pin_rows_sum_to_one, pin_visible_count, pin_isolation, pin_causal_prefix,
+             pin_equivariance]
 PLAN_PINS = [pin_plan_walk]
-DECODE_PINS = [pin_decode_textbook, pin_decode_kv_written, pin_decode_qwen3_library]
-# the Qwen3 pin: transformers takes the rotary angles in fp32 (about 1e-7 relative)
+DECODE_PINS = [pin_decode_textbook, pin_decode_kv_written, pin_decode_qwen3_library,
+               pin_decode_textbook_fork, pin_decode_qwen3_fork]
+# the Qwen3 pins: transformers takes the rotary angles in fp32 (about 1e-7 relative)
 TOLERANCE = {pin_decode_textbook: 1e-10, pin_plan_walk: 0.0, pin_decode_kv_written: 0.0,
-             pin_decode_qwen3_library: 1e-5}
+             pin_decode_qwen3_library: 1e-5, pin_decode_textbook_fork: 1e-10,
+             pin_decode_qwen3_fork: 1e-5}

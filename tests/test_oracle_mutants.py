@@ -72,6 +72,14 @@ MUTANTS = [
                "v_new = _bf16_value(qkv[:, Hq * D:(Hq + Hkv) * D].reshape(T, Hkv, D))"),  # v := k
     ("decode", "(silu(x @ Wg.T) * (x @ Wu.T)) @ Wd.T", "(silu(x @ Wu.T) * (x @ Wg.T)) @ Wd.T"),  # gate/up swapped
     ("decode", "np.ldexp(np.rint(m * 256.0), e - 8)", "np.ldexp(np.floor(m * 256.0), e - 8)"),  # truncation
+    # fork offsets ignored somewhere on the path (a branch must see only its
+    # page's prefix up to its fork point)
+    ("attention", "F = int(plan[\"fork\"][b])", "F = int(prefix_len[p])"),
+    ("plan", "fork = np.asarray(fork_len, dtype=np.int64)", "fork = prefix_len[branch_page]"),
+    ("plan", "visible[:] = fork[token_branch] + past_len[token_branch] + token_j + 1",
+             "visible[:] = prefix_len[branch_page][token_branch] + past_len[token_branch] + token_j + 1"),
+    ("plan", "fork = np.asarray(fork_len, dtype=np.int64)", "fork = np.asarray(fork_len, dtype=np.int64) - 1"),
+    ("decode", "fork = getattr(inp, \"fork_len\", None)", "fork = None"),
 ]
 
 

@@ -183,7 +183,7 @@ def attn_batch_from_structure(structure, num_q_heads, num_kv_heads, head_dim,
                      num_new=structure["num_new"], past_len=structure["past_len"],
                      is_layout=structure.get("is_layout",
                                              np.zeros(len(structure["num_new"]), bool)),
-                     **vals)
+                     fork_len=structure.get("fork_len"), **vals)
 
 
 def draw_fork_len(structure, visual, rng):
