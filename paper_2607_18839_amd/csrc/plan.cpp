@@ -201,9 +201,16 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
            ceil_div(P.prefix_len[p], split);
     return n;
   };
+  // Grow the split until the items fit the target or one split covers every
+  // page's whole prefix: with many pages, kv heads and row groups even one
+  // split per page can exceed the target, and longer splits then change
+  // nothing.
+  int64_t max_prefix = 0;
+  for (int p = 0; p < np; ++p) max_prefix = std::max<int64_t>(max_prefix, P.prefix_len[p]);
+  const int64_t mult_cap = std::max<int64_t>(1, ceil_div(max_prefix, kSharedSplitUnit));
   int64_t units = shared_items_for(kSharedSplitUnit);
-  int64_t mult = std::max<int64_t>(1, ceil_div(units, kSharedTargetItems));
-  while (shared_items_for(kSharedSplitUnit * mult) > kSharedTargetItems) ++mult;   // ceilings per page
+  int64_t mult = std::min(mult_cap, std::max<int64_t>(1, ceil_div(units, kSharedTargetItems)));
+  while (mult < mult_cap && shared_items_for(kSharedSplitUnit * mult) > kSharedTargetItems) ++mult;   // ceilings per page
   // (paged K/V: at most 64 tiles per item, each item's tile rows fit a wave)
   P.split_keys = (int32_t)std::min<int64_t>(kSharedSplitUnit * mult, b.paged ? 4096 : INT32_MAX / 2);
   // each page's prefix is cut into page_splits[p] ranges of equal length

@@ -252,6 +252,34 @@ def test_fork_work_lists_cover_visible_keys_once(name, st, Hq, Hkv):
     assert np.all(slot_writes == 1)
 
 
+@pytest.mark.timeout(60)
+def test_plan_with_more_row_groups_than_the_item_target():
+    """48 pages x 33 branches: even one key split per page gives 864 shared
+    items, more than the planner's target of about one per CU, so growing the
+    split cannot reach the target.  The planner must stop at one split per
+    page (it once looped forever here) and still cover every (page, kv
+    head, row group) prefix range [0, P_p) exactly once."""
+    npg, nbr, G = 48, 33, 8
+    rng = np.random.default_rng(3)
+    st = dict(prefix_len=rng.integers(1024, 4097, npg).astype(np.int32),
+              branch_page=np.repeat(np.arange(npg), nbr).astype(np.int32),
+              num_new=np.tile([1] + [4] * (nbr - 1), npg).astype(np.int32),
+              past_len=rng.integers(0, 300, npg * nbr).astype(np.int32))
+    info = _lib.hpd_plan_query(_plan(st))
+    S = _lib.SI
+    spans = {}
+    for it in info["shared_items"]:
+        key = (it[S["page"]], it[S["kvh"]], it[S["row0"]])
+        spans.setdefault(key, []).append((it[S["key0"]], it[S["key1"]]))
+    page_T = np.bincount(st["branch_page"], weights=st["num_new"], minlength=npg).astype(int)
+    assert len(spans) == sum(2 * -(-int(T) * G // 128) for T in page_T)
+    for (p, g, r0), iv in spans.items():
+        iv.sort()
+        assert iv[0][0] == 0 and iv[-1][1] == st["prefix_len"][p]
+        assert all(a[1] == b[0] for a, b in zip(iv, iv[1:])), (p, g, r0, iv)
+    assert len(info["shared_items"]) == len(spans)    # one split per page
+
+
 def test_embed_and_pmtp_entry_points_validate_before_launching(lib):
     """hpd_embed_tokens and hpd_verify_draft_step reject bad arguments on the
     host, before any launch (fake device addresses are never touched)."""
