@@ -60,3 +60,26 @@ def assert_parity(got, want, dtype, what=""):
         assert mx <= F32_MAX_ABS and rl <= F32_REL_L2, f"{what}: max abs {mx:.3e}, rel L2 {rl:.3e}"
     assert np.all(np.isfinite(got)), f"{what}: non-finite output"
     return mx, rl
+
+
+def bf16_value(bits):
+    return (np.asarray(bits, np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def assert_cache_rows(got_bits, want_bits, what=""):
+    """Appended K/V rows against the oracle's bf16 rows.
+
+    Both sides round a projection to bf16.  The GPU's fp32 projection of a
+    bf16-rounded input differs from the oracle's fp64 one by about 1e-3 of
+    the value, so the two roundings agree or land on neighbouring bf16
+    values: the bar is one bf16 ulp at the largest magnitude present,
+    2^(floor(log2 max|v|) - 7), and rel L2 <= 5e-3 over the rows.
+    """
+    got, want = bf16_value(got_bits), bf16_value(want_bits)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite cache row (a slot was not written)"
+    top = float(np.abs(want).max())
+    bar = 2.0 ** (np.floor(np.log2(top)) - 7) if top > 0 else 0.0
+    mx, rl = errors(got, want)
+    assert mx <= bar and rl <= BF16_REL_L2, f"{what}: max abs {mx:.3e} (bar {bar:.3e}), rel L2 {rl:.3e}"
+    return mx, rl, float(np.mean(got_bits != want_bits))
+

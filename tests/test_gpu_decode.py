@@ -4,11 +4,12 @@ import numpy as np
 import pytest
 import torch
 
+import functools
+
 from oracle.decode import decode_step
 from workloads import get_config, make_decode_inputs
-from workloads.gen import DecodeInputs
 
-from ._gpu import BF16_MAX_ABS, BF16_REL_L2, announce, errors, to_dev
+from ._gpu import BF16_MAX_ABS, BF16_REL_L2, announce, assert_cache_rows, errors, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -57,18 +58,27 @@ def small_inputs(seed, layers=2):
 
 
 def _check_cache(inp, pk, pv, nk, nv):
-    """New rows match the oracle's bf16 K/V within the parity bar; every
-    other row is bit-identical to the input."""
+    """New rows match the oracle's bf16 K/V (one bf16 ulp, see
+    assert_cache_rows); every other row is bit-identical to the input.
+    Returns the largest fraction of appended values whose bits differ."""
     starts = np.concatenate([[0], np.cumsum(inp.past_len + inp.num_new)[:-1]])
     dest = np.concatenate([np.arange(r + L, r + L + k) for r, L, k in zip(starts, inp.past_len, inp.num_new)])
     keep = np.ones(pk[0].shape[0], bool)
     keep[dest] = False
-    val = lambda b: (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    flips = 0.0
     for l in range(inp.num_layers):
         assert np.array_equal(pk[l][keep], inp.priv_k[l][keep]) and np.array_equal(pv[l][keep], inp.priv_v[l][keep])
-        for got, want in ((pk[l][dest], nk[l]), (pv[l][dest], nv[l])):
-            mx, rl = errors(val(got), val(want))
-            assert mx <= BF16_MAX_ABS * 5 and rl <= BF16_REL_L2, f"layer {l} cache rows: {mx:.3e} {rl:.3e}"
+        for nm, got, want in (("k", pk[l][dest], nk[l]), ("v", pv[l][dest], nv[l])):
+            flips = max(flips, assert_cache_rows(got, want, f"layer {l} cache {nm} rows")[2])
+    return flips
+
+
+@functools.lru_cache(maxsize=1)
+def c4_reference():
+    """The c4 inputs (seed 0) and the oracle's whole step on them, computed
+    once per test session (about 10-40 s of fp64 on the host)."""
+    inp = make_decode_inputs("c4", 0)
+    return inp, decode_step(inp)
 
 
 @pytest.mark.parametrize("packed", [False, True], ids=["torch", "packed"])
@@ -85,41 +95,20 @@ def test_small_stack(seed, packed):
     _check_cache(inp, pk, pv, nk, nv)
 
 
-def _sub_batch(inp, branches):
-    """Inputs restricted to some branches of the page (their outputs depend on
-    nothing else: context isolation)."""
-    starts_t = np.concatenate([[0], np.cumsum(inp.num_new)])
-    starts_r = np.concatenate([[0], np.cumsum(inp.past_len + inp.num_new)])
-    tok = np.concatenate([np.arange(starts_t[b], starts_t[b + 1]) for b in branches])
-    rows = np.concatenate([np.arange(starts_r[b], starts_r[b + 1]) for b in branches])
-    sub = DecodeInputs(name=inp.name + "-sub", seed=inp.seed, num_q_heads=inp.num_q_heads,
-                       num_kv_heads=inp.num_kv_heads, head_dim=inp.head_dim, num_layers=inp.num_layers,
-                       hidden=inp.hidden, intermediate=inp.intermediate, rms_eps=inp.rms_eps,
-                       prefix_len=inp.prefix_len, branch_page=inp.branch_page[branches],
-                       num_new=inp.num_new[branches], past_len=inp.past_len[branches],
-                       is_layout=inp.is_layout[branches], hidden_in=inp.hidden_in[tok],
-                       shared_k=inp.shared_k, shared_v=inp.shared_v,
-                       priv_k=[a[rows] for a in inp.priv_k], priv_v=[a[rows] for a in inp.priv_v],
-                       w_qkv=inp.w_qkv, w_o=inp.w_o, w_gate=inp.w_gate, w_up=inp.w_up, w_down=inp.w_down)
-    return sub, tok
-
-
-@pytest.mark.parametrize("packed", [False, True], ids=["torch", "packed"])
-def test_full_c4_sampled_branches(packed):
+@pytest.mark.parametrize("packed", [True, False], ids=["packed", "torch"])
+def test_full_c4_all_branches(packed):
     """c4 at full size (18 layers, 33 branches, 4096-token prefix); with
-    packed weights this is the configuration the benchmark times.  The
-    oracle recomputes 3 sampled branches (layout, the longest and one more
-    content branch) on their own."""
-    announce(f"decode c4 full, sampled branches, packed {packed}")
-    inp = make_decode_inputs("c4", 0)
-    h, pk, pv = run_decode(inp, canary=False, packed=packed)
-    longest = int(np.argmax(np.where(inp.is_layout, -1, inp.past_len)))
-    sample = sorted({0, longest, 7})
-    sub, tok = _sub_batch(inp, sample)
-    ref, _, _ = decode_step(sub)
-    mx, rl = errors(h[tok], ref)
-    print(f"c4 sampled branches {sample}: max abs {mx:.3e} rel L2 {rl:.3e}")
+    packed weights this is the configuration the benchmark times.  Every
+    branch's output and every appended K/V row of every layer (NaN canaries
+    in the slots the step must fill) against the oracle's whole step."""
+    announce(f"decode c4 full, all branches and cache rows, packed {packed}")
+    inp, (ref, nk, nv) = c4_reference()
+    h, pk, pv = run_decode(inp, canary=True, packed=packed)
     assert np.all(np.isfinite(h))
+    mx, rl = errors(h, ref)
+    flips = _check_cache(inp, pk, pv, nk, nv)
+    print(f"c4 all 33 branches, packed {packed}: max abs {mx:.3e} rel L2 {rl:.3e}; "
+          f"cache rows: at most {100 * flips:.2f}% of values one bf16 ulp off")
     assert mx <= BF16_MAX_ABS and rl <= BF16_REL_L2, (mx, rl)
 
 
