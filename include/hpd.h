@@ -184,6 +184,26 @@ hpd_status hpd_branch_attn_step(const hpd_plan *plan, const void *q, const void 
                                 void *out, float *lse, void *workspace, size_t workspace_bytes,
                                 void *stream);
 
+/* hpd_branch_attn_step for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): no workspace argument and no allocation.  The step's scratch
+ * (the plan's tables, then the partial softmax results) lives in a static
+ * array of HPD_NOALLOC_SCRATCH_BYTES inside the library, one per GPU, held
+ * until the process ends; each call copies the plan's tables into it
+ * (stream-ordered, from the plan's host memory) and runs the same kernels
+ * as hpd_branch_attn_step, so the results are bit-identical to it.  No
+ * hpd_plan_upload is needed.
+ * Plans whose hpd_plan_workspace_bytes exceed HPD_NOALLOC_SCRATCH_BYTES
+ * return HPD_ERR_WORKSPACE_TOO_SMALL before anything is enqueued.
+ * All calls on one GPU share its array and the array keeps the last call's
+ * contents: calls that may overlap on one GPU (different streams, or
+ * different host threads without ordering) race; serialise them on one
+ * stream.  Other arguments and errors as hpd_branch_attn_step. */
+#define HPD_NOALLOC_SCRATCH_BYTES (32u << 20)
+hpd_status hpd_branch_attn_step_noalloc(const hpd_plan *plan, const void *q, const void *shared_k,
+                                        const void *shared_v, const void *priv_k, const void *priv_v,
+                                        void *out, float *lse, void *stream);
+
 /* The synthetic decoder stack (pre-norm GQA transformer with RMSNorm and a
  * SwiGLU MLP, section "Overview", paragraph "LLM Decoder").  Weights are bf16
  * device arrays in torch Linear layout W[out][in]; each field points to a

@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(_HERE, "libhpd.so")
 
 HPD_MAX_K = 16
 HPD_HEAD_DIM = 64
+HPD_NOALLOC_SCRATCH_BYTES = 32 << 20   # static scratch of hpd_branch_attn_step_noalloc
 HPD_F32, HPD_BF16 = 0, 1
 STATUS = {0: "HPD_OK", 1: "HPD_ERR_INVALID_ARGUMENT", 2: "HPD_ERR_UNSUPPORTED",
           3: "HPD_ERR_WORKSPACE_TOO_SMALL", 4: "HPD_ERR_HIP", 5: "HPD_ERR_HOST_ALLOC",
@@ -122,6 +123,7 @@ SIGNATURES = {
                                            ctypes.c_void_p]),
     "hpd_pack_gate_up": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                         ctypes.c_void_p, ctypes.c_void_p]),
+    "hpd_branch_attn_step_noalloc": (ctypes.c_int, [ctypes.c_void_p] * 8 + [ctypes.c_void_p]),
     "hpd_kernel_timing": (ctypes.c_int, [ctypes.c_int, ctypes.c_int]),
     "hpd_attn_phase_isolation": (ctypes.c_int, [ctypes.c_int]),
     "hpd_pmtp_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(hpd_model_desc), ctypes.POINTER(hpd_pmtp_desc),
@@ -268,6 +270,11 @@ def hpd_branch_attn_step(plan, q, shared_k, shared_v, priv_k, priv_v, out, lse, 
                          workspace_bytes, stream=None):
     _check(load().hpd_branch_attn_step(plan.handle, q, shared_k, shared_v, priv_k, priv_v, out, lse,
                                        workspace, workspace_bytes, stream), "hpd_branch_attn_step")
+
+
+def hpd_branch_attn_step_noalloc(plan, q, shared_k, shared_v, priv_k, priv_v, out, lse, stream=None):
+    _check(load().hpd_branch_attn_step_noalloc(plan.handle, q, shared_k, shared_v, priv_k, priv_v, out, lse,
+                                               stream), "hpd_branch_attn_step_noalloc")
 
 
 def _ptr_array(ptrs):

@@ -4,6 +4,7 @@
 
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 
@@ -26,6 +27,57 @@ hpd_status hip_err(hipError_t e, const char *where) {
 }
 
 bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
+
+}  // namespace
+
+// Scratch memory of hpd_branch_attn_step_noalloc: plan tables, then the
+// partial softmax results.  Each GPU holds its own copy until the process
+// ends.  In host code this name is only a stand-in for the symbol: the
+// device address comes from hipGetSymbolAddress, once per device.
+__device__ __align__(256) unsigned char scratch[HPD_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch` (looked up on the first call on
+// that device, with that device current).
+hpd_status scratch_address(const char *fn, void **out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_err(e, fn);
+  if (dev < 0 || dev >= kMaxDevices)
+    return set_err(HPD_ERR_UNSUPPORTED, std::string(fn) + ": device id out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_err(e, "hipGetSymbolAddress(scratch)");
+    if (!p || !aligned(p, 256))
+      return set_err(HPD_ERR_HIP, std::string(fn) + ": scratch symbol has no usable device address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return HPD_OK;
+}
+
+// Checks shared by both attention entry points; nothing is launched before
+// they pass.
+hpd_status check_attn_tensors(const char *fn, const hpd_plan *plan, const void *q, const void *shared_k,
+                              const void *shared_v, const void *priv_k, const void *priv_v, const void *out,
+                              const float *lse) {
+  const std::string f(fn);
+  if (!plan) return set_err(HPD_ERR_INVALID_ARGUMENT, f + ": plan is NULL");
+  if (!q || !priv_k || !priv_v || !out) return set_err(HPD_ERR_INVALID_ARGUMENT, f + ": NULL tensor");
+  if (plan->p.shared_rows > 0 && (!shared_k || !shared_v))
+    return set_err(HPD_ERR_INVALID_ARGUMENT, f + ": shared_k/v NULL with a non-empty prefix");
+  if (!aligned(q, 16) || !aligned(priv_k, 16) || !aligned(priv_v, 16) || !aligned(out, 16) ||
+      (shared_k && !aligned(shared_k, 16)) || (shared_v && !aligned(shared_v, 16)) || (lse && !aligned(lse, 4)))
+    return set_err(HPD_ERR_INVALID_ARGUMENT, f + ": tensors must be 16-byte aligned");
+  return HPD_OK;
+}
 
 }  // namespace
 
@@ -115,16 +167,10 @@ hpd_status hpd_branch_attn_step(const hpd_plan *plan, const void *q, const void 
                                 const void *shared_v, const void *priv_k, const void *priv_v,
                                 void *out, float *lse, void *workspace, size_t workspace_bytes,
                                 void *stream) {
-  if (!plan) return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_branch_attn_step: plan is NULL");
+  hpd_status st = check_attn_tensors("hpd_branch_attn_step", plan, q, shared_k, shared_v, priv_k, priv_v, out, lse);
+  if (st != HPD_OK) return st;
   const hpd::Plan &P = plan->p;
-  if (!q || !priv_k || !priv_v || !out || !workspace)
-    return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_branch_attn_step: NULL tensor or workspace");
-  if (P.shared_rows > 0 && (!shared_k || !shared_v))
-    return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_branch_attn_step: shared_k/v NULL with a non-empty prefix");
-  if (!aligned(q, 16) || !aligned(priv_k, 16) || !aligned(priv_v, 16) || !aligned(out, 16) ||
-      (shared_k && !aligned(shared_k, 16)) || (shared_v && !aligned(shared_v, 16)) ||
-      (lse && !aligned(lse, 4)))
-    return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_branch_attn_step: tensors must be 16-byte aligned");
+  if (!workspace) return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_branch_attn_step: NULL workspace");
   if (!aligned(workspace, 256))
     return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_branch_attn_step: workspace must be 256-byte aligned");
   if (workspace_bytes < P.workspace_bytes)
@@ -132,6 +178,33 @@ hpd_status hpd_branch_attn_step(const hpd_plan *plan, const void *q, const void 
   hipError_t e = hpd::launch_branch_attention(P, q, shared_k, shared_v, priv_k, priv_v, out, lse,
                                               workspace, (hipStream_t)stream);
   if (e != hipSuccess) return hip_err(e, "hpd_branch_attn_step");
+  return HPD_OK;
+}
+
+hpd_status hpd_branch_attn_step_noalloc(const hpd_plan *plan, const void *q, const void *shared_k,
+                                        const void *shared_v, const void *priv_k, const void *priv_v,
+                                        void *out, float *lse, void *stream) {
+  static const char *fn = "hpd_branch_attn_step_noalloc";
+  hpd_status st = check_attn_tensors(fn, plan, q, shared_k, shared_v, priv_k, priv_v, out, lse);
+  if (st != HPD_OK) return st;
+  const hpd::Plan &P = plan->p;
+  if (P.workspace_bytes > (size_t)HPD_NOALLOC_SCRATCH_BYTES)
+    return set_err(HPD_ERR_WORKSPACE_TOO_SMALL,
+                   std::string(fn) + ": the plan needs " + std::to_string(P.workspace_bytes) +
+                       " bytes of scratch, more than the library's static " +
+                       std::to_string((size_t)HPD_NOALLOC_SCRATCH_BYTES) + " (use hpd_branch_attn_step)");
+  void *ws = nullptr;
+  st = scratch_address(fn, &ws);
+  if (st != HPD_OK) return st;
+  // The plan's tables go into this device's scratch first (stream-ordered
+  // before the kernels that read them); the partials behind them are written
+  // by the kernels before they are read, so nothing needs clearing.
+  hipError_t e = hipSuccess;
+  if (P.table_bytes > 0)
+    e = hipMemcpyAsync(ws, P.table_image.data(), P.table_bytes, hipMemcpyHostToDevice, (hipStream_t)stream);
+  if (e == hipSuccess)
+    e = hpd::launch_branch_attention(P, q, shared_k, shared_v, priv_k, priv_v, out, lse, ws, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_err(e, fn);
   return HPD_OK;
 }
 
