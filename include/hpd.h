@@ -298,7 +298,16 @@ size_t hpd_decode_workspace_bytes(const hpd_model_desc *model, const hpd_plan *p
  * input norm enter their products as bf16; the MLP projections run in fp16
  * (the bf16 weights convert exactly, the MLP input norm and the SwiGLU
  * product are rounded to fp16); all accumulation and the residual stream in
- * fp32. */
+ * fp32.
+ * fp16 range: the MLP input is written as h * gamma_mlp * s_t, with s_t the
+ * power of two at or below the token's attention-norm factor
+ * 1 / RMS(h before the attention); the gate/up projection divides by s_t
+ * (both exact).  Since |h_i| <= sqrt(hidden) * RMS(h), an element stays
+ * below fp16's 65504 while |gamma_mlp_i| * RMS(h after the attention) /
+ * RMS(h before) < 65504 / (2 sqrt(hidden)) (1023 at hidden 1024), whatever
+ * the scale of h.  The SwiGLU product silu(x W_gate^T) * (x W_up^T) of the
+ * normalised input must itself stay below 65504 in magnitude.  Past either
+ * bound the step's outputs become inf or NaN (no error is returned). */
 hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan,
                            const float *hidden_in, float *hidden_out,
                            const void *const *shared_k, const void *const *shared_v,

@@ -13,7 +13,9 @@
 //     the Qwen3-style QK norm and rotary embedding of q and the new k rows)
 //   2 branch attention (one launch for the shared-prefix and private work
 //     items, then the merge) -> a (bf16)
-//   3 O GEMM: h += a W_o^T; x = h * gamma_mlp (fp16), sums of squares
+//   3 O GEMM: h += a W_o^T; x = h * gamma_mlp * s (fp16, s the power of two
+//     of the attention norm's factor of the token, undone by the next GEMM),
+//     sums of squares
 //   4 gate/up GEMM (fp16), SwiGLU -> m (fp16)
 //   5 down GEMM (fp16): h += m W_down^T; x = h * gamma_attn[l + 1] (bf16),
 //     sums of squares (not after the last layer)
@@ -44,7 +46,7 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 struct DecodeLayout {
   int T, Tpad, H, I, nq, nkv;
   int rg_qkv, rg_o, rg_gu, rg_down;
-  size_t off_x, off_q, off_attn, off_m, off_ss, bytes;
+  size_t off_x, off_q, off_attn, off_m, off_ss, off_ss_mlp, off_scale, bytes;
 };
 
 DecodeLayout decode_layout(const hpd_model_desc &m, const Plan &P) {
@@ -70,6 +72,8 @@ DecodeLayout decode_layout(const hpd_model_desc &m, const Plan &P) {
   L.off_attn = take((size_t)L.Tpad * L.nq * 2);
   L.off_m = take((size_t)L.Tpad * L.I * 2);
   L.off_ss = take((size_t)L.Tpad * (L.H / kGemmTile) * sizeof(float));
+  L.off_ss_mlp = take((size_t)L.Tpad * (L.H / kGemmTile) * sizeof(float));
+  L.off_scale = take((size_t)L.Tpad * sizeof(float));
   L.bytes = off;
   return L;
 }
@@ -221,7 +225,10 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
   __bf16 *x = (__bf16 *)(ws + L.off_x);   // x = h * gamma: bf16 (attention input) or fp16 (MLP input)
   __bf16 *q = (__bf16 *)(ws + L.off_q), *attn = (__bf16 *)(ws + L.off_attn);
   __bf16 *mlp = (__bf16 *)(ws + L.off_m);   // SwiGLU product, fp16 bits
-  float *ss = (float *)(ws + L.off_ss);     // sums of squares of h per 32 columns
+  // sums of squares of h per 32 columns: at the attention norm's input and at
+  // the MLP norm's input
+  float *ss = (float *)(ws + L.off_ss), *ss_mlp = (float *)(ws + L.off_ss_mlp);
+  float *scale = (float *)(ws + L.off_scale);   // per token: power of two of the attention norm factor
   const hpd::PlanDev dev = hpd::plan_dev(P, workspace);
   float *h = hidden_out;
   // packed weights: every activation buffer (x, attn, m) is kept in the packed
@@ -261,6 +268,7 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
     g.v_cache = (__bf16 *)priv_v[l];
     g.n_kv = L.nkv;
     g.dest = dev.token_dest;
+    g.scale_out = scale;
     e = hpd::launch_gemm(g, false, hpd::kEpiQKV, hpd::KK_GEMM_QKV, stream);
     if (e != hipSuccess) break;
     if (qwen3) {   // 1b: QK norm and rotary embedding of q and the new k rows
@@ -274,18 +282,22 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
     e = hpd::launch_branch_attention(P, q, shared_k ? shared_k[l] : nullptr, shared_v ? shared_v[l] : nullptr,
                                      priv_k[l], priv_v[l], attn, nullptr, workspace, stream, packed);
     if (e != hipSuccess) break;
-    // 3: O projection into h; MLP norm input (fp16)
+    // 3: O projection into h; MLP norm input (fp16), scaled by the power of
+    // two of the attention norm's factor so that it stays in fp16's range
     g = base(L.rg_o, attn, L.H, L.nq);
     g.w0 = (const __bf16 *)m.w_o[l];
     g.h = h;
     g.x_out = x;
     g.x_out_f16 = true;
     g.gamma = gamma(m.g_mlp_norm, l);
-    g.ss_out = ss;
+    g.ss_out = ss_mlp;
+    g.scale_in = scale;
     e = hpd::launch_gemm(g, false, hpd::kEpiResidual, hpd::KK_GEMM_O, stream);
     if (e != hipSuccess) break;
     // 4: gate/up projection, SwiGLU (fp16)
     g = base(L.rg_gu, x, 2 * L.I, L.H);
+    g.ss_in = ss_mlp;
+    g.scale_in = scale;
     g.w0 = (const __bf16 *)m.w_gate[l];   // packed: the interleaved gate/up pair
     g.w1 = packed ? nullptr : (const __bf16 *)m.w_up[l];
     g.m_out = mlp;

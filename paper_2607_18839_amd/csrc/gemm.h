@@ -36,6 +36,12 @@ struct GemmArgs {
   int T, Tpad;
   // QKV / SwiGLU: per-token norm factor from ss_in [Tpad][n_ss] (sum / H + eps)
   const float *ss_in; int n_ss; float inv_H, eps;
+  // fp16 norm inputs: a per-token power of two s_t [T] (pow2_scale of a norm
+  // factor).  The residual epilogue writes x_out = h * gamma * s_t; the
+  // SwiGLU epilogue divides its products by s_t.  NULL = no scaling.
+  const float *scale_in;
+  // QKV epilogue: writes s_t = pow2_scale(its RMSNorm factor) [T] (NULL = not)
+  float *scale_out;
   // QKV epilogue
   __bf16 *q_out; int n_q;                   // q[t][0..n_q)
   __bf16 *k_cache, *v_cache; int n_kv;      // cache rows dest[t]
@@ -65,6 +71,17 @@ __device__ __forceinline__ uint64_t argmax_key(float v, int id) {
   return ((uint64_t)u << 32) | (uint32_t)(0xFFFFFFFFu - (uint32_t)id);
 }
 __device__ __forceinline__ int argmax_id(uint64_t key) { return (int)(0xFFFFFFFFu - (uint32_t)key); }
+
+// The power of two s <= inv (an RMSNorm factor), clamped to [2^-100,
+// 2^100].  An fp16 norm input x = h * gamma is written as x * s with s from
+// the token's previous norm factor, which brings the row near unit scale so
+// that a large residual stream does not overflow fp16 (65504); its consumer
+// divides by the same s.  s is a power of two, so both scalings are exact.
+__device__ __forceinline__ float pow2_scale(float inv) {
+  if (!(inv >= 0x1p-100f)) return inv > 0x1p100f ? 0x1p100f : 0x1p-100f;   // NaN too
+  if (inv > 0x1p100f) return 0x1p100f;
+  return __uint_as_float(__float_as_uint(inv) & 0x7f800000u);
+}
 
 // Start of a step: h = h_in (if different), x = h * gamma, ss, and zero rows
 // T..Tpad-1 of x and of `zero_rows` ([Tpad][zero_cols]).

@@ -69,11 +69,15 @@ struct EpilogueIn {
   f32x4 h[4], gamma[4];   // residual: h row slice and gamma (ones if none)
   int dest;               // QKV: private cache row of the token
   float inv_rms;          // QKV, SwiGLU: RMSNorm factor of the token
+  float scale;            // residual, SwiGLU: s_t of the fp16 norm input (scale_in), else 1
 };
 
+// Loaded before the main loop: plan data and the per-token scale, which were
+// written at least two launches earlier.
 template <int EPI>
 __device__ __forceinline__ void load_early(const GemmArgs &g, int t, EpilogueIn &in) {
   if constexpr (EPI == kEpiQKV) in.dest = t < g.T ? g.dest[t] : 0;
+  else in.scale = g.scale_in ? g.scale_in[min(t, g.T - 1)] : 1.f;
 }
 
 template <int EPI>
@@ -130,7 +134,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs &g, const f32x16 &acc, E
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int n = tile * kGemmTile + 8 * i + 4 * half;
-      const f32x4 v = in.h[i] * in.gamma[i];
+      const f32x4 v = in.h[i] * in.gamma[i] * in.scale;
       const int64_t off = g.act_packed ? packed_offset(t, n, g.N) : (int64_t)t * g.N + n;
       if (g.x_out_f16) {
         f16x4 o;
@@ -158,13 +162,15 @@ __device__ __forceinline__ void epilogue(const GemmArgs &g, const f32x16 &acc, E
         else if (n < g.n_q + g.n_kv) *(bf16x4 *)(g.k_cache + (int64_t)in.dest * g.n_kv + (n - g.n_q)) = v;
         else *(bf16x4 *)(g.v_cache + (int64_t)in.dest * g.n_kv + (n - g.n_q - g.n_kv)) = v;
       }
+      if (g.scale_out && tile == 0 && half == 0) g.scale_out[t] = pow2_scale(inv_rms);
     } else {   // SwiGLU: m = silu(gate) * up, fp16; rows t >= T are written as zeros
+      const float f = inv_rms / in.scale;   // exact: s_t is a power of two
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         f16x4 mv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float gt = acc[4 * i + r] * inv_rms, up = acc[4 * i + 8 + r] * inv_rms;
+          const float gt = acc[4 * i + r] * f, up = acc[4 * i + 8 + r] * f;
           mv[r] = (_Float16)(t < g.T ? gt / (1.0f + __expf(-gt)) * up : 0.f);
         }
         const int col = tile * 16 + 8 * i + 4 * half;

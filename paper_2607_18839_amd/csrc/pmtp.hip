@@ -33,8 +33,8 @@ int round32(int x) { return (x + kGemmTile - 1) / kGemmTile * kGemmTile; }
 
 struct PmtpLayout {
   int T, Tpad, nb, nbpad, H, V, Id, kmax, ntile;
-  size_t off_x_lm, off_ss_lm, off_amax_v, off_f, off_x_d, off_ss_d, off_m_d, off_x_f, off_ss_f, off_amax_d,
-      off_tok, bytes;
+  size_t off_x_lm, off_ss_lm, off_amax_v, off_f, off_x_d, off_ss_d, off_scale_d, off_m_d, off_x_f, off_ss_f,
+      off_amax_d, off_tok, bytes;
 };
 
 PmtpLayout pmtp_layout(const hpd_model_desc &m, const hpd_pmtp_desc &d, const Plan &P) {
@@ -60,6 +60,7 @@ PmtpLayout pmtp_layout(const hpd_model_desc &m, const hpd_pmtp_desc &d, const Pl
   L.off_f = take((size_t)L.nbpad * L.H * 4);
   L.off_x_d = take((size_t)L.nbpad * 2 * L.H * 2);
   L.off_ss_d = take((size_t)L.nbpad * (2 * L.H / kGemmTile) * 4);
+  L.off_scale_d = take((size_t)L.nbpad * 4);
   L.off_m_d = take((size_t)L.nbpad * L.Id * 2);
   L.off_x_f = take((size_t)L.nbpad * L.H * 2);
   L.off_ss_f = take((size_t)L.nbpad * (L.H / kGemmTile) * 4);
@@ -149,9 +150,9 @@ __global__ __launch_bounds__(256) void verify_kernel(PlanDev dev, int nb, int nt
 // fp16 draft MLP, with the sums of squares over each 32 columns.  Padding
 // rows are zero.
 __global__ __launch_bounds__(256) void draft_input_kernel(int it, int nb, int ntile, const uint64_t *amax,
-                                                          const __bf16 *embed, const float *f, int H,
-                                                          __bf16 *x_d, float *ss_d, int32_t *cur_tok,
-                                                          int32_t *draft_out) {
+                                                          const __bf16 *embed, const float *f, int H, float eps,
+                                                          __bf16 *x_d, float *ss_d, float *scale_d,
+                                                          int32_t *cur_tok, int32_t *draft_out) {
   typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
   typedef float f32x4 __attribute__((ext_vector_type(4)));
   __shared__ uint64_t sh[4];
@@ -169,26 +170,35 @@ __global__ __launch_bounds__(256) void draft_input_kernel(int it, int nb, int nt
   __syncthreads();
   if (threadIdx.x == 0) tok_sh = real ? cur_tok[b] : 0;
   __syncthreads();
-  const int tok = tok_sh, W = 2 * H;
+  const int tok = tok_sh, W = 2 * H, n_ss = W / kGemmTile;
+  auto value = [&](int c) -> f32x4 {
+    if (!real) return f32x4{0.f, 0.f, 0.f, 0.f};
+    if (c < H) return *(const f32x4 *)(f + (int64_t)b * H + c);
+    const bf16x4 e = *(const bf16x4 *)(embed + (int64_t)tok * H + (c - H));
+    return f32x4{(float)e[0], (float)e[1], (float)e[2], (float)e[3]};
+  };
+  // pass 1: sums of squares per 32-column tile
   for (int c = 4 * threadIdx.x; c < W; c += 1024) {
-    f32x4 v = {0.f, 0.f, 0.f, 0.f};
-    if (real) {
-      if (c < H) {
-        v = *(const f32x4 *)(f + (int64_t)b * H + c);
-      } else {
-        const bf16x4 e = *(const bf16x4 *)(embed + (int64_t)tok * H + (c - H));
-        v = f32x4{(float)e[0], (float)e[1], (float)e[2], (float)e[3]};
-      }
-    }
+    const f32x4 v = value(c);
     float sq = fmaf(v[0], v[0], fmaf(v[1], v[1], fmaf(v[2], v[2], v[3] * v[3])));
     sq += __shfl_xor(sq, 1);   // 8 consecutive threads cover one 32-column tile
     sq += __shfl_xor(sq, 2);
     sq += __shfl_xor(sq, 4);
-    if ((threadIdx.x & 7) == 0) ss_d[(int64_t)b * (W / kGemmTile) + c / kGemmTile] = sq;
+    if ((threadIdx.x & 7) == 0) ss_d[(int64_t)b * n_ss + c / kGemmTile] = sq;
+  }
+  __syncthreads();   // the row's sums, written by the whole workgroup, are visible to it
+  // pass 2: the row as fp16, scaled by the power of two of its norm factor,
+  // which the SwiGLU GEMM divides back out
+  float sum = 0.f;
+  for (int i = 0; i < n_ss; ++i) sum += ss_d[(int64_t)b * n_ss + i];
+  const float s = pow2_scale(1.0f / sqrtf(sum / (float)W + eps));
+  if (threadIdx.x == 0) scale_d[b] = s;
+  for (int c = 4 * threadIdx.x; c < W; c += 1024) {
+    const f32x4 v = value(c);
     typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
     f16x4 o;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) o[r] = (_Float16)v[r];
+    for (int r = 0; r < 4; ++r) o[r] = (_Float16)(v[r] * s);
     *(f16x4 *)((_Float16 *)x_d + packed_offset(b, c, W)) = o;
   }
 }
@@ -301,6 +311,7 @@ hpd_status hpd_verify_draft_step(const hpd_model_desc *model, const hpd_pmtp_des
   float *f = (float *)(ws + L.off_f);
   __bf16 *x_d = (__bf16 *)(ws + L.off_x_d), *m_d = (__bf16 *)(ws + L.off_m_d), *x_f = (__bf16 *)(ws + L.off_x_f);
   float *ss_d = (float *)(ws + L.off_ss_d), *ss_f = (float *)(ws + L.off_ss_f);
+  float *scale_d = (float *)(ws + L.off_scale_d);   // per branch: the draft input's power-of-two prescale
   int32_t *tok = (int32_t *)(ws + L.off_tok);
   const __bf16 *g_final = (const __bf16 *)pmtp->g_final;
 
@@ -332,7 +343,8 @@ hpd_status hpd_verify_draft_step(const hpd_model_desc *model, const hpd_pmtp_des
   // drafting: iterations 1 .. W - 1 (W = the window)
   for (int it = 1; it < L.kmax && e == hipSuccess; ++it) {
     hpd::launch(hpd::KK_DRAFT_MLP, hpd::draft_input_kernel, dim3(L.nbpad), dim3(256), stream, it, L.nb, L.ntile,
-                amax_d, (const __bf16 *)pmtp->embed, f, L.H, x_d, ss_d, tok, draft_out);
+                amax_d, (const __bf16 *)pmtp->embed, f, L.H, model->rms_eps, x_d, ss_d, scale_d, tok,
+                draft_out);
     e = hipGetLastError();
     if (e != hipSuccess) break;
     hpd::GemmArgs g{};   // gate/up over [f ; e], SwiGLU, RMSNorm folded
@@ -346,6 +358,7 @@ hpd_status hpd_verify_draft_step(const hpd_model_desc *model, const hpd_pmtp_des
     g.T = L.nb;
     g.Tpad = L.nbpad;
     g.ss_in = ss_d;
+    g.scale_in = scale_d;   // the draft input's power-of-two prescale
     g.n_ss = 2 * L.H / hpd::kGemmTile;
     g.inv_H = 1.0f / (float)(2 * L.H);
     g.eps = model->rms_eps;

@@ -201,3 +201,27 @@ def test_small_stack_multipage(seed):
     print(f"multipage seed {seed}: T {len(h)} max abs {mx:.3e} rel L2 {rl:.3e}")
     assert mx <= BF16_MAX_ABS and rl <= BF16_REL_L2, (mx, rl)
     _check_cache(inp, pk, pv, nk, nv)
+
+
+@pytest.mark.parametrize("packed", [True, False], ids=["packed", "torch"])
+def test_large_residual_stream_stays_in_fp16_range(packed):
+    """hidden_in scaled by 2^15 (exact): |h * gamma| reaches about 1.3e5,
+    beyond fp16's 65504, so an fp16 MLP input written unscaled would be
+    inf.  The O projection writes it times the power of two of the token's
+    attention-norm factor, and the gate/up projection divides by it (both
+    exact), so the step matches the oracle.  At |h| < 2^17 the fp32 residual
+    stream has an ulp of 2^-7 and each of the 4 residual adds may round by
+    half of it.  So the update h_out - h_in is held to 1e-2 + 4 * 2^-8 max
+    abs and 1e-2 rel L2."""
+    announce(f"decode with a residual stream beyond fp16 range, packed {packed}")
+    inp = small_inputs(4)
+    inp.hidden_in = (inp.hidden_in * np.float32(2 ** 15)).astype(np.float32)
+    assert np.abs(inp.hidden_in).max() > 65504 * 1.5
+    h, pk, pv = run_decode(inp, packed=packed)
+    ref, nk, nv = decode_step(inp)
+    assert np.all(np.isfinite(h)), "non-finite output: the fp16 norm input overflowed"
+    h_in = inp.hidden_in.astype(np.float64)
+    mx, rl = errors(h - h_in, ref - h_in)
+    print(f"large residual stream, packed {packed}: update max abs {mx:.3e} rel L2 {rl:.3e}")
+    assert mx <= 1e-2 + 4 * 2.0 ** -8 and rl <= 1e-2, (mx, rl)
+    _check_cache(inp, pk, pv, nk, nv)

@@ -142,3 +142,15 @@ def test_verify_draft_c4_full_vocab():
     c = get_config("c4")["pmtp"]
     pm = make_pmtp_inputs(inp.hidden, c["vocab"], c["draft_inner"], c["weight_std"], 0)
     assert _check(inp, pm, 0) > 0.9
+
+
+def test_verify_draft_large_hidden_state():
+    """Hidden states scaled by 2^15 (exact), past fp16's range: the draft
+    input [f ; embed(t)] is written in fp16 times the power of two of its
+    own norm factor and the draft GEMM divides it back out, so the drafts
+    stay valid argmaxes of the oracle's logits."""
+    announce("pmtp with hidden states beyond fp16 range")
+    inp = small_inputs(1)
+    inp.hidden_in = (inp.hidden_in * np.float32(2 ** 15)).astype(np.float32)
+    pm = make_pmtp_inputs(inp.hidden, 2048, 256, 0.05, 1)
+    assert _check(inp, pm, 1) > 0.9
