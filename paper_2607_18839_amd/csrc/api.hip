@@ -175,6 +175,7 @@ hpd_status hpd_branch_attn_step(const hpd_plan *plan, const void *q, const void 
     return set_err(HPD_ERR_INVALID_ARGUMENT, "hpd_branch_attn_step: workspace must be 256-byte aligned");
   if (workspace_bytes < P.workspace_bytes)
     return set_err(HPD_ERR_WORKSPACE_TOO_SMALL, "hpd_branch_attn_step: workspace too small");
+  const hpd::TraceRange range("hpd_branch_attn_step");
   hipError_t e = hpd::launch_branch_attention(P, q, shared_k, shared_v, priv_k, priv_v, out, lse,
                                               workspace, (hipStream_t)stream);
   if (e != hipSuccess) return hip_err(e, "hpd_branch_attn_step");

@@ -28,6 +28,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdio>
 #include <string>
 
 #include "gemm.h"
@@ -254,11 +255,16 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
     return g;
   };
 
+  const hpd::TraceRange step_range("hpd_decode_step");
   const bool qwen3 = m.q_norm || m.k_norm || m.rope_theta > 0.f;
   const int Hq = P.attn.num_q_heads, Hkv = P.attn.num_kv_heads;
   hipError_t e = hpd::launch_norm_input(hidden_in, h, L.T, L.Tpad, L.H, gamma(m.g_attn_norm, 0), x, ss, attn,
                                          L.nq, packed, stream);
   for (int l = 0; l < m.num_layers && e == hipSuccess; ++l) {
+    char layer_name[32];
+    std::snprintf(layer_name, sizeof layer_name, "layer %d", l);
+    const hpd::TraceRange layer_range(layer_name);
+    hpd::TracePhase phase("qkv");
     // 1: QKV projection; the epilogue appends the new K/V rows to the cache
     hpd::GemmArgs g = base(L.rg_qkv, x, L.nq + 2 * L.nkv, L.H);
     g.w0 = (const __bf16 *)m.w_qkv[l];
@@ -279,9 +285,11 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
       if ((e = hipGetLastError()) != hipSuccess) break;
     }
     // 2: attention over the shared prefix and the private rows
+    phase.next("attention");
     e = hpd::launch_branch_attention(P, q, shared_k ? shared_k[l] : nullptr, shared_v ? shared_v[l] : nullptr,
                                      priv_k[l], priv_v[l], attn, nullptr, workspace, stream, packed);
     if (e != hipSuccess) break;
+    phase.next("o_proj");
     // 3: O projection into h; MLP norm input (fp16), scaled by the power of
     // two of the attention norm's factor so that it stays in fp16's range
     g = base(L.rg_o, attn, L.H, L.nq);
@@ -294,6 +302,7 @@ hpd_status hpd_decode_step(const hpd_model_desc *model, const hpd_plan *plan, co
     g.scale_in = scale;
     e = hpd::launch_gemm(g, false, hpd::kEpiResidual, hpd::KK_GEMM_O, stream);
     if (e != hipSuccess) break;
+    phase.next("mlp");
     // 4: gate/up projection, SwiGLU (fp16)
     g = base(L.rg_gu, x, 2 * L.I, L.H);
     g.ss_in = ss_mlp;

@@ -50,6 +50,31 @@ struct TimedEvents {
 TimedEvents timed_events(int kind);
 bool attn_phase_isolation();   // hpd_attn_phase_isolation
 
+// A roctx range (HPD_ROCTX=1) for the lifetime of the object: phases of a
+// step in a profiler's marker trace.
+class TraceRange {
+ public:
+  explicit TraceRange(const char *name);
+  ~TraceRange();
+  TraceRange(const TraceRange &) = delete;
+  TraceRange &operator=(const TraceRange &) = delete;
+
+ private:
+  bool on_;
+};
+// Consecutive phases: next() closes the current range and opens another.
+class TracePhase {
+ public:
+  explicit TracePhase(const char *name);
+  void next(const char *name);
+  ~TracePhase();
+  TracePhase(const TracePhase &) = delete;
+  TracePhase &operator=(const TracePhase &) = delete;
+
+ private:
+  bool on_;
+};
+
 template <typename... KArgs, typename... Args>
 void launch(int kind, void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t stream, Args... args) {
   const TimedEvents ev = timed_events(kind);

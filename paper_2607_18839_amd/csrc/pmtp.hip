@@ -303,6 +303,7 @@ hpd_status hpd_verify_draft_step(const hpd_model_desc *model, const hpd_pmtp_des
     return HPD_ERR_WORKSPACE_TOO_SMALL;
   }
   hipStream_t stream = (hipStream_t)stream_;
+  const hpd::TraceRange range("hpd_verify_draft_step");
   unsigned char *ws = (unsigned char *)workspace;
   const hpd::PlanDev dev = hpd::plan_dev(P, workspace);
   __bf16 *x_lm = (__bf16 *)(ws + L.off_x_lm);

@@ -6,7 +6,10 @@
 // nothing.
 #include <hip/hip_runtime.h>
 
+#include <dlfcn.h>
+
 #include <atomic>
+#include <cstdlib>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -55,6 +58,51 @@ TimedEvents timed_events(int kind) {
 }
 
 bool attn_phase_isolation() { return g_phase_isolation.load(std::memory_order_relaxed); }
+
+// roctx ranges around the phases of a step (HPD_ROCTX=1 in the environment):
+// the rocprofiler-sdk roctx library is opened on first use; without it, or
+// with the variable unset, ranges cost one branch.  The ranges mark the host
+// enqueueing the phases, so they bracket kernels when the step runs eagerly;
+// a captured graph replays the kernels without them.
+namespace {
+struct Roctx {
+  int (*push)(const char *) = nullptr;
+  int (*pop)() = nullptr;
+};
+const Roctx &roctx() {
+  static const Roctx r = [] {
+    Roctx x;
+    const char *env = std::getenv("HPD_ROCTX");
+    if (!env || std::string(env) != "1") return x;
+    void *h = dlopen("librocprofiler-sdk-roctx.so.1", RTLD_NOW | RTLD_LOCAL);
+    if (!h) h = dlopen("librocprofiler-sdk-roctx.so", RTLD_NOW | RTLD_LOCAL);
+    if (!h) return x;
+    x.push = (int (*)(const char *))dlsym(h, "roctxRangePushA");
+    x.pop = (int (*)())dlsym(h, "roctxRangePop");
+    if (!x.push || !x.pop) x.push = nullptr, x.pop = nullptr;
+    return x;
+  }();
+  return r;
+}
+}  // namespace
+
+TraceRange::TraceRange(const char *name) : on_(roctx().push != nullptr) {
+  if (on_) roctx().push(name);
+}
+TraceRange::~TraceRange() {
+  if (on_) roctx().pop();
+}
+TracePhase::TracePhase(const char *name) : on_(roctx().push != nullptr) {
+  if (on_) roctx().push(name);
+}
+void TracePhase::next(const char *name) {
+  if (!on_) return;
+  roctx().pop();
+  roctx().push(name);
+}
+TracePhase::~TracePhase() {
+  if (on_) roctx().pop();
+}
 
 }  // namespace hpd
 
