@@ -59,14 +59,14 @@ __device__ __forceinline__ u32x4 bf16x8_to_f16x8(u32x4 v) {
   return r;
 }
 
-// Epilogue operands of a tile.  Only the token's cache row (QKV, plan data)
-// is loaded before the main loop.  The residual row slice, the next norm's
-// weights and the per-token sums of squares were written or are read right
-// next to data the previous kernel wrote, and loading them early measurably
-// delays the loop's first steps (the loads retire in order), so the packed
-// kernel loads them in the epilogue.
+// Epilogue operands of a tile.  The token's cache row (QKV, plan data) and
+// scale are loaded before the main loop; the residual row slice, the next
+// norm's weights and the per-token sums of squares after the loads of the
+// first pipeline steps (packed kernel, load_pre) or after the loop.
+constexpr int kSsPrefetch = 32;   // sums of squares per token held in registers (hidden <= 1024)
 struct EpilogueIn {
   f32x4 h[4], gamma[4];   // residual: h row slice and gamma (ones if none)
+  f32x4 ss[kSsPrefetch / 4];   // QKV, SwiGLU: the token's sums of squares (load_pre)
   int dest;               // QKV: private cache row of the token
   float inv_rms;          // QKV, SwiGLU: RMSNorm factor of the token
   float scale;            // residual, SwiGLU: s_t of the fp16 norm input (scale_in), else 1
@@ -105,6 +105,40 @@ __device__ __forceinline__ void load_late(const GemmArgs &g, int t, int tile, in
       sum += (v[0] + v[1]) + (v[2] + v[3]);
     }
     in.inv_rms = 1.0f / sqrtf(sum * g.inv_H + g.eps);
+  }
+}
+
+// The packed kernel's epilogue loads, split around its main loop: load_pre
+// issues them right after the loads of the first pipeline steps, so that the
+// waits for those steps do not cover them and their latency overlaps the
+// loop; load_post reduces them.  (Issued before the first steps' loads they
+// delayed the loop: loads retire in order.)  Every buffer they read was
+// written at least two launches earlier (h by the residual projection
+// before the previous kernel, the sums of squares and gamma earlier still).
+// Sums of squares beyond kSsPrefetch values per token are loaded late.
+template <int EPI>
+__device__ __forceinline__ void load_pre(const GemmArgs &g, int t, int tile, int half, EpilogueIn &in) {
+  if constexpr (EPI == kEpiResidual) {
+    load_late<EPI>(g, t, tile, half, in);
+  } else if (g.n_ss <= kSsPrefetch) {
+    const float *sr = g.ss_in + (int64_t)t * g.n_ss;
+#pragma unroll
+    for (int i = 0; i < kSsPrefetch / 4; ++i)
+      in.ss[i] = 4 * i < g.n_ss ? *(const f32x4 *)(sr + 4 * i) : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+}
+template <int EPI>
+__device__ __forceinline__ void load_post(const GemmArgs &g, int t, int tile, int half, EpilogueIn &in) {
+  if constexpr (EPI != kEpiResidual) {
+    if (g.n_ss <= kSsPrefetch) {   // the sum in load_late's order
+      float sum = 0.f;
+#pragma unroll
+      for (int i = 0; i < kSsPrefetch / 4; ++i)
+        if (4 * i < g.n_ss) sum += (in.ss[i][0] + in.ss[i][1]) + (in.ss[i][2] + in.ss[i][3]);
+      in.inv_rms = 1.0f / sqrtf(sum * g.inv_H + g.eps);
+    } else {
+      load_late<EPI>(g, t, tile, half, in);
+    }
   }
 }
 
@@ -442,6 +476,7 @@ __global__ __launch_bounds__(256) void gemm_packed_kernel(GemmArgs g) {
   // so that no load sits under a runtime condition
 #pragma unroll
   for (int u = 0; u < S - 1; ++u) load(min(u, nsteps - 1), u);
+  if (kgi == 0) load_pre<EPI>(g, t, tile, half, ein);   // behind the first steps' loads
   if (nsteps >= 2 * S - 1) {
     const int n_main = (nsteps - (2 * S - 1)) / S + 1;
     for (int gi = 0; gi < n_main; ++gi) {
@@ -457,8 +492,7 @@ __global__ __launch_bounds__(256) void gemm_packed_kernel(GemmArgs g) {
     with_rem<2 * S - 2>(nsteps, [&](auto rem) { tail(0, rem); });            // 1 .. 2 S - 2
   }
 
-  // the epilogue's own loads overlap the K-group hand-over
-  if (kgi == 0) load_late<EPI>(g, t, tile, half, ein);
+  if (kgi == 0) load_post<EPI>(g, t, tile, half, ein);
   if constexpr (KG > 1) {
     // K groups 1.. hand their tiles to K group 0, which adds them in order
     __shared__ float red[(KG - 1) * RG * 16 * 64];
