@@ -387,11 +387,32 @@ template <typename T> struct WaveAttn {
           ld16(ka[kb][st], (const T *)(kt_next + key * Tl::kRowBytes + 16 * Tl::kchunk(key, 4 * half + st)));
       }
     }
+    step_frags<FSUM>(kt_next != nullptr, ka, vt, voff, s_cur, s_next, key0, limit, masked, c);
+  }
+
+  // Raw scores S^T of a K tile held in registers: ka[kb][st] is the K
+  // operand of key block kb (32 keys) and contraction step st, as qk_ring
+  // reads it from LDS.
+  __device__ __forceinline__ void qk_frags(const Frag<T> (&ka)[2][4], f32x16 (&s)[2]) {
+    for (int r = 0; r < 16; ++r) { s[0][r] = 0.f; s[1][r] = 0.f; }
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) mma(s[kb], ka[kb][st], qf[st]);
+  }
+
+  // step_ring with the next tile's K operand already in registers (ka, used
+  // if has_next).
+  template <bool FSUM = false>
+  __device__ __forceinline__ void step_frags(bool has_next, const Frag<T> (&ka)[2][4], const unsigned char *vt,
+                                             const int (&voff)[2], f32x16 (&s_cur)[2], f32x16 (&s_next)[2], int key0,
+                                             int limit, bool masked, float c) {
+    static_assert(sizeof(T) == 2, "bf16 only");
     u32x2t vr[16];   // [b][st][hh]
     ds_read_tr16_tile<0>(vr, vt + voff[0], vt + voff[1]);
     // matrix core first: the next tile's scores need only the K reads, and
     // run while the VALU does this tile's softmax
-    if (kt_next) {
+    if (has_next) {
       for (int r = 0; r < 16; ++r) { s_next[0][r] = 0.f; s_next[1][r] = 0.f; }
 #pragma unroll
       for (int st = 0; st < 4; ++st)
@@ -632,6 +653,8 @@ struct AttnArgs {
   float c;   // softmax scale * log2(e)
   Plan::RegularShared reg;
   int priv_first;   // bf16 kernel: private workgroups take the first grid slots
+  int priv_per_wg;  // bf16 kernel: private items per workgroup (1..kPrivMaxPerWG)
+  int priv_slots;   // bf16 kernel: private workgroups, rounded up to a multiple of 8
   int paged;        // K/V rows through the plan's tile tables
 };
 
@@ -746,11 +769,12 @@ __global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
 // copy count the same.
 constexpr int kPairRing = 4;
 
-// Private work items of the bf16 kernel: one per wave on kPrivPerWG waves of
-// a workgroup, each wave with kPrivWaveBytes of LDS for the item's K and V
-// tiles (an item has at most kPrivateChunkKeys = 128 keys: two tiles).
-constexpr int kPrivPerWG = 4;
-constexpr int kPrivWaveBytes = 2 * 2 * 64 * 128;
+// Private work items of the bf16 kernel: one per wave on the first
+// priv_per_wg (at most kPrivMaxPerWG = all 8) waves of a workgroup, each wave
+// with kPrivWaveBytes of LDS for the item's V tiles (an item has at most
+// kPrivateChunkKeys = 128 keys: two tiles; its K tiles go to registers).
+constexpr int kPrivMaxPerWG = 8;
+constexpr int kPrivWaveBytes = 2 * 64 * 128;
 static_assert(kPrivateChunkKeys <= 128, "a private item fits two tiles");
 __device__ __forceinline__ void private_item_ring(const AttnArgs &a, int item, int lane, unsigned char *lds);
 
@@ -758,23 +782,25 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   using T = __bf16;
   using Tl = Tile<T>;
   constexpr int S = kPairRing, kTileBytes = 64 * 128, kTile = 2 * kTileBytes, kPair = 2 * kTile;
-  constexpr int kRingBytes = S * kPair, kPrivBytes = kPrivPerWG * kPrivWaveBytes;
+  constexpr int kRingBytes = S * kPair, kPrivBytes = kPrivMaxPerWG * kPrivWaveBytes;
   __shared__ __attribute__((aligned(16))) unsigned char lds[kRingBytes > kPrivBytes ? kRingBytes : kPrivBytes];
 
-  // Workgroups run either kPrivPerWG private items or one shared item.  Both
+  // Workgroups run either priv_per_wg private items or one shared item.  Both
   // ranges are rounded up to multiples of 8 so that the shared items keep
   // the XCD-aware order of the other kernels.  priv_first (the grid fits the
   // chip in one round): the private range comes first, so the longer
   // dependency chain of a private item starts first; otherwise the shared
   // items, the larger work, are dispatched first and the private items fill
   // in behind them.
-  const int n_priv_wg = (a.n_private + kPrivPerWG - 1) / kPrivPerWG;
-  const int n_priv_slots = (n_priv_wg + 7) / 8 * 8, n_shared_slots = (a.n_shared + 7) / 8 * 8;
+  // (the private slot count comes from the host: a division by the runtime
+  // items per workgroup would delay every workgroup's start)
+  const int n_priv_slots = a.priv_slots, n_shared_slots = (a.n_shared + 7) / 8 * 8;
   const int priv0 = a.priv_first ? 0 : n_shared_slots, shared0 = a.priv_first ? n_priv_slots : 0;
   const int bid = blockIdx.x;
   if (bid >= priv0 && bid < priv0 + n_priv_slots) {
-    const int wave = threadIdx.x >> 6, pi = (bid - priv0) * kPrivPerWG + wave;
-    if (wave < kPrivPerWG && pi < a.n_private)
+    // wave-uniform (scalar loads of the item's fields)
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), pi = (bid - priv0) * a.priv_per_wg + wave;
+    if (wave < a.priv_per_wg && pi < a.n_private)
       private_item_ring(a, pi, threadIdx.x & 63, lds + wave * kPrivWaveBytes);
     return;
   }
@@ -895,21 +921,24 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   w.write_f16(lds + 4 * 34 * 64 * 4 + rw * 4096, (_Float16 *)a.dev.part_o, a.dev.part_lse, prow_of, lane, true);
 }
 
-// One private work item on one wave of the bf16 kernel, in the wave's own
-// kPrivWaveBytes of LDS (no other wave touches it).  Both K/V tiles of the
-// item are copied straight into LDS in the ring layout (tile 0, then the Q
-// loads, then tile 1), then processed with the ring arithmetic.  Key rows
-// past the item's range are clamped to its last key and masked.
+// One private work item on one wave of the bf16 kernel.  Every load of the
+// item is issued at once: its K rows straight into the registers of the
+// QK^T operand (per MFMA a lane needs 16 contiguous bytes of one key row),
+// its V rows into the wave's own kPrivWaveBytes of LDS in the ring layout
+// (the PV operand is read transposed from there; no other wave touches the
+// region), its Q fragments and the partial-row indices of its rows.  Key
+// rows past the item's range are clamped to its last key and masked; an
+// item of one tile loads its second tile clamped as well (not used), so
+// that no load depends on the item's length.
 __device__ __forceinline__ void private_item_ring(const AttnArgs &a, int item, int lane, unsigned char *lds) {
   using T = __bf16;
-  using Tl = Tile<T>;
   constexpr int kTileBytes = 64 * 128;
   const int32_t *it = a.dev.private_items + (int64_t)item * PI_NFIELDS;
   const int g = it[PI_KVH], row0 = it[PI_ROW0], nrows = it[PI_NROWS];
   const int key0 = it[PI_KEY0], key1 = it[PI_KEY1], slot = it[PI_SLOT], past = it[PI_PAST];
   const int priv_row = it[PI_PRIV_ROW], q_row = it[PI_Q_ROW];
 
-  const int rloc = lane & 31;
+  const int rloc = lane & 31, half = lane >> 5;
   const bool valid = rloc < nrows;
   const int R = row0 + rloc;                            // stacked row of (branch, g)
   const int j = valid ? R / a.G : 0;                    // draft index within the branch
@@ -922,51 +951,68 @@ __device__ __forceinline__ void private_item_ring(const AttnArgs &a, int item, i
   const int64_t stride = (int64_t)a.Hkv * D;
   const T *kbase = (const T *)a.priv_k + (int64_t)g * D;
   const T *vbase = (const T *)a.priv_v + (int64_t)g * D;
-  // paged K/V: lanes 0 and 1 hold the pool rows of the item's two tiles
-  const int tile_row = a.paged && lane < ntiles ? a.dev.priv_tiles[priv_row + (key0 >> 6) + lane] : 0;
-  // tile c: 8 copies of K rows 8 i + lane / 8 (physical chunk lane % 8) and
-  // 8 of V, 16 per tile
+  // K/V row of key k (clamped into the item's range) loaded for tile c is
+  // base[c] + k - first key of tile min(c, ntiles - 1): with one tile, tile
+  // 1's keys are all the item's last key, in tile 0.  Paged K/V: the pool
+  // rows of the item's tiles, read before any copy is issued (a wait for
+  // them behind the copies would wait for the copies too).
+  int64_t base[2];
+  if (a.paged) {
+    const int tile_row = a.dev.priv_tiles[priv_row + (key0 >> 6) + min(lane & 1, ntiles - 1)];
+    base[0] = __builtin_amdgcn_readlane(tile_row, 0);
+    base[1] = __builtin_amdgcn_readlane(tile_row, 1);
+  } else {
+    base[0] = (int64_t)priv_row + key0;
+    base[1] = (int64_t)priv_row + key0 + 64 * (ntiles - 1);
+  }
+  auto row_of = [&](int c, int k) -> int64_t { return base[c] + (k - key0 - 64 * min(c, ntiles - 1)); };
+  // first partial slot of the token of the wave's row `lane` (lanes 0..31
+  // with a query), loaded with the tiles
+  const int tr = q_row + (row0 + (lane & 31)) / a.G;
+  const int tslot = a.dev.token_slots[2 * (lane < nrows ? tr : q_row)];
+  // V tile c: 8 copies of rows 8 i + lane / 8 (physical chunk lane % 8)
   const int rsub = lane >> 3, pch = lane & 7;
-  auto issue = [&](int c) {
-    unsigned char *st = lds + c * 2 * kTileBytes;
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
     const int kt = key0 + 64 * c;
-    const int64_t base = a.paged ? (int64_t)__builtin_amdgcn_readlane(tile_row, c) : (int64_t)priv_row + kt;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int row = 8 * i + rsub;
-      const int64_t r = base + (min(kt + row, key1 - 1) - kt);
-      dma16(kbase + r * stride + 8 * Tl::kchunk(row, pch), st + 1024 * i);
-      dma16(vbase + r * stride + 8 * vchunk(row, pch), st + kTileBytes + 1024 * i);
+      const int64_t r = row_of(c, min(kt + row, key1 - 1));
+      dma16(vbase + r * stride + 8 * vchunk(row, pch), lds + c * kTileBytes + 1024 * i);
     }
-  };
-  issue(0);
+  }
+  // K tile c: key block kb, contraction step st holds dims 32 half + 8 st ..
+  // + 8 of key 32 kb + lane % 32 (the order of the Q fragments)
+  Frag<T> ka[2][2][4];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const int kt = key0 + 64 * c;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const T *kr = kbase + row_of(c, min(kt + 32 * kb + rloc, key1 - 1)) * stride + 32 * half;
+#pragma unroll
+      for (int st = 0; st < 4; ++st) ld16(ka[c][kb][st], kr + 8 * st);
+    }
+  }
   WaveAttn<T> w;
   w.init((const T *)a.q + ((int64_t)t * a.Hq + hq) * D, valid, lane);
-  if (ntiles > 1) {
-    issue(1);
-    wait_vm<16>();   // tile 0 and the Q fragments
-  } else {
-    wait_vm<0>();
-  }
+  wait_vm<0>();   // the V copies into LDS (the register loads are waited for by the compiler)
   int voff[2];
   WaveAttn<T>::vt_offsets(lane, voff);
   f32x16 s_cur[2], s_next[2];
-  w.qk_ring(lds, s_cur, lane);
-  if (ntiles > 1) wait_vm<0>();   // tile 1 (its K is read by the first step)
-  w.step_ring<true>(ntiles > 1 ? lds + 2 * kTileBytes : nullptr, lds + kTileBytes, voff, s_cur, s_next, key0, limit,
-                    key0 + 64 > wmin, a.c, lane);
+  w.qk_frags(ka[0], s_cur);
+  w.step_frags<true>(ntiles > 1, ka[1], lds, voff, s_cur, s_next, key0, limit, key0 + 64 > wmin, a.c);
   if (ntiles > 1) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) { s_cur[0][r] = s_next[0][r]; s_cur[1][r] = s_next[1][r]; }
-    w.step_ring<true>(nullptr, lds + 3 * kTileBytes, voff, s_cur, s_next, key0 + 64, limit, key0 + 128 > wmin, a.c,
-                      lane);
+    w.step_frags<true>(false, ka[1], lds + kTileBytes, voff, s_cur, s_next, key0 + 64, limit, key0 + 128 > wmin,
+                       a.c);
   }
-  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the tiles are consumed; tile 0 becomes write scratch
-  auto prow_of = [&](int r) -> int64_t {
-    if (r >= nrows) return -1;
-    const int Rr = row0 + r, tr = q_row + Rr / a.G;
-    return ((int64_t)a.dev.token_slots[2 * tr] + slot) * a.Hq + g * a.G + Rr % a.G;
-  };
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the V tiles are consumed; tile 0 becomes write scratch
+  // partial row of the wave's row `lane` (the planner keeps partial rows below 2^31)
+  const int my_prow = lane < nrows ? (tslot + slot) * a.Hq + g * a.G + (row0 + lane) % a.G : -1;
+  auto prow_of = [&](int r) -> int64_t { return __shfl(my_prow, r); };
   w.write_f16(lds, (_Float16 *)a.dev.part_o, a.dev.part_lse, prow_of, lane, false);
 }
 
@@ -1134,18 +1180,36 @@ hipError_t launch_branch_attention(const Plan &P, const void *q, const void *sha
   a.paged = P.paged ? 1 : 0;
   const bool bf16 = P.attn.dtype == HPD_BF16;
   if (bf16) {
-    // one launch: the private items (kPrivPerWG per workgroup) and the
-    // shared-prefix items; phase isolation: the shared items, then the
-    // private items, in launches of their own
-    auto grid = [](const AttnArgs &x) {
-      const int n_priv_wg = (x.n_private + kPrivPerWG - 1) / kPrivPerWG;
-      return (n_priv_wg + 7) / 8 * 8 + (x.n_shared + 7) / 8 * 8;
+    // one launch: the private items and the shared-prefix items; phase
+    // isolation: the shared items, then the private items, in launches of
+    // their own
+    auto priv_slots = [](const AttnArgs &x) {
+      const int n_priv_wg = (x.n_private + x.priv_per_wg - 1) / x.priv_per_wg;
+      return (n_priv_wg + 7) / 8 * 8;
     };
-    a.priv_first = grid(a) <= num_cus() ? 1 : 0;
+    auto grid = [&](const AttnArgs &x) { return priv_slots(x) + (x.n_shared + 7) / 8 * 8; };
+    // Private items per workgroup: the fewest that still fit the grid on
+    // the chip in one round (one workgroup per CU: the launch's LDS), so
+    // that the items spread over the CUs the shared items leave free.  When
+    // the grid takes more than one round anyway, the private workgroups
+    // follow the shared ones and fill the CUs those free, 4 items each
+    // (measured on the 16-page workload, 252 shared items and 1,422 private
+    // ones: 46.4 us per launch; 8 per workgroup 47.6 us, 2 per workgroup
+    // 51.6 us, the private workgroups first 51.4 us).
+    auto fit = [&](AttnArgs &x) {
+      for (x.priv_per_wg = 1; x.priv_per_wg < kPrivMaxPerWG; ++x.priv_per_wg)
+        if (grid(x) <= num_cus()) break;
+      x.priv_first = grid(x) <= num_cus() ? 1 : 0;
+      if (!x.priv_first) x.priv_per_wg = 4;
+      x.priv_slots = priv_slots(x);
+    };
+    fit(a);
     if (attn_phase_isolation()) {
       AttnArgs sh = a, pr = a;
       sh.n_private = 0;
       pr.n_shared = 0;
+      fit(sh);
+      fit(pr);
       if (sh.n_shared > 0) launch(KK_SHARED, shared_prefix_ring_kernel, dim3(grid(sh)), dim3(512), stream, sh);
       if (pr.n_private > 0) launch(KK_PRIVATE, shared_prefix_ring_kernel, dim3(grid(pr)), dim3(512), stream, pr);
     } else if (grid(a) > 0) {

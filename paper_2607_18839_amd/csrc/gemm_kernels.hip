@@ -122,9 +122,10 @@ __device__ __forceinline__ void load_pre(const GemmArgs &g, int t, int tile, int
     load_late<EPI>(g, t, tile, half, in);
   } else if (g.n_ss <= kSsPrefetch) {
     const float *sr = g.ss_in + (int64_t)t * g.n_ss;
+    // unconditional loads (an index past the row repeats its last four
+    // values, unused): a load under a condition would be followed by a wait
 #pragma unroll
-    for (int i = 0; i < kSsPrefetch / 4; ++i)
-      in.ss[i] = 4 * i < g.n_ss ? *(const f32x4 *)(sr + 4 * i) : f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < kSsPrefetch / 4; ++i) in.ss[i] = *(const f32x4 *)(sr + min(4 * i, g.n_ss - 4));
   }
 }
 template <int EPI>
