@@ -138,36 +138,49 @@ def main():
     print(json.dumps(res))
 
 
-def _graph_time(torch, step, n_graphs, K, W):
-    """Captures n_graphs HIP graphs (torch's CUDAGraph on ROCm), graph i
-    running step(i) once, replays them round-robin W times untimed, then
-    times exactly K replays, with an event after each.  Returns (mean ms per
-    step, K, {p10, p50, p90} of the per-step times in ms)."""
+def _graph_time(torch, step, n_inputs, K, W, per_graph=1):
+    """Captures HIP graphs (torch's CUDAGraph on ROCm) of per_graph
+    consecutive steps each, step j running step(j % n_inputs), so that the
+    graphs together cover every input (max(1, n_inputs // per_graph) graphs).
+    Replays them round-robin for the W warm-up steps untimed, then times
+    exactly K steps (K / per_graph replays; per_graph divides K) with an event
+    after each replay.  Several steps per graph keep the GPU busy when one
+    step is shorter than the host's cost of a replay.  Returns (mean ms per
+    step, K, {p10, p50, p90} of the per-replay times / per_graph in ms)."""
+    assert K % per_graph == 0
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):           # eager warm-up outside capture
-        for i in range(n_graphs):
+        for i in range(n_inputs):
             step(i)
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     graphs = []
-    for i in range(n_graphs):
+    for i in range(max(1, n_inputs // per_graph)):
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            step(i)
+            for j in range(per_graph):
+                step((i * per_graph + j) % n_inputs)
         graphs.append(g)
-    for w in range(max(1, W)):
-        graphs[w % n_graphs].replay()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    for w in range(max(1, -(-W // per_graph))):
+        graphs[w % len(graphs)].replay()
+    n = K // per_graph
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
     torch.cuda.synchronize()
     ev[0].record()
-    for i in range(K):
-        graphs[i % n_graphs].replay()
+    for i in range(n):
+        graphs[i % len(graphs)].replay()
         ev[i + 1].record()
     torch.cuda.synchronize()
-    per = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(K)])
+    per = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(n)]) / per_graph
     pct = {f"p{q}": float(np.percentile(per, q)) for q in (10, 50, 90)}
-    return ev[0].elapsed_time(ev[K]) / K, K, pct
+    return ev[0].elapsed_time(ev[n]) / K, K, pct
+
+
+def _steps_per_graph(K):
+    """Steps per graph for the single-layer workloads: the largest of 8, 5,
+    4, 2, 1 that divides K."""
+    return next(g for g in (8, 5, 4, 2, 1) if K % g == 0)
 
 
 def _kernel_pass(torch, _lib, step, K, W, queue_cycles=20_000_000):
@@ -325,7 +338,8 @@ def bench_attention(args, torch, _lib):
         q, sk, sv, pk, pv = replicas[i % reps]
         layer(q, sk, sv, pk, pv, out=out)
 
-    ms, timed, pct = _graph_time(torch, step, reps, args.steps, args.warmup)
+    per_graph = _steps_per_graph(args.steps)
+    ms, timed, pct = _graph_time(torch, step, reps, args.steps, args.warmup, per_graph)
     kern = _kernel_pass(torch, _lib, step, min(args.steps, 20), args.warmup, queue_cycles=2_000_000)
     w = attn_work(b.prefix_len, b.branch_page, b.num_new, b.past_len, b.num_q_heads, b.num_kv_heads, 64,
                   s_in, s_in, b.fork_len)
@@ -353,7 +367,7 @@ def bench_attention(args, torch, _lib):
         "metric": "branch-tokens/s per decode step", "value": w["T"] / (ms / 1e3), "unit": "branch-tokens/s",
         "n_gpus": 1, "steps": timed, "warmup": args.warmup, "ms_per_step": ms, "latency_ms": pct,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": b.dtype, "data": "synthetic", "timing": "HIP graph replay (one step per graph, one graph per input replica)",
+        "dtype": b.dtype, "data": "synthetic", "timing": f"HIP graph replay ({per_graph} steps per graph, each on its own input replica)",
         "config": {"workload": f"{args.workload}: single attention layer", "pages": b.num_pages,
                    "branches": b.num_branches, "branch_tokens": w["T"],
                    "prefix_len_total": int(b.prefix_len.sum()),
