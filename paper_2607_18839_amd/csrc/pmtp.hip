@@ -177,30 +177,50 @@ __global__ __launch_bounds__(256) void draft_input_kernel(int it, int nb, int nt
     const bf16x4 e = *(const bf16x4 *)(embed + (int64_t)tok * H + (c - H));
     return f32x4{(float)e[0], (float)e[1], (float)e[2], (float)e[3]};
   };
-  // pass 1: sums of squares per 32-column tile
-  for (int c = 4 * threadIdx.x; c < W; c += 1024) {
-    const f32x4 v = value(c);
+  // pass 1: sums of squares per 32-column tile (for the SwiGLU GEMM's norm
+  // factor) and of the whole row, reduced in registers and LDS; the row's
+  // first kCache chunks per thread stay in registers for pass 2
+  constexpr int kCache = 4;
+  __shared__ float wsum[4];
+  f32x4 vals[kCache];
+  float part = 0.f;
+  auto tile_sum = [&](int c, const f32x4 &v) {
     float sq = fmaf(v[0], v[0], fmaf(v[1], v[1], fmaf(v[2], v[2], v[3] * v[3])));
+    part += sq;
     sq += __shfl_xor(sq, 1);   // 8 consecutive threads cover one 32-column tile
     sq += __shfl_xor(sq, 2);
     sq += __shfl_xor(sq, 4);
     if ((threadIdx.x & 7) == 0) ss_d[(int64_t)b * n_ss + c / kGemmTile] = sq;
+  };
+#pragma unroll
+  for (int i = 0; i < kCache; ++i) {
+    const int c = 4 * threadIdx.x + 1024 * i;
+    vals[i] = c < W ? value(c) : f32x4{0.f, 0.f, 0.f, 0.f};
+    if (c < W) tile_sum(c, vals[i]);
   }
-  __syncthreads();   // the row's sums, written by the whole workgroup, are visible to it
+  for (int c = 4 * threadIdx.x + 1024 * kCache; c < W; c += 1024) tile_sum(c, value(c));
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = part;
+  __syncthreads();
   // pass 2: the row as fp16, scaled by the power of two of its norm factor,
   // which the SwiGLU GEMM divides back out
-  float sum = 0.f;
-  for (int i = 0; i < n_ss; ++i) sum += ss_d[(int64_t)b * n_ss + i];
+  const float sum = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
   const float s = pow2_scale(1.0f / sqrtf(sum / (float)W + eps));
   if (threadIdx.x == 0) scale_d[b] = s;
-  for (int c = 4 * threadIdx.x; c < W; c += 1024) {
-    const f32x4 v = value(c);
-    typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+  typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+  auto put = [&](int c, const f32x4 &v) {
     f16x4 o;
 #pragma unroll
     for (int r = 0; r < 4; ++r) o[r] = (_Float16)(v[r] * s);
     *(f16x4 *)((_Float16 *)x_d + packed_offset(b, c, W)) = o;
+  };
+#pragma unroll
+  for (int i = 0; i < kCache; ++i) {
+    const int c = 4 * threadIdx.x + 1024 * i;
+    if (c < W) put(c, vals[i]);
   }
+  for (int c = 4 * threadIdx.x + 1024 * kCache; c < W; c += 1024) put(c, value(c));
 }
 
 // Embedding rows of the tokens a step feeds, as fp32 (one workgroup per token).
