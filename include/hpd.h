@@ -142,6 +142,15 @@ typedef struct {
   const int32_t *private_items;   /* [num_private_items][12] fields: csrc/plan.h */
   const int32_t *token_slots;     /* [T][2] first partial slot, slot count     */
   int64_t num_partial_slots;      /* partial (O, lse) rows = slots * Hq        */
+  const int32_t *pos_token;       /* [T][2] (token, visible prefix F_b) held by
+                                     stacked position i of the shared-prefix
+                                     items: a page's positions are page_q_row[p]
+                                     .. + page_T[p] - 1, and its stacked row r
+                                     (per kv head) is query head g * G + r % G
+                                     of position page_q_row[p] + r / G.  Without
+                                     fork offsets position i holds token i; with
+                                     them a page's tokens are ordered by
+                                     descending F_b (ties: token order)        */
 } hpd_plan_info;
 
 /* Build a plan: validates the descriptors (see each field above), computes

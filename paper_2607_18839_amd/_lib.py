@@ -65,7 +65,7 @@ class hpd_plan_info(ctypes.Structure):
                 ("visible", c_i32p), ("shared_rows", ctypes.c_int64), ("priv_rows", ctypes.c_int64),
                 ("num_shared_items", ctypes.c_int32), ("num_private_items", ctypes.c_int32),
                 ("shared_items", c_i32p), ("private_items", c_i32p), ("token_slots", c_i32p),
-                ("num_partial_slots", ctypes.c_int64)]
+                ("num_partial_slots", ctypes.c_int64), ("pos_token", c_i32p)]
 
 
 PP = ctypes.POINTER(ctypes.c_void_p)
@@ -259,7 +259,8 @@ def hpd_plan_query(plan):
                 shared_rows=info.shared_rows, priv_rows=info.priv_rows,
                 shared_items=arr(info.shared_items, info.num_shared_items, SI_NFIELDS),
                 private_items=arr(info.private_items, info.num_private_items, PI_NFIELDS),
-                token_slots=arr(info.token_slots, T, 2), num_partial_slots=info.num_partial_slots)
+                token_slots=arr(info.token_slots, T, 2), num_partial_slots=info.num_partial_slots,
+                pos_token=arr(info.pos_token, T, 2))
 
 
 def hpd_plan_upload(plan, workspace, nbytes, stream=None):

@@ -147,6 +147,7 @@ hpd_status hpd_plan_query(const hpd_plan *plan, hpd_plan_info *o) {
   o->private_items = P.private_items.data();
   o->token_slots = P.token_slots.data();
   o->num_partial_slots = P.num_slots;
+  o->pos_token = P.pos_token.data();
   return HPD_OK;
 }
 

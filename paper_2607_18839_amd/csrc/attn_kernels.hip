@@ -643,6 +643,12 @@ __device__ __forceinline__ int wave_min(int v) {
   return v;
 }
 
+__device__ __forceinline__ int wave_max(int v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = max(v, __shfl_xor(v, off));
+  return v;
+}
+
 // ------------------------------------------------------------ shared kernel
 
 struct AttnArgs {
@@ -696,6 +702,22 @@ __device__ __forceinline__ SharedItem shared_item(const AttnArgs &a, int item) {
   return si;
 }
 
+// Token of stacked position pos of a shared item's page, and with fork
+// offsets the row's key limit (min of limit and the token's visible
+// prefix).  Sorted pages (fork offsets) map positions through the plan's
+// pos_token table, whose entries also carry the visible prefix.
+__device__ __forceinline__ void row_token(const AttnArgs &a, int flags, int page_q_row, int pos, bool valid,
+                                          int &t, int &limit) {
+  if (flags & SI_FLAG_SORTED) {
+    const int2 e = *(const int2 *)(a.dev.pos_token + 2 * (int64_t)(page_q_row + pos));
+    t = e.x;
+    if (valid) limit = min(limit, e.y);
+  } else {
+    t = page_q_row + pos;
+    if ((flags & SI_FLAG_FORK) && valid) limit = min(limit, a.dev.token_fork[t]);
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
   constexpr int NT = 256;
@@ -717,12 +739,12 @@ __global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
   const int rloc = wave * 32 + (lane & 31);
   const bool valid = rloc < nrows;
   const int R = row0 + rloc;                           // stacked row of (page, g)
-  const int t = page_q_row + (valid ? R / a.G : 0);
+  int t, limit = key1;
+  row_token(a, flags, page_q_row, valid ? R / a.G : 0, valid, t, limit);
   const int hq = g * a.G + (valid ? R % a.G : 0);
-  int limit = key1;
-  if ((flags & SI_FLAG_FORK) && valid) limit = min(limit, a.dev.token_fork[t]);
   const bool wave_active = wave * 32 < nrows;
   const int wmin = wave_min(valid ? limit : key1);
+  const int wmax = wave_max(valid ? limit : key0);   // keys past it: no row of the wave sees them
 
   const int64_t stride = (int64_t)a.Hkv * D;
   const T *kbase = (const T *)a.shared_k + (int64_t)g * D;
@@ -744,7 +766,7 @@ __global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
       ld.load(kbase + row(k0 + 64), stride, key1 - k0 - 64, tid);
       ld.load_v(vbase + row(k0 + 64), stride, key1 - k0 - 64, tid);
     }
-    if (wave_active) w.tile(lds[i & 1], k0, limit, k0 + 64 > wmin, a.c, lane);
+    if (wave_active && k0 < wmax) w.tile(lds[i & 1], k0, limit, k0 + 64 > wmin, a.c, lane);
     if (i + 1 < ntiles) ld.store(lds[(i + 1) & 1], tid);
     __syncthreads();
   }
@@ -818,12 +840,14 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   const int rloc = rw * 32 + (lane & 31);
   const bool valid = rloc < nrows;
   const int R = row0 + rloc;                           // stacked row of (page, g)
-  const int t = page_q_row + (valid ? R / a.G : 0);
+  int t, limit = key1;
+  row_token(a, flags, page_q_row, valid ? R / a.G : 0, valid, t, limit);
   const int hq = g * a.G + (valid ? R % a.G : 0);
-  int limit = key1;
-  if ((flags & SI_FLAG_FORK) && valid) limit = min(limit, a.dev.token_fork[t]);
   const bool wave_active = rw * 32 < nrows;
   const int wmin = wave_min(valid ? limit : key1);
+  // key tiles of the item that some row of this wave sees (fork offsets:
+  // the rest are skipped; their copies are still issued for the others)
+  const int ntw = max(0, (min(key1, wave_max(valid ? limit : key0)) - key0 + 63) / 64);
 
   const int64_t stride = (int64_t)a.Hkv * D;
   const T *kbase = (const T *)a.shared_k + (int64_t)g * D;
@@ -875,7 +899,7 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   const int my_prow = valid && limit > key0 ? (my_slots + slot) * a.Hq + hq : -1;
   ring_barrier();   // pair 0 visible to every wave
   f32x16 s_cur[2], s_next[2];
-  if (wave_active && par < ntiles) w.qk_ring(lds + par * kTile, s_cur, lane);
+  if (wave_active && par < ntw) w.qk_ring(lds + par * kTile, s_cur, lane);
   for (int j = 0; j < npairs; ++j) {
     // pair j + 1 visible; the slot of pair j - 1 (read in iteration j - 1) is free
     if (j + 1 < npairs) {
@@ -884,8 +908,8 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
       if (j + 3 < npairs) issue(j + 3);
     }
     const int ti = 2 * j + par;
-    if (wave_active && ti < ntiles) {
-      const unsigned char *kt_next = ti + 2 < ntiles ? lds + ((j + 1) % S) * kPair + par * kTile : nullptr;
+    if (wave_active && ti < ntw) {
+      const unsigned char *kt_next = ti + 2 < ntw ? lds + ((j + 1) % S) * kPair + par * kTile : nullptr;
       const int k0 = key0 + 64 * ti;
       w.step_ring(kt_next, lds + (j % S) * kPair + par * kTile + kTileBytes, voff, s_cur, s_next, k0, limit,
                   k0 + 64 > wmin, a.c, lane);
@@ -1158,6 +1182,7 @@ PlanDev plan_dev(const Plan &P, void *workspace) {
   d.token_fork = (const int32_t *)(ws + P.off_token_fork);
   d.token_dest = (const int32_t *)(ws + P.off_token_dest);
   d.token_vis = (const int32_t *)(ws + P.off_token_vis);
+  d.pos_token = (const int32_t *)(ws + P.off_pos_token);
   d.counters = (int32_t *)(ws + P.off_counters);
   d.part_o = (float *)(ws + P.off_part_o);
   d.part_lse = (float *)(ws + P.off_part_lse);

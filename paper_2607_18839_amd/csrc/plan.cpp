@@ -189,16 +189,67 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
                                         : (int32_t)(P.priv_row[i] + P.past_len[i] + j);
     }
 
+  // ---- stacked positions.  Position i of page p (its rows i * G .. i * G +
+  // G - 1 per kv head) holds token pos_token[page_q_row + i].  With fork
+  // offsets the page's tokens are stacked in descending order of their fork
+  // point (ties keep token order), so that a work item, and each wave of it,
+  // holds rows whose visible prefixes are close: items end at the largest
+  // fork point of their rows and waves skip the key tiles none of their rows
+  // sees.
+  P.pos_token.resize(2 * (size_t)P.T);
+  std::vector<char> page_sorted(np, 0);
+  for (int p = 0; p < np; ++p) {
+    const int q0 = P.page_q_row[p], n = P.page_T[p];
+    std::vector<int32_t> order(n);
+    for (int i = 0; i < n; ++i) order[i] = q0 + i;
+    if (P.has_fork)
+      std::stable_sort(order.begin(), order.end(),
+                       [&](int32_t x, int32_t y) { return P.token_fork[x] > P.token_fork[y]; });
+    for (int i = 0; i < n; ++i) {
+      P.pos_token[2 * (size_t)(q0 + i)] = order[i];
+      P.pos_token[2 * (size_t)(q0 + i) + 1] = P.token_fork[order[i]];
+      if (order[i] != q0 + i) page_sorted[p] = 1;
+    }
+  }
+  // Largest visible prefix among the rows of each (page, row group).
+  const int group_rows = kSharedWaves * kTileRows;
+  std::vector<std::vector<int32_t>> group_fork(np);
+  for (int p = 0; p < np; ++p) {
+    const int R = P.page_T[p] * G;
+    for (int r0 = 0; r0 < R; r0 += group_rows) {
+      int f = 0;
+      for (int r = r0; r < std::min(R, r0 + group_rows); ++r)
+        f = std::max(f, P.pos_token[2 * (size_t)(P.page_q_row[p] + r / G) + 1]);
+      group_fork[p].push_back(f);
+    }
+  }
+
   // ---- partial slots per token
   // Prefix keys per shared work item: a multiple of kSharedSplitUnit, sized so
   // that the shared-prefix work is about one workgroup per CU
   // (kSharedTargetItems); longer items amortise each workgroup's fixed
   // start-up and write-out, and fewer splits mean fewer partials to merge.
+  // Each page's prefix is cut into equal ranges of at most `split` keys
+  // (rounded up to kSharedSplitUnit), so one page's items are balanced.
+  auto split_shape = [&](int p, int64_t split, int32_t &ns, int32_t &sk) {
+    ns = (int32_t)ceil_div(P.prefix_len[p], split);
+    sk = ns > 0 ? (int32_t)(kSharedSplitUnit * ceil_div(ceil_div(P.prefix_len[p], ns), kSharedSplitUnit)) : 0;
+    if (sk > 0) ns = (int32_t)ceil_div(P.prefix_len[p], sk);
+  };
+  // Items for a split length.  With fork offsets, a row group's items stop
+  // at its largest fork point.
   auto shared_items_for = [&](int64_t split) {
     int64_t n = 0;
-    for (int p = 0; p < np; ++p)
-      n += (int64_t)Hkv * ceil_div((int64_t)P.page_T[p] * G, (int64_t)kSharedWaves * kTileRows) *
-           ceil_div(P.prefix_len[p], split);
+    for (int p = 0; p < np; ++p) {
+      if (!P.has_fork) {
+        n += (int64_t)Hkv * (int64_t)group_fork[p].size() * ceil_div(P.prefix_len[p], split);
+        continue;
+      }
+      int32_t ns, sk;
+      split_shape(p, split, ns, sk);
+      if (sk == 0) continue;
+      for (int32_t f : group_fork[p]) n += (int64_t)Hkv * std::min<int64_t>(ns, ceil_div(f, sk));
+    }
     return n;
   };
   // Grow the split until the items fit the target or one split covers every
@@ -213,15 +264,8 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   while (mult < mult_cap && shared_items_for(kSharedSplitUnit * mult) > kSharedTargetItems) ++mult;   // ceilings per page
   // (paged K/V: at most 64 tiles per item, each item's tile rows fit a wave)
   P.split_keys = (int32_t)std::min<int64_t>(kSharedSplitUnit * mult, b.paged ? 4096 : INT32_MAX / 2);
-  // each page's prefix is cut into page_splits[p] ranges of equal length
-  // (rounded up to kSharedSplitUnit), so one page's items are balanced
   std::vector<int32_t> page_splits(np), page_split_keys(np);
-  for (int p = 0; p < np; ++p) {
-    page_splits[p] = (int32_t)ceil_div(P.prefix_len[p], P.split_keys);
-    page_split_keys[p] = page_splits[p] > 0 ? (int32_t)(kSharedSplitUnit *
-        ceil_div(ceil_div(P.prefix_len[p], page_splits[p]), kSharedSplitUnit)) : 0;
-    if (page_split_keys[p] > 0) page_splits[p] = (int32_t)ceil_div(P.prefix_len[p], page_split_keys[p]);
-  }
+  for (int p = 0; p < np; ++p) split_shape(p, P.split_keys, page_splits[p], page_split_keys[p]);
   // Shared splits a branch sees: those starting below its visible prefix
   // (all of its page's splits without fork offsets).  Its tokens' partial
   // slots are those splits, then its private chunks.
@@ -251,7 +295,6 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   // item no row of which sees its first key is not emitted, and a row writes
   // its partial of the split only if it sees the split's first key (the
   // kernels apply the same rule).
-  const int group_rows = kSharedWaves * kTileRows;
   for (int p = 0; p < np; ++p) {
     const int Pp = P.prefix_len[p];
     const int R = P.page_T[p] * G;
@@ -264,12 +307,12 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
           int k1 = std::min(Pp, k0 + page_split_keys[p]);
           int flags = 0;
           if (P.has_fork) {
-            int max_fork = 0;
-            for (int r = r0; r < r0 + nr; ++r) max_fork = std::max(max_fork, P.token_fork[P.page_q_row[p] + r / G]);
+            const int max_fork = group_fork[p][r0 / group_rows];
             if (max_fork <= k0) continue;
             k1 = std::min(k1, max_fork);
             for (int r = r0; r < r0 + nr; ++r)
-              if (P.token_fork[P.page_q_row[p] + r / G] < k1) flags |= SI_FLAG_FORK;
+              if (P.pos_token[2 * (size_t)(P.page_q_row[p] + r / G) + 1] < k1) flags |= SI_FLAG_FORK;
+            if (page_sorted[p]) flags |= SI_FLAG_SORTED;
           }
           int32_t it[SI_NFIELDS] = {};
           it[SI_PAGE] = p; it[SI_KVH] = g; it[SI_ROW0] = r0; it[SI_NROWS] = nr;
@@ -335,6 +378,8 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   off = align256(off + P.token_dest.size() * sizeof(int32_t));
   P.off_token_vis = off;
   off = align256(off + P.visible.size() * sizeof(int32_t));
+  P.off_pos_token = off;
+  off = align256(off + P.pos_token.size() * sizeof(int32_t));
   P.off_counters = off;   // zeroed by the upload; every user resets what it uses
   off = align256(off + kNumCounters * sizeof(int32_t));
   P.table_bytes = off;
@@ -358,6 +403,7 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   put(P.off_token_fork, P.token_fork);
   put(P.off_token_dest, P.token_dest);
   put(P.off_token_vis, P.visible);
+  put(P.off_pos_token, P.pos_token);
 
   *out = std::move(P);
   return HPD_OK;

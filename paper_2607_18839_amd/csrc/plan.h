@@ -39,6 +39,7 @@ constexpr int kSharedSplitUnit = 128;   // shared work items cover multiples of 
 constexpr int kSharedTargetItems = 256; // aim: about one shared-prefix workgroup per CU
 constexpr int kPrivateChunkKeys = 128;  // private keys per private work item
 constexpr int SI_FLAG_FORK = 1;      // rows have their own fork limits
+constexpr int SI_FLAG_SORTED = 2;    // stacked positions map to tokens through pos_token
 constexpr int kNumCounters = 8192;   // self-resetting arrival counters (split-K / merges)
 
 struct Plan {
@@ -64,6 +65,11 @@ struct Plan {
   std::vector<int32_t> token_slots;                   // [T][2]: first slot, count
   std::vector<int32_t> token_fork;                    // [T] visible prefix per token
   std::vector<int32_t> token_dest;                    // [T] private row of token t: priv_row + L + j
+  // [T][2] (token, visible prefix) of each stacked position.  With fork
+  // offsets a page's tokens are stacked in descending order of their fork
+  // point, so that each work item (and each wave of it) holds rows whose
+  // visible prefixes are close; without them position = token.
+  std::vector<int32_t> pos_token;
   // (visible[t] - 1 is token t's position in its branch's sequence)
   int64_t num_slots = 0;                              // partial rows = num_slots * Hq
   int32_t split_keys = 0;                             // prefix keys per shared work item
@@ -78,7 +84,7 @@ struct Plan {
   // device workspace layout (byte offsets, 256-aligned)
   size_t off_shared_tiles = 0, off_priv_tiles = 0, off_branch_q_row = 0, off_branch_new = 0;
   size_t off_shared_items = 0, off_private_items = 0, off_token_slots = 0,
-         off_token_fork = 0, off_token_dest = 0, off_token_vis = 0, off_counters = 0, off_part_o = 0, off_part_lse = 0, table_bytes = 0,
+         off_token_fork = 0, off_token_dest = 0, off_pos_token = 0, off_token_vis = 0, off_counters = 0, off_part_o = 0, off_part_lse = 0, table_bytes = 0,
          workspace_bytes = 0;
   std::vector<unsigned char> table_image;             // host copy of [0, table_bytes)
 

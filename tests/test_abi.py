@@ -65,6 +65,8 @@ def test_work_lists_cover_every_key_once(name, st, Hq, Hkv):
     shared_cov = [np.zeros((Hq, P[cp["token_branch"][t] * 0 + st["branch_page"][cp["token_branch"][t]]]), np.int64)
                   for t in range(T)]
     S, Pi = _lib.SI, _lib.PI
+    # without fork offsets position t holds token t
+    assert np.array_equal(info["pos_token"][:, 0], np.arange(T))
     for it in info["shared_items"]:
         p, g = it[S["page"]], it[S["kvh"]]
         assert it[S["page_q_row"]] == cp["page_q_row"][p] and it[S["prefix_row"]] == cp["prefix_row"][p]
@@ -228,11 +230,28 @@ def test_fork_work_lists_cover_visible_keys_once(name, st, Hq, Hkv):
     S, Pi = _lib.SI, _lib.PI
     slot_writes = np.zeros((info["num_partial_slots"], Hq), np.int64)
     cov = [np.zeros((Hq, int(fork[tb[t]])), np.int64) for t in range(T)]
+    pos = info["pos_token"]
+    # each page's positions hold a permutation of its tokens, by descending
+    # fork point (ties in token order), each with its own fork point
+    for p in range(len(st["prefix_len"])):
+        q0, n = cp["page_q_row"][p], cp["page_T"][p]
+        toks = pos[q0:q0 + n, 0]
+        assert sorted(toks) == list(range(q0, q0 + n))
+        assert np.array_equal(pos[q0:q0 + n, 1], fork[tb[toks]])
+        key = [(-int(fork[tb[t]]), int(t)) for t in toks]
+        assert key == sorted(key)
     for it in info["shared_items"]:
         p, g, k0, k1 = it[S["page"]], it[S["kvh"]], it[S["key0"]], it[S["key1"]]
         assert k0 < k1
-        for r in range(it[S["row0"]], it[S["row0"]] + it[S["nrows"]]):
-            t = cp["page_q_row"][p] + r // G
+        rows = range(it[S["row0"]], it[S["row0"]] + it[S["nrows"]])
+        # the item ends at its split's end or at the largest fork point of its rows
+        max_f = max(int(pos[cp["page_q_row"][p] + r // G, 1]) for r in rows)
+        assert k1 <= max_f and (k1 == max_f or k1 % 128 == 0 or k1 == st["prefix_len"][p])
+        sorted_page = not np.array_equal(pos[cp["page_q_row"][p]:cp["page_q_row"][p] + cp["page_T"][p], 0],
+                                         np.arange(cp["page_q_row"][p], cp["page_q_row"][p] + cp["page_T"][p]))
+        assert bool(it[S["flags"]] & 2) == sorted_page
+        for r in rows:
+            t = int(pos[cp["page_q_row"][p] + r // G, 0])
             h = g * G + r % G
             F = int(fork[tb[t]])
             cov[t][h, k0:min(k1, F)] += 1

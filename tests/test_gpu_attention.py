@@ -90,6 +90,35 @@ def test_fork_lengths():
     assert np.abs(lse - lref).max() <= LSE_ABS
 
 
+FORK_CASES = {
+    # three pages, ragged k and L, forks drawn per branch
+    "three_pages": ([700, 1500, 333], [0, 0, 0, 1, 1, 2, 2, 2], [1, 4, 4, 1, 4, 2, 3, 4],
+                    [10, 50, 0, 5, 200, 64, 1, 9], 16, 2),
+    # G = 12: a token's 12 rows straddle 32-row waves and 128-row items
+    "g12": ([900], [0, 0, 0, 0, 0], [1, 4, 4, 3, 2], [30, 7, 0, 100, 12], 12, 1),
+    # G = 1 and 24 branches: waves of sorted rows that skip most key tiles
+    "g1_many": ([2048], [0] * 24, [1] + [4] * 23, list(range(0, 240, 10)), 4, 4),
+}
+
+
+@pytest.mark.parametrize("case", list(FORK_CASES))
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_fork_sorted_rows(case, dtype):
+    """Fork offsets: the planner stacks each page's tokens by descending fork
+    point and the kernels skip the key tiles a wave's rows do not see."""
+    announce(f"fork sorted {case} {dtype}")
+    b = _custom(*FORK_CASES[case], dtype=dtype, seed=13)
+    rng = np.random.default_rng(len(case))
+    P_b = b.prefix_len[b.branch_page]
+    fork = np.array([rng.integers(0, int(P) + 1) for P in P_b], np.int32)
+    fork[0], fork[-1] = P_b[0], 0
+    b.fork_len = fork
+    O, lse = run_batch(b, fork_len=fork)
+    Oref, lref = attention_for_batch(b)
+    assert_parity(O, Oref, dtype, case)
+    assert np.abs(lse - lref).max() <= LSE_ABS
+
+
 def test_custom_offsets_and_canaries():
     """Rows live at caller-chosen offsets; every row outside the plan is NaN
     and must never be read."""
