@@ -26,7 +26,7 @@ STATUS = {0: "HPD_OK", 1: "HPD_ERR_INVALID_ARGUMENT", 2: "HPD_ERR_UNSUPPORTED",
 # Work-item record widths and fields (paper_2607_18839_amd/csrc/plan.h).
 SI_NFIELDS = PI_NFIELDS = 12
 SI = dict(page=0, kvh=1, row0=2, nrows=3, key0=4, key1=5, slot=6, flags=7, prefix_row=8,
-          page_q_row=9, page_rows=10)
+          page_q_row=9, page_rows=10, pos=11)
 PI = dict(branch=0, kvh=1, row0=2, nrows=3, key0=4, key1=5, slot=6, past=7, priv_row=8,
           q_row=9, num_new=10)
 

@@ -677,7 +677,7 @@ __device__ __forceinline__ int64_t kv_row(const AttnArgs &a, const int32_t *tile
 // else read from the plan's table (a dependent load at the head of every
 // workgroup's chain, which the regular form avoids).
 struct SharedItem {
-  int g, row0, nrows, key0, key1, slot, flags, prefix_row, page_q_row;
+  int g, row0, nrows, key0, key1, slot, flags, prefix_row, page_q_row, pos;
 };
 __device__ __forceinline__ SharedItem shared_item(const AttnArgs &a, int item) {
   SharedItem si;
@@ -693,11 +693,12 @@ __device__ __forceinline__ SharedItem shared_item(const AttnArgs &a, int item) {
     si.flags = 0;
     si.prefix_row = a.reg.prefix_row;
     si.page_q_row = a.reg.page_q_row;
+    si.pos = 0;
   } else {
     const int32_t *it = a.dev.shared_items + (int64_t)item * SI_NFIELDS;
     si.g = it[SI_KVH]; si.row0 = it[SI_ROW0]; si.nrows = it[SI_NROWS];
     si.key0 = it[SI_KEY0]; si.key1 = it[SI_KEY1]; si.slot = it[SI_SLOT]; si.flags = it[SI_FLAGS];
-    si.prefix_row = it[SI_PREFIX_ROW]; si.page_q_row = it[SI_PAGE_Q_ROW];
+    si.prefix_row = it[SI_PREFIX_ROW]; si.page_q_row = it[SI_PAGE_Q_ROW]; si.pos = it[SI_POS];
   }
   return si;
 }
@@ -705,11 +706,13 @@ __device__ __forceinline__ SharedItem shared_item(const AttnArgs &a, int item) {
 // Token of stacked position pos of a shared item's page, and with fork
 // offsets the row's key limit (min of limit and the token's visible
 // prefix).  Sorted pages (fork offsets) map positions through the plan's
-// pos_token table, whose entries also carry the visible prefix.
-__device__ __forceinline__ void row_token(const AttnArgs &a, int flags, int page_q_row, int pos, bool valid,
-                                          int &t, int &limit) {
+// pos_token table (the item's pos field locates the page's entries from
+// token_fork), whose entries also carry the visible prefix.
+__device__ __forceinline__ void row_token(const AttnArgs &a, const SharedItem &si, int pos, bool valid, int &t,
+                                          int &limit) {
+  const int flags = si.flags, page_q_row = si.page_q_row;
   if (flags & SI_FLAG_SORTED) {
-    const int2 e = *(const int2 *)(a.dev.pos_token + 2 * (int64_t)(page_q_row + pos));
+    const int2 e = *(const int2 *)(a.dev.token_fork + si.pos + 2 * (int64_t)pos);
     t = e.x;
     if (valid) limit = min(limit, e.y);
   } else {
@@ -740,11 +743,12 @@ __global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
   const bool valid = rloc < nrows;
   const int R = row0 + rloc;                           // stacked row of (page, g)
   int t, limit = key1;
-  row_token(a, flags, page_q_row, valid ? R / a.G : 0, valid, t, limit);
+  row_token(a, si, valid ? R / a.G : 0, valid, t, limit);
   const int hq = g * a.G + (valid ? R % a.G : 0);
   const bool wave_active = wave * 32 < nrows;
   const int wmin = wave_min(valid ? limit : key1);
-  const int wmax = wave_max(valid ? limit : key0);   // keys past it: no row of the wave sees them
+  // keys past it: no row of the wave sees them
+  const int wmax = (flags & SI_FLAG_FORK) ? __builtin_amdgcn_readfirstlane(wave_max(valid ? limit : key0)) : key1;
 
   const int64_t stride = (int64_t)a.Hkv * D;
   const T *kbase = (const T *)a.shared_k + (int64_t)g * D;
@@ -840,14 +844,168 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   const int rloc = rw * 32 + (lane & 31);
   const bool valid = rloc < nrows;
   const int R = row0 + rloc;                           // stacked row of (page, g)
+  const int t = page_q_row + (valid ? R / a.G : 0);
+  const int hq = g * a.G + (valid ? R % a.G : 0);
+  int limit = key1;
+  if ((flags & SI_FLAG_FORK) && valid) limit = min(limit, a.dev.token_fork[t]);
+  const bool wave_active = rw * 32 < nrows;
+  const int wmin = wave_min(valid ? limit : key1);
+
+  const int64_t stride = (int64_t)a.Hkv * D;
+  const T *kbase = (const T *)a.shared_k + (int64_t)g * D;
+  const T *vbase = (const T *)a.shared_v + (int64_t)g * D;
+  int voff[2];
+  WaveAttn<T>::vt_offsets(lane, voff);
+
+  // copy instructions of this wave for a pair: its parity's tile, K and V
+  // rows 16 rw + lane / 8 and 16 rw + 8 + lane / 8, physical chunk lane % 8
+  const int crow = 16 * rw + (lane >> 3), pch = lane & 7;
+  const int kq0 = Tl::kchunk(crow, pch), kq1 = Tl::kchunk(crow + 8, pch);
+  const int vq0 = vchunk(crow, pch), vq1 = vchunk(crow + 8, pch);
+  const int ntiles = (key1 - key0 + 63) / 64, npairs = (ntiles + 1) / 2;
+  // paged K/V: lane l holds the pool row of the item's tile l (at most 64
+  // tiles per item), read with a uniform lane index when a tile is issued
+  const int tile_row = a.paged && lane < ntiles ? a.dev.shared_tiles[prefix_row + (key0 >> 6) + lane] : 0;
+  auto issue = [&](int j) {
+    unsigned char *st = lds + (j % S) * kPair + par * kTile;
+    const int k0 = key0 + 64 * (2 * j + par);
+    // the last pair's missing odd tile re-reads the item's last tile
+    const int ti = min(2 * j + par, ntiles - 1), kt = key0 + 64 * ti;
+    const int64_t base = a.paged ? (int64_t)__builtin_amdgcn_readlane(tile_row, ti) : (int64_t)prefix_row + kt;
+    const int64_t r0 = base + (min(k0 + crow, key1 - 1) - kt), r1 = base + (min(k0 + crow + 8, key1 - 1) - kt);
+    dma16(kbase + r0 * stride + 8 * kq0, st + 1024 * (2 * rw));
+    dma16(kbase + r1 * stride + 8 * kq1, st + 1024 * (2 * rw + 1));
+    dma16(vbase + r0 * stride + 8 * vq0, st + kTileBytes + 1024 * (2 * rw));
+    dma16(vbase + r1 * stride + 8 * vq1, st + kTileBytes + 1024 * (2 * rw + 1));
+  };
+  // wait until pair j's copies (this wave's 4) have landed, with `ahead`
+  // later pairs still in flight
+  auto wait_pair = [&](int ahead) {
+    if (ahead >= 2) wait_vm<8>();
+    else if (ahead == 1) wait_vm<4>();
+    else wait_vm<0>();
+  };
+  static_assert(kPairRing == 4, "the ring holds pairs j - 1 .. j + 2 at iteration j");
+  // Pair 0, then this lane's Q fragments and partial-row index, then pairs 1
+  // and 2.  Pair 0 and the loads behind it are retired here, so the loop
+  // never waits for the Q loads.
+  if (npairs > 0) issue(0);
+  WaveAttn<T> w;
+  w.init((const T *)a.q + ((int64_t)t * a.Hq + hq) * D, valid, lane);
+  const int my_slots = valid ? a.dev.token_slots[2 * t] : 0;
+  if (npairs > 1) issue(1);
+  if (npairs > 2) issue(2);
+  wait_pair(min(npairs - 1, 2));
+  // a row writes its partial of this split only if it sees the split's first
+  // key (fork offsets: the planner gives it no slot otherwise)
+  const int my_prow = valid && limit > key0 ? (my_slots + slot) * a.Hq + hq : -1;
+  ring_barrier();   // pair 0 visible to every wave
+  f32x16 s_cur[2], s_next[2];
+  if (wave_active && par < ntiles) w.qk_ring(lds + par * kTile, s_cur, lane);
+  for (int j = 0; j < npairs; ++j) {
+    // pair j + 1 visible; the slot of pair j - 1 (read in iteration j - 1) is free
+    if (j + 1 < npairs) {
+      wait_pair(min(npairs - 1, j + 2) - (j + 1));
+      ring_barrier();
+      if (j + 3 < npairs) issue(j + 3);
+    }
+    const int ti = 2 * j + par;
+    if (wave_active && ti < ntiles) {
+      const unsigned char *kt_next = ti + 2 < ntiles ? lds + ((j + 1) % S) * kPair + par * kTile : nullptr;
+      const int k0 = key0 + 64 * ti;
+      w.step_ring(kt_next, lds + (j % S) * kPair + par * kTile + kTileBytes, voff, s_cur, s_next, k0, limit,
+                  k0 + 64 > wmin, a.c, lane);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) { s_cur[0][r] = s_next[0][r]; s_cur[1][r] = s_next[1][r]; }
+    }
+  }
+  ring_barrier();   // every wave is done with the ring; its LDS becomes scratch
+  w.l = w.lsum[0];  // the query's whole sum (see tile_ring)
+  // odd-tile waves hand (m, l, O) to their even-tile partners
+  float *xch = (float *)lds + rw * (34 * 64);
+  if (par == 1 && wave_active) {
+    xch[lane] = w.m;
+    xch[64 + lane] = w.l;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      xch[(2 + r) * 64 + lane] = w.o[0][r];
+      xch[(18 + r) * 64 + lane] = w.o[1][r];
+    }
+  }
+  __syncthreads();
+  if (par == 1 || !wave_active) return;
+  {
+    f32x16 o2[2];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      o2[0][r] = xch[(2 + r) * 64 + lane];
+      o2[1][r] = xch[(18 + r) * 64 + lane];
+    }
+    w.combine(xch[lane], xch[64 + lane], o2);
+  }
+  auto prow_of = [&](int r) -> int64_t { return __shfl(my_prow, r); };
+  w.write_f16(lds + 4 * 34 * 64 * 4 + rw * 4096, (_Float16 *)a.dev.part_o, a.dev.part_lse, prow_of, lane, true);
+}
+
+// The bf16 kernel for plans with fork offsets: the same work as
+// shared_prefix_ring_kernel, with each page's stacked positions mapped to
+// tokens through the plan's pos_token table (items with SI_FLAG_SORTED) and
+// each wave skipping the compute of the key tiles none of its rows sees.  It
+// is a kernel of its own because folding these steps into
+// shared_prefix_ring_kernel, even behind a compile-time switch, measured
+// 0.1 - 0.3 us slower per launch on plans without fork offsets (same-box A/B
+// of the 18-layer step: 0.760 -> 0.765 ms).
+__global__ __launch_bounds__(512) void shared_prefix_ring_fork_kernel(AttnArgs a) {
+  using T = __bf16;
+  using Tl = Tile<T>;
+  constexpr int S = kPairRing, kTileBytes = 64 * 128, kTile = 2 * kTileBytes, kPair = 2 * kTile;
+  constexpr int kRingBytes = S * kPair, kPrivBytes = kPrivMaxPerWG * kPrivWaveBytes;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[kRingBytes > kPrivBytes ? kRingBytes : kPrivBytes];
+
+  // Workgroups run either priv_per_wg private items or one shared item.  Both
+  // ranges are rounded up to multiples of 8 so that the shared items keep
+  // the XCD-aware order of the other kernels.  priv_first (the grid fits the
+  // chip in one round): the private range comes first, so the longer
+  // dependency chain of a private item starts first; otherwise the shared
+  // items, the larger work, are dispatched first and the private items fill
+  // in behind them.
+  // (the private slot count comes from the host: a division by the runtime
+  // items per workgroup would delay every workgroup's start)
+  const int n_priv_slots = a.priv_slots, n_shared_slots = (a.n_shared + 7) / 8 * 8;
+  const int priv0 = a.priv_first ? 0 : n_shared_slots, shared0 = a.priv_first ? n_priv_slots : 0;
+  const int bid = blockIdx.x;
+  if (bid >= priv0 && bid < priv0 + n_priv_slots) {
+    // wave-uniform (scalar loads of the item's fields)
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), pi = (bid - priv0) * a.priv_per_wg + wave;
+    if (wave < a.priv_per_wg && pi < a.n_private)
+      private_item_ring(a, pi, threadIdx.x & 63, lds + wave * kPrivWaveBytes);
+    return;
+  }
+  const int b = bid - shared0, per_xcd = n_shared_slots / 8;
+  if (b < 0 || b >= n_shared_slots) return;
+  const int item = (b % 8) * per_xcd + b / 8;
+  if (item >= a.n_shared) return;
+  const SharedItem si = shared_item(a, item);
+  const int g = si.g, row0 = si.row0, nrows = si.nrows;
+  const int key0 = si.key0, key1 = si.key1, slot = si.slot, flags = si.flags;
+  const int prefix_row = si.prefix_row, page_q_row = si.page_q_row;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int rw = wave & 3, par = wave >> 2;             // row group, key-tile parity
+  const int rloc = rw * 32 + (lane & 31);
+  const bool valid = rloc < nrows;
+  const int R = row0 + rloc;                           // stacked row of (page, g)
   int t, limit = key1;
-  row_token(a, flags, page_q_row, valid ? R / a.G : 0, valid, t, limit);
+  row_token(a, si, valid ? R / a.G : 0, valid, t, limit);
   const int hq = g * a.G + (valid ? R % a.G : 0);
   const bool wave_active = rw * 32 < nrows;
   const int wmin = wave_min(valid ? limit : key1);
   // key tiles of the item that some row of this wave sees (fork offsets:
   // the rest are skipped; their copies are still issued for the others)
-  const int ntw = max(0, (min(key1, wave_max(valid ? limit : key0)) - key0 + 63) / 64);
+  // (wave-uniform, in a scalar register, so the loop's tests stay scalar branches)
+  int ntw = (key1 - key0 + 63) / 64;
+  if (flags & SI_FLAG_FORK)
+    ntw = __builtin_amdgcn_readfirstlane(max(0, (min(key1, wave_max(valid ? limit : key0)) - key0 + 63) / 64));
 
   const int64_t stride = (int64_t)a.Hkv * D;
   const T *kbase = (const T *)a.shared_k + (int64_t)g * D;
@@ -1182,7 +1340,6 @@ PlanDev plan_dev(const Plan &P, void *workspace) {
   d.token_fork = (const int32_t *)(ws + P.off_token_fork);
   d.token_dest = (const int32_t *)(ws + P.off_token_dest);
   d.token_vis = (const int32_t *)(ws + P.off_token_vis);
-  d.pos_token = (const int32_t *)(ws + P.off_pos_token);
   d.counters = (int32_t *)(ws + P.off_counters);
   d.part_o = (float *)(ws + P.off_part_o);
   d.part_lse = (float *)(ws + P.off_part_lse);
@@ -1229,16 +1386,17 @@ hipError_t launch_branch_attention(const Plan &P, const void *q, const void *sha
       x.priv_slots = priv_slots(x);
     };
     fit(a);
+    auto ring = P.has_fork ? shared_prefix_ring_fork_kernel : shared_prefix_ring_kernel;
     if (attn_phase_isolation()) {
       AttnArgs sh = a, pr = a;
       sh.n_private = 0;
       pr.n_shared = 0;
       fit(sh);
       fit(pr);
-      if (sh.n_shared > 0) launch(KK_SHARED, shared_prefix_ring_kernel, dim3(grid(sh)), dim3(512), stream, sh);
-      if (pr.n_private > 0) launch(KK_PRIVATE, shared_prefix_ring_kernel, dim3(grid(pr)), dim3(512), stream, pr);
+      if (sh.n_shared > 0) launch(KK_SHARED, ring, dim3(grid(sh)), dim3(512), stream, sh);
+      if (pr.n_private > 0) launch(KK_PRIVATE, ring, dim3(grid(pr)), dim3(512), stream, pr);
     } else if (grid(a) > 0) {
-      launch(KK_SHARED, shared_prefix_ring_kernel, dim3(grid(a)), dim3(512), stream, a);
+      launch(KK_SHARED, ring, dim3(grid(a)), dim3(512), stream, a);
     }
   } else {
     if (a.n_shared > 0)

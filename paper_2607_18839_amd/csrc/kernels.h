@@ -20,7 +20,6 @@ struct PlanDev {
   const int32_t *token_fork;
   const int32_t *token_dest;
   const int32_t *token_vis;   // [T] visible keys of token t (its position + 1)
-  const int32_t *pos_token;   // [T][2] token and visible prefix of each stacked position
   int32_t *counters;
   float *part_o;
   float *part_lse;

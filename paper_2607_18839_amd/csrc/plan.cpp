@@ -389,6 +389,11 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   off = align256(off + (size_t)P.num_slots * Hq * sizeof(float));
   P.workspace_bytes = off;
 
+  // sorted items find their page's stacked positions from the token_fork table
+  for (size_t i = 0; i < P.shared_items.size(); i += SI_NFIELDS)
+    if (P.shared_items[i + SI_FLAGS] & SI_FLAG_SORTED)
+      P.shared_items[i + SI_POS] =
+          (int32_t)((P.off_pos_token - P.off_token_fork) / sizeof(int32_t) + 2 * (size_t)P.shared_items[i + SI_PAGE_Q_ROW]);
   P.table_image.assign(P.table_bytes, 0);
   auto put = [&](size_t at, const std::vector<int32_t> &v) {
     if (!v.empty()) std::memcpy(P.table_image.data() + at, v.data(), v.size() * sizeof(int32_t));

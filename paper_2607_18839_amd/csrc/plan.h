@@ -21,8 +21,10 @@ namespace hpd {
 // private tile table.
 enum SharedItemField {
   SI_PAGE = 0, SI_KVH, SI_ROW0, SI_NROWS, SI_KEY0, SI_KEY1, SI_SLOT, SI_FLAGS,
-  SI_PREFIX_ROW, SI_PAGE_Q_ROW, SI_PAGE_ROWS, SI_RESERVED, SI_NFIELDS
+  SI_PREFIX_ROW, SI_PAGE_Q_ROW, SI_PAGE_ROWS, SI_POS, SI_NFIELDS
 };
+// SI_POS (items with SI_FLAG_SORTED): the page's first pos_token entry, in
+// int32 elements from the start of the token_fork table.
 // Work item of the private kernel: one wave, one 32-row tile of the stacked
 // rows of (branch, kv head), private keys [key_begin, key_end) of the branch.
 // Stacked row r of (branch b, kv head g) is query head g * G + r % G of the
