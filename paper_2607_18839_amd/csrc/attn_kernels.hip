@@ -1256,6 +1256,9 @@ __global__ __launch_bounds__(64) void private_kernel_f32(AttnArgs a) {
 template <typename TO, typename TP>
 __global__ __launch_bounds__(256) void merge_kernel(PlanDev dev, TO *out, float *lse, int T, int Hq,
                                                     int out_packed) {
+  // every argument in one round trip to the argument segment
+  asm volatile("" ::"s"(T), "s"(Hq), "s"(dev.token_slots), "s"(dev.part_o), "s"(dev.part_lse), "s"(out), "s"(lse),
+               "s"(out_packed));
   constexpr int B = 16;
   const int row = blockIdx.x * 16 + (threadIdx.x >> 4);
   if (row >= T * Hq) return;

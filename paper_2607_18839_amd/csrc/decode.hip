@@ -90,6 +90,9 @@ DecodeLayout decode_layout(const hpd_model_desc &m, const Plan &P) {
 __global__ __launch_bounds__(256) void qk_norm_rope_kernel(PlanDev dev, __bf16 *q, __bf16 *k_cache, int T, int Hq,
                                                            int Hkv, const __bf16 *gq, const __bf16 *gk, float eps,
                                                            float theta) {
+  // the arguments in one round trip to the argument segment
+  asm volatile("" ::"s"(dev.token_dest), "s"(dev.token_vis), "s"(q), "s"(k_cache), "s"(T), "s"(Hq), "s"(Hkv), "s"(gq),
+               "s"(gk), "s"(eps), "s"(theta));
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, nh = Hq + Hkv;
   const int64_t item = (int64_t)blockIdx.x * 4 + wave;   // (token, head)
   if (item >= (int64_t)T * nh) return;

@@ -113,6 +113,9 @@ __global__ __launch_bounds__(256) void verify_kernel(PlanDev dev, int nb, int nt
                                                      float *f, int32_t *cur_tok) {
   __shared__ int ystar[HPD_MAX_K];
   __shared__ int acc_n;
+  // the arguments in one round trip to the argument segment
+  asm volatile("" ::"s"(dev.branch_q_row), "s"(dev.branch_new), "s"(nb), "s"(ntile), "s"(amax), "s"(tokens_in),
+               "s"(hidden), "s"(H), "s"(f), "s"(cur_tok));
   const int b = blockIdx.x;
   float *fr = f + (int64_t)b * H;
   if (b >= nb) {   // padding rows of the draft state stay finite
@@ -228,6 +231,8 @@ __global__ __launch_bounds__(256) void embed_kernel(const __bf16 *embed, int V, 
                                                     float *out) {
   typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
   typedef float f32x4 __attribute__((ext_vector_type(4)));
+  // the arguments in one round trip to the argument segment
+  asm volatile("" ::"s"(embed), "s"(V), "s"(H), "s"(tokens), "s"(out));
   const int t = blockIdx.x, tok = tokens[t];
   const bool ok = tok >= 0 && tok < V;
   for (int c = 4 * threadIdx.x; c < H; c += 1024) {
