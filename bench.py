@@ -204,12 +204,12 @@ def _kernel_pass(torch, _lib, step, K, W, queue_cycles=20_000_000):
             if not k.startswith("_") and c}
 
 
-def _phase_pass(torch, _lib, step, K, W, work, queue_cycles=2_000_000, measured=False):
+def _phase_pass(torch, _lib, step, K, W, work, queue_cycles=2_000_000, measured=False, workload="c4"):
     """Per-kernel durations with the attention phases in launches of their own
     (hpd_attn_phase_isolation): the shared-prefix items alone (MFMA-bound) and
     the private items alone (HBM-bound), next to the co-scheduled launch.
     measured: also the rocprofv3-measured HBM bytes of each phase launch
-    (profiles/traffic_c4.md, taken on the c4 step) and the rate they give."""
+    (profiles/traffic_<workload>.md) and the rate they give."""
     _lib.hpd_attn_phase_isolation(True)
     try:
         kern = _kernel_pass(torch, _lib, step, K, W, queue_cycles)
@@ -227,7 +227,7 @@ def _phase_pass(torch, _lib, step, K, W, work, queue_cycles=2_000_000, measured=
         out["private_hbm_frac"] = work["private_bytes"] / pr / 1e3 / HBM_PEAK_GBS
     if measured:
         for phase, us in (("shared_phase", sh), ("private_phase", pr)):
-            tb = _traffic(phase)
+            tb = _traffic(phase, workload)
             if us and tb:
                 out[phase + "_measured_bytes"] = tb
                 out[phase + "_measured_gbs"] = tb / us / 1e3
@@ -280,15 +280,16 @@ def _to_pool(torch, t, rows, n_rows):
     return out
 
 
-def _traffic(kind):
-    """HBM bytes per launch of kernel kind from profiles/traffic_c4.md (rocprofv3
-    FETCH_SIZE / WRITE_SIZE runs scaled by a plain copy kernel's readings), or
-    None when the kernel's source has changed since the counters were taken."""
+def _traffic(kind, workload="c4"):
+    """HBM bytes per launch of kernel kind from profiles/traffic_<workload>.md
+    (rocprofv3 FETCH_SIZE / WRITE_SIZE runs scaled by a plain copy kernel's
+    readings), or None when there is no such summary or the kernel's source
+    has changed since the counters were taken."""
     import hashlib
     import re
     root = os.path.dirname(os.path.abspath(__file__))
     try:
-        text = open(os.path.join(root, "profiles", "traffic_c4.md")).read()
+        text = open(os.path.join(root, "profiles", f"traffic_{workload}.md")).read()
         block = json.loads(re.search(r"```json\n(.*?)```", text, re.S).group(1))
         k = block["kernels"][kind]
         src = os.path.join(root, "paper_2607_18839_amd", "csrc", k["source"])
@@ -356,12 +357,14 @@ def bench_attention(args, torch, _lib):
         kern["private"].update(bytes=w["private_bytes"], gbs=w["private_bytes"] / pr / 1e3,
                                hbm_frac=w["private_bytes"] / pr / 1e3 / HBM_PEAK_GBS)
     if b.dtype == "bf16":
-        kern["phases_isolated"] = _phase_pass(torch, _lib, step, min(args.steps, 20), args.warmup, w)
+        kern["phases_isolated"] = _phase_pass(torch, _lib, step, min(args.steps, 20), args.warmup, w,
+                                              measured=not args.paged, workload=args.workload)
     roof = None
     if sh:
         ach = sh_flop / sh / 1e6
         roof = {"bound": "mfma", "kernel": "shared_prefix", "achieved": ach, "peak": peak_mfma,
-                "unit": "TFLOP/s", "frac": ach / peak_mfma, "traffic": None,
+                "unit": "TFLOP/s", "frac": ach / peak_mfma,
+                "traffic": None if args.paged else _traffic("shared_prefix", args.workload),
                 "algorithmic_per_launch": sh_flop}
     res = {
         "metric": "branch-tokens/s per decode step", "value": w["T"] / (ms / 1e3), "unit": "branch-tokens/s",
@@ -490,12 +493,14 @@ def bench_decode(args, torch, _lib):
     kern["phases_isolated"] = _phase_pass(torch, _lib, step, min(args.steps, 10), args.warmup, aw,
                                           measured=args.workload == "c4" and not args.paged)
     d = kern[dom]
+    # the measured bytes belong to the c4 step with packed weights and contiguous K/V
+    tr = _traffic(dom) if args.workload == "c4" and not args.paged and args.weights == "packed" else None
     if d.get("bound") == "mfma":
         roof = {"bound": "mfma", "kernel": dom, "achieved": d["tflops"], "peak": BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": d["frac"], "traffic": _traffic(dom), "algorithmic_per_launch": d["flop"]}
+                "unit": "TFLOP/s", "frac": d["frac"], "traffic": tr, "algorithmic_per_launch": d["flop"]}
     else:
         roof = {"bound": "hbm", "kernel": dom, "achieved": d.get("gbs"), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": d.get("frac"), "traffic": _traffic(dom), "algorithmic_per_launch": d.get("bytes")}
+                "frac": d.get("frac"), "traffic": tr, "algorithmic_per_launch": d.get("bytes")}
     res = {
         "metric": "branch-tokens/s per decode step", "value": T / (ms / 1e3), "unit": "branch-tokens/s",
         "n_gpus": 1, "steps": timed, "warmup": args.warmup, "ms_per_step": ms, "latency_ms": pct,
