@@ -16,7 +16,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libhpd.so")
-PEAKS = os.path.join(PKG, "peaks")   # microbenchmark executable of the box's own peaks (run by hand)
+PEAKS = os.path.join(PKG, "peaks")   # microbenchmark of the box's own peaks (bench.py runs it for box_peaks)
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
