@@ -250,7 +250,7 @@ __device__ __forceinline__ void ring_barrier() { asm volatile("s_waitcnt lgkmcnt
 template <typename T> struct WaveAttn {
   Frag<T> qf[4];      // Q^T operand for the 4 contraction steps of D = 64
   f32x16 o[2];        // O^T accumulators: dims 0..31 and 32..63
-  f32x16 lsum;        // tile_ring: row sums of P on the matrix core (every register = l)
+  f32x16 lsum;        // step_ring: row sums of P on the matrix core (every register = l)
   float m;            // running max of the scaled log2 scores of this query
   float l;            // this lane's share of the running sum (tile())
   int half;           // lane / 32
@@ -366,10 +366,15 @@ template <typename T> struct WaveAttn {
   // reads and run while the VALU does the softmax of this tile's raw scores
   // s_cur, then this tile's PV and row-sum MFMAs.  (Measured: giving the
   // two waves of a SIMD opposite orders, QK^T last on one of them, is
-  // slower.)  FSUM: the row sums are instead taken
-  // in fp32 on the VALU into l (this lane's half of the keys), which keeps
-  // the exported log-sum-exp exact to fp32 rounding when a row sees only a
-  // few keys (the matrix-core sum adds bf16-rounded probabilities).
+  // slower.)  The running max is raised only when a score exceeds it by
+  // more than 2^8 (log2 units): the probabilities then stay <= 256, and the
+  // O / row-sum rescale is skipped for the (common) tiles that do not raise
+  // it.  The row sums are taken on the matrix core (an all-ones A operand
+  // makes every output row of lsum the sum over the tile's keys).  FSUM: they
+  // are instead taken in fp32 on the VALU into l (this lane's half of the
+  // keys), which keeps the exported log-sum-exp exact to fp32 rounding when a
+  // row sees only a few keys (the matrix-core sum adds bf16-rounded
+  // probabilities).
   template <bool FSUM = false>
   __device__ __forceinline__ void step_ring(const unsigned char *kt_next, const unsigned char *vt, const int (&voff)[2],
                                             f32x16 (&s_cur)[2], f32x16 (&s_next)[2], int key0, int limit,
@@ -479,81 +484,6 @@ template <typename T> struct WaveAttn {
     }
   }
 
-  // bf16 tile from the LDS ring: K tile kt (Tile<bf16> swizzle), V tile vt.
-  // Same arithmetic as tile() apart from the lazily raised max (see
-  // softmax_pv_ring).
-  __device__ __forceinline__ void tile_ring(const unsigned char *kt, const unsigned char *vt, const int (&voff)[2],
-                                            int key0, int limit, bool masked, float c, int lane) {
-    f32x16 s[2];
-    qk_ring(kt, s, lane);
-    softmax_pv_ring(s, vt, voff, key0, limit, masked, c, lane);
-  }
-
-  // Softmax of raw scores s (tile with first key key0) and O^T += V^T P^T
-  // from the V tile vt ([key][dims], vchunk swizzle).  voff: this lane's
-  // transpose-read offsets for dims blocks 0 and 1 (see vt_offsets).  The
-  // running max is only raised when a score exceeds it by more than 2^8
-  // (log2 units): the probabilities then stay <= 256, and the O / l rescale
-  // is skipped for the (common) tiles that do not raise it.
-  __device__ __forceinline__ void softmax_pv_ring(f32x16 (&s)[2], const unsigned char *vt, const int (&voff)[2],
-                                                  int key0, int limit, bool masked, float c, int lane) {
-    if (masked) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = key0 + 32 * kb + (r >> 2) * 8 + 4 * half + (r & 3);
-          if (key >= limit) s[kb][r] = -INFINITY;
-        }
-    }
-    float mx = s[0][0];
-#pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
-#pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32)) * c;
-    if (__ballot(mx > m + 8.f)) {   // wave-uniform: some query's max grew by > 2^8
-      const float m_new = fmaxf(m, mx);
-      const float alpha = __builtin_amdgcn_exp2f(m - (m_new == -INFINITY ? 0.f : m_new));
-      m = m_new;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) { o[0][r] *= alpha; o[1][r] *= alpha; lsum[r] *= alpha; }
-    }
-    const float m_use = m == -INFINITY ? 0.f : m;
-    float p[32];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      p[r] = __builtin_amdgcn_exp2f(fmaf(s[0][r], c, -m_use));
-      p[16 + r] = __builtin_amdgcn_exp2f(fmaf(s[1][r], c, -m_use));
-    }
-    Frag<T> pf[4];
-#pragma unroll
-    for (int st = 0; st < 4; ++st) from_f32(pf[st], p + 8 * st);
-    // row sums of the (bf16) probabilities on the matrix core: an all-ones
-    // A operand makes every output row of lsum the sum over the tile's keys
-    Frag<T> ones;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) ones.v[e] = (__bf16)1.f;
-#pragma unroll
-    for (int st = 0; st < 4; ++st) mma(lsum, ones, pf[st]);
-    // PV step st, lane half h, element e contracts key
-    // 32 (st / 2) + 16 (st % 2) + 8 (e / 4) + 4 h + e % 4 (the S^T register
-    // order of p); dims block b: lane group g = lane / 16 covers dims
-    // 32 b + 16 (g % 2) + (lane % 16).
-    u32x2t vr[16];   // [b][st][hh]
-    ds_read_tr16_tile<0>(vr, vt + voff[0], vt + voff[1]);
-    lds_wait_tr(vr);
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int st = 0; st < 4; ++st) {
-        Frag<T> va;
-        va.v = __builtin_bit_cast(bf16x8, u32x4{vr[(b * 4 + st) * 2][0], vr[(b * 4 + st) * 2][1],
-                                                vr[(b * 4 + st) * 2 + 1][0], vr[(b * 4 + st) * 2 + 1][1]});
-        mma(o[b], va, pf[st]);
-      }
-  }
-
   // Transpose-read offsets (bytes, within a V tile) of this lane for dims
   // blocks 0 and 1 at key offset 0: the lane addresses key 4 h + (lane % 16) / 4
   // and dims 32 b + 16 ((lane / 16) % 2) + 4 (lane % 4).  Adding 8, 16 or 32
@@ -588,7 +518,7 @@ template <typename T> struct WaveAttn {
   // dims] (16-byte chunk q of row r at q ^ (r & 7)), and are stored back 8
   // whole 128-byte rows per instruction.  prow_of(r) gives the partial row of
   // the wave's row r (lane % 32 order), or -1 for a row without a query.
-  // l_total: l already holds the query's whole sum (tile_ring), rather than
+  // l_total: l already holds the query's whole sum (step_ring), rather than
   // this lane's share of it (tile()).
   template <typename RowFn>
   __device__ __forceinline__ void write_f16(unsigned char *scratch, _Float16 *part_o, float *part_lse,
@@ -920,7 +850,7 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
     }
   }
   ring_barrier();   // every wave is done with the ring; its LDS becomes scratch
-  w.l = w.lsum[0];  // the query's whole sum (see tile_ring)
+  w.l = w.lsum[0];  // the query's whole sum (the row-sum MFMAs of step_ring)
   // odd-tile waves hand (m, l, O) to their even-tile partners
   float *xch = (float *)lds + rw * (34 * 64);
   if (par == 1 && wave_active) {
@@ -1076,7 +1006,7 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_fork_kernel(AttnArgs a
     }
   }
   ring_barrier();   // every wave is done with the ring; its LDS becomes scratch
-  w.l = w.lsum[0];  // the query's whole sum (see tile_ring)
+  w.l = w.lsum[0];  // the query's whole sum (the row-sum MFMAs of step_ring)
   // odd-tile waves hand (m, l, O) to their even-tile partners
   float *xch = (float *)lds + rw * (34 * 64);
   if (par == 1 && wave_active) {
