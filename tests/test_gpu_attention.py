@@ -53,6 +53,11 @@ EDGE = {
     "tiny": ([1], [0, 0, 0], [1, 1, 1], [0, 0, 0], 8, 2),
     # a page with no branches between two pages with branches
     "idle_page": ([33, 500, 257], [0, 2, 2], [4, 4, 1], [10, 127, 128], 16, 2),
+    # a prefix ten times the workloads' longest: many splits per row group
+    "long_prefix": ([40000], [0] * 5, [1, 4, 4, 4, 3], [512, 7, 130, 0, 64], 16, 2),
+    # private histories far beyond the workloads' 1024 clip: 40 private chunks
+    # and more than 16 partial slots per token (several merge batches)
+    "long_private": ([64], [0, 0, 0], [4, 1, 4], [5000, 3071, 129], 16, 2),
 }
 
 
