@@ -1178,43 +1178,54 @@ __global__ __launch_bounds__(64) void private_kernel_f32(AttnArgs a) {
 
 // ------------------------------------------------------------ merge kernel
 
-// 16 threads per (token, head) row, 4 dims each, 8 rows per 128-thread
-// workgroup (measured against 16 rows per 256 threads: the c4 step
-// 0.749 -> 0.747 ms, the 16-page merge 6.8 -> 6.4 us; 32 and 64 rows per
-// workgroup were slower, 4 rows no faster).  Partial lse values are in
-// log2 units; the exported lse is natural-log.  One pass over the partials in
-// batches of 16 (every load of a batch issued before its first use), with a
-// running max: sum_i 2^(lse_i - m) O_i / sum_i 2^(lse_i - m), partials in
-// slot order.
-template <typename TO, typename TP>
+// TPR threads per (token, head) row, D / TPR dims each, 128-thread
+// workgroups.  Partial lse values are in log2 units; the exported lse is
+// natural-log.  One pass over the partials in batches of 16 (every load of
+// a batch issued before its first use), with a running max:
+// sum_i 2^(lse_i - m) O_i / sum_i 2^(lse_i - m), partials in slot order.
+// The host takes TPR = 16 for up to kMergeWideRows rows (the launch is
+// latency-bound: more, smaller workgroups) and TPR = 8 above (throughput-
+// bound: half the loads, each twice as wide).  Measured: 16 threads per row
+// in 128-thread workgroups against 256-thread ones, the c4 step 0.749 ->
+// 0.747 ms (32 and 64 rows per workgroup slower, 4 no faster); 8 threads per
+// row: the 16-page merge (21,312 rows) 6.4 -> 4.6 us, while at 2,064 rows
+// (c4) the narrow form stays the faster.
+constexpr int kMergeWideRows = 4096;
+template <typename TO, typename TP, int TPR>
 __global__ __launch_bounds__(128) void merge_kernel(PlanDev dev, TO *out, float *lse, int T, int Hq,
                                                     int out_packed) {
   // every argument in one round trip to the argument segment
   asm volatile("" ::"s"(T), "s"(Hq), "s"(dev.token_slots), "s"(dev.part_o), "s"(dev.part_lse), "s"(out), "s"(lse),
                "s"(out_packed));
-  constexpr int B = 16;
-  const int row = blockIdx.x * 8 + (threadIdx.x >> 4);
+  static_assert(TPR == 8 || TPR == 16, "threads per row");
+  constexpr int B = 16, DPT = D / TPR, NV = DPT / 4;   // dims per thread, in 4-wide vectors
+  const int row = blockIdx.x * (128 / TPR) + (int)threadIdx.x / TPR;
   if (row >= T * Hq) return;
-  const int sub = threadIdx.x & 15;
+  const int sub = threadIdx.x % TPR;
   const int t = row / Hq, h = row % Hq;
   const int first = dev.token_slots[2 * t], cnt = dev.token_slots[2 * t + 1];
   const float *lse_p = dev.part_lse + (int64_t)first * Hq + h;
-  const TP *o_p = (const TP *)dev.part_o + ((int64_t)first * Hq + h) * D + 4 * sub;
+  const TP *o_p = (const TP *)dev.part_o + ((int64_t)first * Hq + h) * D + DPT * sub;
   float m = -INFINITY, wsum = 0.f;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  f32x4 acc[NV];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) acc[v] = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int i0 = 0; i0 < cnt; i0 += B) {
     float lb[B];
-    f32x4 ob[B];
+    f32x4 ob[B][NV];
 #pragma unroll
     for (int i = 0; i < B; ++i) {
       const int64_t j = min(i0 + i, cnt - 1);
       lb[i] = lse_p[j * Hq];
       if constexpr (sizeof(TP) == 2) {
-        typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
-        const f16x4 h4 = *(const f16x4 *)(o_p + j * Hq * D);
-        ob[i] = f32x4{(float)h4[0], (float)h4[1], (float)h4[2], (float)h4[3]};
+        typedef _Float16 f16xN __attribute__((ext_vector_type(DPT)));
+        const f16xN hv = *(const f16xN *)(o_p + j * Hq * D);
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+          ob[i][v] = f32x4{(float)hv[4 * v], (float)hv[4 * v + 1], (float)hv[4 * v + 2], (float)hv[4 * v + 3]};
       } else {
-        ob[i] = *(const f32x4 *)(o_p + j * Hq * D);
+#pragma unroll
+        for (int v = 0; v < NV; ++v) ob[i][v] = *(const f32x4 *)(o_p + j * Hq * D + 4 * v);
       }
     }
     float mb = m;
@@ -1224,27 +1235,35 @@ __global__ __launch_bounds__(128) void merge_kernel(PlanDev dev, TO *out, float 
     const float mu = mb == -INFINITY ? 0.f : mb;
     const float alpha = __builtin_amdgcn_exp2f(m - mu);   // 0 on the first batch (m = -inf)
     wsum *= alpha;
-    acc *= alpha;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) acc[v] *= alpha;
 #pragma unroll
     for (int i = 0; i < B; ++i) {
       if (i0 + i < cnt) {
         const float wgt = __builtin_amdgcn_exp2f(lb[i] - mu);
         wsum += wgt;
-        acc += wgt * ob[i];
+#pragma unroll
+        for (int v = 0; v < NV; ++v) acc[v] += wgt * ob[i][v];
       }
     }
     m = mb;
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-  // out is [T][Hq * D], row-major or (16-bit outputs only) packed
-  TO *dst = out + (out_packed ? packed_offset(t, h * D + 4 * sub, Hq * D) : (int64_t)row * D + 4 * sub);
+  // out is [T][Hq * D], row-major or (16-bit outputs only) packed; a
+  // thread's DPT (4 or 8) columns start at a multiple of DPT, so they are
+  // contiguous in the packed layout too
+  TO *dst = out + (out_packed ? packed_offset(t, h * D + DPT * sub, Hq * D) : (int64_t)row * D + DPT * sub);
   if constexpr (sizeof(TO) == 2) {
-    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-    bf16x4 r;
-    for (int e = 0; e < 4; ++e) r[e] = (__bf16)(acc[e] * inv);
-    *(bf16x4 *)dst = r;
+    typedef __bf16 bf16xN __attribute__((ext_vector_type(DPT)));
+    bf16xN r;
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) r[4 * v + e] = (__bf16)(acc[v][e] * inv);
+    *(bf16xN *)dst = r;
   } else {
-    *(f32x4 *)dst = acc * inv;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) *(f32x4 *)(dst + 4 * v) = acc[v] * inv;
   }
   if (lse && sub == 0) lse[row] = wsum > 0.f ? (m + __builtin_amdgcn_logf(wsum)) * kLn2 : -INFINITY;
 }
@@ -1340,15 +1359,24 @@ hipError_t launch_branch_attention(const Plan &P, const void *q, const void *sha
     if (a.n_private > 0) launch(KK_PRIVATE, private_kernel_f32, dim3(a.n_private), dim3(64), stream, a);
   }
   const int rows = P.T * P.attn.num_q_heads;
-  const dim3 mgrid((rows + 7) / 8), mblock(128);
   const int T = P.T, Hq = P.attn.num_q_heads;
+  const bool wide = rows > kMergeWideRows;
+  const dim3 mgrid(wide ? (rows + 15) / 16 : (rows + 7) / 8), mblock(128);
   // bf16 inputs: fp16 partials; fp32 inputs: fp32 partials
+  // The narrow instances are named first, so that they are emitted first,
+  // right behind the attention kernels.  (Measured: with the wide ones
+  // first, the c4 step ran 0.747 -> 0.750 ms, the narrow merge itself no
+  // slower: the code's placement in the library moves the step by that much.)
+  auto merge = [&](auto k16, auto k8, auto *o, int packed) {
+    if (wide) launch(KK_MERGE, k8, mgrid, mblock, stream, a.dev, o, lse, T, Hq, packed);
+    else launch(KK_MERGE, k16, mgrid, mblock, stream, a.dev, o, lse, T, Hq, packed);
+  };
   if (P.attn.out_dtype == HPD_BF16) {
-    if (bf16) launch(KK_MERGE, merge_kernel<__bf16, _Float16>, mgrid, mblock, stream, a.dev, (__bf16 *)out, lse, T, Hq, out_packed ? 1 : 0);
-    else launch(KK_MERGE, merge_kernel<__bf16, float>, mgrid, mblock, stream, a.dev, (__bf16 *)out, lse, T, Hq, out_packed ? 1 : 0);
+    if (bf16) merge(merge_kernel<__bf16, _Float16, 16>, merge_kernel<__bf16, _Float16, 8>, (__bf16 *)out, out_packed ? 1 : 0);
+    else merge(merge_kernel<__bf16, float, 16>, merge_kernel<__bf16, float, 8>, (__bf16 *)out, out_packed ? 1 : 0);
   } else {
-    if (bf16) launch(KK_MERGE, merge_kernel<float, _Float16>, mgrid, mblock, stream, a.dev, (float *)out, lse, T, Hq, 0);
-    else launch(KK_MERGE, merge_kernel<float, float>, mgrid, mblock, stream, a.dev, (float *)out, lse, T, Hq, 0);
+    if (bf16) merge(merge_kernel<float, _Float16, 16>, merge_kernel<float, _Float16, 8>, (float *)out, 0);
+    else merge(merge_kernel<float, float, 16>, merge_kernel<float, float, 8>, (float *)out, 0);
   }
   return hipGetLastError();
 }

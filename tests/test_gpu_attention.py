@@ -58,6 +58,9 @@ EDGE = {
     # private histories far beyond the workloads' 1024 clip: 40 private chunks
     # and more than 16 partial slots per token (several merge batches)
     "long_private": ([64], [0, 0, 0], [4, 1, 4], [5000, 3071, 129], 16, 2),
+    # more than 4,096 (token, head) rows: the merge's wide form
+    "many_rows": ([300, 200], [0] * 40 + [1] * 37, [1] + [4] * 39 + [1] + [4] * 36,
+                  [(7 * i) % 90 for i in range(77)], 16, 2),
 }
 
 
