@@ -280,12 +280,21 @@ def _to_pool(torch, t, rows, n_rows):
     return out
 
 
+def code_digest(path):
+    """sha256 of a C++/HIP source with its comments, trailing blanks and empty
+    lines removed: an edit of the comments alone leaves it unchanged."""
+    import hashlib
+    import re
+    text = re.sub(r"/\*.*?\*/", "", open(path, encoding="utf-8").read(), flags=re.S)
+    lines = [re.sub(r"//.*$", "", l).rstrip() for l in text.splitlines()]
+    return hashlib.sha256("\n".join(l for l in lines if l).encode()).hexdigest()
+
+
 def _traffic(kind, workload="c4"):
     """HBM bytes per launch of kernel kind from profiles/traffic_<workload>.md
     (rocprofv3 FETCH_SIZE / WRITE_SIZE runs scaled by a plain copy kernel's
     readings), or None when there is no such summary or the kernel's source
-    has changed since the counters were taken."""
-    import hashlib
+    code (comments aside) has changed since the counters were taken."""
     import re
     root = os.path.dirname(os.path.abspath(__file__))
     try:
@@ -293,7 +302,7 @@ def _traffic(kind, workload="c4"):
         block = json.loads(re.search(r"```json\n(.*?)```", text, re.S).group(1))
         k = block["kernels"][kind]
         src = os.path.join(root, "paper_2607_18839_amd", "csrc", k["source"])
-        if hashlib.sha256(open(src, "rb").read()).hexdigest() != block["source_sha256"][k["source"]]:
+        if code_digest(src) != block["code_sha256"][k["source"]]:
             return None
         return k["traffic_bytes"]
     except (OSError, KeyError, AttributeError, ValueError):

@@ -6,17 +6,23 @@
 // causal among themselves (section "Integration with P-MTP").  The layer is
 // computed in split form:
 //
-//   shared kernel   for each (page, kv head): the query rows of ALL branches
+//   shared items    for each (page, kv head): the query rows of ALL branches
 //                   of the page that use this kv head are stacked into 32-row
 //                   MFMA tiles (row r = token r / G, head g * G + r % G), so a
 //                   prefix K/V tile is fetched once and used by every branch.
-//                   Each workgroup = 4 waves = 128 stacked rows over one key
-//                   range; it writes a partial (O, log2-sum-exp) per row.
-//   private kernel  for each (branch, kv head, key chunk): one wave attends
-//                   the branch's ragged private rows with the bottom-right
-//                   causal mask (draft j sees private keys 0 .. L_b + j).
+//                   An item = 128 stacked rows over one key range; it writes
+//                   a partial (O, log2-sum-exp) per row.
+//   private items   for each (branch, kv head, key chunk of <= 128 keys): the
+//                   branch's ragged private rows with the bottom-right causal
+//                   mask (draft j sees private keys 0 .. L_b + j).
 //   merge kernel    per (token, query head): log-sum-exp merge of all
 //                   partials into the output row and its natural-log lse.
+//
+// bf16: one launch (shared_prefix_ring_kernel, or its fork-offset twin) runs
+// both kinds of item: a shared item on a workgroup of 8 waves (4 row groups x
+// the even and the odd key tiles) fed by an LDS ring of direct global -> LDS
+// copies, a private item on one wave.  fp32: shared_prefix_kernel<float> and
+// private_kernel_f32, register-staged.
 //
 // MFMA formulation (v_mfma_f32_32x32x16_bf16; fp32 inputs use eight
 // v_mfma_f32_32x32x2_f32 per step): scores are computed transposed,
@@ -24,9 +30,10 @@
 // 32-key block.  The row max then needs a single cross-lane exchange (lane ^
 // 32), the row sum none until the end, and the P^T registers are directly the
 // B operand of O^T += V^T P^T.  The contraction index of QK^T is permuted
-// (lane half h, step s -> dims 32h + 8s .. +7, identical for K and Q), and
-// V^T is stored in LDS with key bits 2 and 3 swapped so that each PV operand
-// is one contiguous 16-byte LDS read.
+// (lane half h, step s -> dims 32h + 8s .. +7, identical for K and Q).  The
+// PV operand is one contiguous 16-byte LDS read: the fp32 tiles store V^T
+// with key bits 2 and 3 swapped; the bf16 ring stores V as loaded and reads
+// it transposed (ds_read_b64_tr_b16).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>

@@ -44,7 +44,17 @@ def test_traffic_summaries_parse_and_cover_the_reported_kernels():
         assert block["fetch_factor"] > 0 and block["write_factor"] > 0
         for n in names:
             k = block["kernels"][n]
-            assert k["traffic_bytes"] > 0 and k["source"] in block["source_sha256"]
+            assert k["traffic_bytes"] > 0 and k["source"] in block["code_sha256"]
             got = bench._traffic(n, workload)
             assert got is None or got == k["traffic_bytes"]
     assert bench._traffic("shared_prefix", "c9") is None   # no summary: no figure
+
+
+def test_code_digest_ignores_comments_only(tmp_path):
+    sys.path.insert(0, ROOT)
+    import bench
+    a, b, c = tmp_path / "a.hip", tmp_path / "b.hip", tmp_path / "c.hip"
+    a.write_text("int f(int x) {  // doubles\n  return 2 * x;\n}\n")
+    b.write_text("/* header */\n// a note\nint f(int x) {\n\n  return 2 * x;   // the same code\n}\n")
+    c.write_text("int f(int x) {\n  return 3 * x;\n}\n")
+    assert bench.code_digest(str(a)) == bench.code_digest(str(b)) != bench.code_digest(str(c))
