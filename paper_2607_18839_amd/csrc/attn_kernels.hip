@@ -21,8 +21,8 @@
 // bf16: one launch (shared_prefix_ring_kernel, or its fork-offset twin) runs
 // both kinds of item: a shared item on a workgroup of 8 waves (4 row groups x
 // the even and the odd key tiles) fed by an LDS ring of direct global -> LDS
-// copies, a private item on one wave.  fp32: shared_prefix_kernel<float> and
-// private_kernel_f32, register-staged.
+// copies, a private item on one wave.  fp32: attn_f32_kernel, also one
+// launch, register-staged (a shared item on 4 waves, a private item on one).
 //
 // MFMA formulation (v_mfma_f32_32x32x16_bf16; fp32 inputs use eight
 // v_mfma_f32_32x32x2_f32 per step): scores are computed transposed,
@@ -658,18 +658,12 @@ __device__ __forceinline__ void row_token(const AttnArgs &a, const SharedItem &s
   }
 }
 
+// One shared-prefix item of the register-staged form (fp32) on a 256-thread
+// workgroup: K/V tiles through two LDS buffers of Tile<T>::kBytes at lds.
 template <typename T>
-__global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
+__device__ __forceinline__ void shared_item_staged(const AttnArgs &a, int item, unsigned char *lds) {
   constexpr int NT = 256;
   using Tl = Tile<T>;
-  __shared__ __attribute__((aligned(16))) unsigned char lds[2][Tl::kBytes];
-
-  // XCD-aware order: consecutive workgroup ids go round-robin over the 8
-  // XCDs; give each XCD a contiguous run of items, so items that read the
-  // same key range share one L2.
-  const int per_xcd = gridDim.x / 8;
-  const int item = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (item >= a.n_shared) return;
   const SharedItem si = shared_item(a, item);
   const int g = si.g, row0 = si.row0, nrows = si.nrows;
   const int key0 = si.key0, key1 = si.key1, slot = si.slot, flags = si.flags;
@@ -699,7 +693,7 @@ __global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
   const int ntiles = (key1 - key0 + 63) / 64;
   ld.load(kbase + row(key0), stride, key1 - key0, tid);
   ld.load_v(vbase + row(key0), stride, key1 - key0, tid);
-  ld.store(lds[0], tid);
+  ld.store(lds, tid);
   __syncthreads();
   for (int i = 0; i < ntiles; ++i) {
     const int k0 = key0 + 64 * i;
@@ -707,8 +701,8 @@ __global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
       ld.load(kbase + row(k0 + 64), stride, key1 - k0 - 64, tid);
       ld.load_v(vbase + row(k0 + 64), stride, key1 - k0 - 64, tid);
     }
-    if (wave_active && k0 < wmax) w.tile(lds[i & 1], k0, limit, k0 + 64 > wmin, a.c, lane);
-    if (i + 1 < ntiles) ld.store(lds[(i + 1) & 1], tid);
+    if (wave_active && k0 < wmax) w.tile(lds + (i & 1) * Tl::kBytes, k0, limit, k0 + 64 > wmin, a.c, lane);
+    if (i + 1 < ntiles) ld.store(lds + ((i + 1) & 1) * Tl::kBytes, tid);
     __syncthreads();
   }
   // a row writes its partial of this split only if it sees the split's first
@@ -718,7 +712,7 @@ __global__ __launch_bounds__(256) void shared_prefix_kernel(AttnArgs a) {
   if (wave_active) w.write(a.dev.part_o, a.dev.part_lse, prow, writes);
 }
 
-// bf16 shared-prefix kernel: same items and arithmetic as shared_prefix_kernel,
+// bf16 shared-prefix kernel: same items and arithmetic as shared_item_staged,
 // on 8 waves: waves w and w + 4 own the same 32 rows and take the even and
 // odd key tiles of the item, so two waves share each SIMD; their states are
 // combined through LDS at the end.  K and V stream through an LDS ring of
@@ -1137,7 +1131,7 @@ __device__ __forceinline__ void private_item_ring(const AttnArgs &a, int item, i
 
 // ------------------------------------------------------------ private kernel
 
-// One fp32 private work item on a one-wave workgroup, staged through the
+// One fp32 private work item on one wave, staged through the wave's own
 // LDS tile `lds` (Tile<float>::kBytes).
 __device__ __forceinline__ void private_item_f32(const AttnArgs &a, int item, int lane, unsigned char *lds) {
   using T = float;
@@ -1167,20 +1161,35 @@ __device__ __forceinline__ void private_item_f32(const AttnArgs &a, int item, in
     const int64_t r = kv_row(a, a.dev.priv_tiles, priv_row, k0, k0) * stride;
     ld.load(kbase + r, stride, key1 - k0, lane);
     ld.load_v(vbase + r, stride, key1 - k0, lane);
-    __syncthreads();   // previous tile fully consumed
+    // the wave's own LDS tile: its reads of the previous tile are done before
+    // the stores, and the stores before the reads (one wave, so no barrier)
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     ld.store(lds, lane);
-    __syncthreads();
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     w.tile(lds, k0, limit, k0 + 64 > wmin, a.c, lane);
   }
   const int64_t prow = valid ? ((int64_t)a.dev.token_slots[2 * t] + slot) * a.Hq + hq : 0;
   w.write(a.dev.part_o, a.dev.part_lse, prow, valid);
 }
 
-// fp32 private kernel: one wave per item.
-__global__ __launch_bounds__(64) void private_kernel_f32(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) unsigned char lds[Tile<float>::kBytes];
-  if ((int)blockIdx.x >= a.n_private) return;
-  private_item_f32(a, blockIdx.x, threadIdx.x, lds);
+// fp32 attention in one launch: the shared items on the first workgroups
+// (XCD-aware order: consecutive workgroup ids go round-robin over the 8
+// XCDs, so each XCD gets a contiguous run of items and items that read the
+// same key range share one L2), then the private items, one per wave and 4
+// per workgroup, each wave with its own LDS tile.
+__global__ __launch_bounds__(256) void attn_f32_kernel(AttnArgs a) {
+  using Tl = Tile<float>;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[4 * Tl::kBytes];
+  const int n_shared_slots = (a.n_shared + 7) / 8 * 8, bid = blockIdx.x;
+  if (bid < n_shared_slots) {
+    const int per_xcd = n_shared_slots / 8;
+    const int item = (bid % 8) * per_xcd + bid / 8;
+    if (item < a.n_shared) shared_item_staged<float>(a, item, lds);
+    return;
+  }
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int pi = (bid - n_shared_slots) * 4 + wave;
+  if (pi < a.n_private) private_item_f32(a, pi, threadIdx.x & 63, lds + wave * Tl::kBytes);
 }
 
 // ------------------------------------------------------------ merge kernel
@@ -1361,9 +1370,18 @@ hipError_t launch_branch_attention(const Plan &P, const void *q, const void *sha
       launch(KK_SHARED, ring, dim3(grid(a)), dim3(512), stream, a);
     }
   } else {
-    if (a.n_shared > 0)
-      launch(KK_SHARED, shared_prefix_kernel<float>, dim3((a.n_shared + 7) / 8 * 8), dim3(256), stream, a);
-    if (a.n_private > 0) launch(KK_PRIVATE, private_kernel_f32, dim3(a.n_private), dim3(64), stream, a);
+    // one launch, as for bf16; phase isolation: the shared items, then the
+    // private items, in launches of their own
+    auto grid = [](const AttnArgs &x) { return (x.n_shared + 7) / 8 * 8 + (x.n_private + 3) / 4; };
+    if (attn_phase_isolation()) {
+      AttnArgs sh = a, pr = a;
+      sh.n_private = 0;
+      pr.n_shared = 0;
+      if (sh.n_shared > 0) launch(KK_SHARED, attn_f32_kernel, dim3(grid(sh)), dim3(256), stream, sh);
+      if (pr.n_private > 0) launch(KK_PRIVATE, attn_f32_kernel, dim3(grid(pr)), dim3(256), stream, pr);
+    } else if (grid(a) > 0) {
+      launch(KK_SHARED, attn_f32_kernel, dim3(grid(a)), dim3(256), stream, a);
+    }
   }
   const int rows = P.T * P.attn.num_q_heads;
   const int T = P.T, Hq = P.attn.num_q_heads;
