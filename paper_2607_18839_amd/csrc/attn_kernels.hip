@@ -346,21 +346,28 @@ template <typename T> struct WaveAttn {
     }
   }
 
-  // Raw scores S^T of a K tile in the ring (Tile<bf16> swizzle): the two
-  // 32-key blocks' MFMA chains are interleaved.
-  __device__ __forceinline__ void qk_ring(const unsigned char *kt, f32x16 (&s)[2], int lane) {
-    static_assert(sizeof(T) == 2, "bf16 only");
+  // Byte offsets, within a K tile of the ring (Tile<bf16> swizzle), of this
+  // lane's operand for contraction step st of key block 0 (key lane % 32).
+  // Key block 1 (32 keys on) is 32 rows further with the same swizzle, so it
+  // is a constant offset from these.
+  __device__ static __forceinline__ void k_offsets(int lane, int (&koff)[4]) {
     using Tl = Tile<T>;
     const int kr = lane & 31;
+#pragma unroll
+    for (int st = 0; st < 4; ++st) koff[st] = kr * Tl::kRowBytes + 16 * Tl::kchunk(kr, 4 * (lane >> 5) + st);
+  }
+
+  // Raw scores S^T of a K tile in the ring (Tile<bf16> swizzle): the two
+  // 32-key blocks' MFMA chains are interleaved.
+  __device__ __forceinline__ void qk_ring(const unsigned char *kt, const int (&koff)[4], f32x16 (&s)[2]) {
+    static_assert(sizeof(T) == 2, "bf16 only");
+    using Tl = Tile<T>;
     for (int r = 0; r < 16; ++r) { s[0][r] = 0.f; s[1][r] = 0.f; }
     Frag<T> a[2][4];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const int key = 32 * kb + kr;
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int st = 0; st < 4; ++st)
-        ld16(a[kb][st], (const T *)(kt + key * Tl::kRowBytes + 16 * Tl::kchunk(key, 4 * half + st)));
-    }
+      for (int st = 0; st < 4; ++st) ld16(a[kb][st], (const T *)(kt + koff[st] + 32 * kb * Tl::kRowBytes));
 #pragma unroll
     for (int st = 0; st < 4; ++st)
 #pragma unroll
@@ -383,21 +390,18 @@ template <typename T> struct WaveAttn {
   // row sees only a few keys (the matrix-core sum adds bf16-rounded
   // probabilities).
   template <bool FSUM = false>
-  __device__ __forceinline__ void step_ring(const unsigned char *kt_next, const unsigned char *vt, const int (&voff)[2],
-                                            f32x16 (&s_cur)[2], f32x16 (&s_next)[2], int key0, int limit,
-                                            bool masked, float c, int lane) {
+  __device__ __forceinline__ void step_ring(const unsigned char *kt_next, const int (&koff)[4], const unsigned char *vt,
+                                            const int (&voff)[2], f32x16 (&s_cur)[2], f32x16 (&s_next)[2], int key0,
+                                            int limit, bool masked, float c) {
     static_assert(sizeof(T) == 2, "bf16 only");
     using Tl = Tile<T>;
-    const int kr = lane & 31;
     Frag<T> ka[2][4];
     if (kt_next) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const int key = 32 * kb + kr;
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int st = 0; st < 4; ++st)
-          ld16(ka[kb][st], (const T *)(kt_next + key * Tl::kRowBytes + 16 * Tl::kchunk(key, 4 * half + st)));
-      }
+          ld16(ka[kb][st], (const T *)(kt_next + koff[st] + 32 * kb * Tl::kRowBytes));
     }
     step_frags<FSUM>(kt_next != nullptr, ka, vt, voff, s_cur, s_next, key0, limit, masked, c);
   }
@@ -770,7 +774,8 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   const int key0 = si.key0, key1 = si.key1, slot = si.slot, flags = si.flags;
   const int prefix_row = si.prefix_row, page_q_row = si.page_q_row;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // (wave-uniform, so that the ring's slot and copy addresses stay scalar)
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int rw = wave & 3, par = wave >> 2;             // row group, key-tile parity
   const int rloc = rw * 32 + (lane & 31);
   const bool valid = rloc < nrows;
@@ -782,32 +787,47 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   const bool wave_active = rw * 32 < nrows;
   const int wmin = wave_min(valid ? limit : key1);
 
-  const int64_t stride = (int64_t)a.Hkv * D;
   const T *kbase = (const T *)a.shared_k + (int64_t)g * D;
   const T *vbase = (const T *)a.shared_v + (int64_t)g * D;
-  int voff[2];
+  int voff[2], koff[4];
   WaveAttn<T>::vt_offsets(lane, voff);
+  WaveAttn<T>::k_offsets(lane, koff);
 
   // copy instructions of this wave for a pair: its parity's tile, K and V
-  // rows 16 rw + lane / 8 and 16 rw + 8 + lane / 8, physical chunk lane % 8
+  // rows 16 rw + lane / 8 and 16 rw + 8 + lane / 8, physical chunk lane % 8.
+  // A tile's first row is a scalar address; each lane adds its 32-bit byte
+  // offset within the tile (the copies' scalar-base + vector-offset form),
+  // so the copies of a tile that lies wholly inside the item take no vector
+  // arithmetic.
   const int crow = 16 * rw + (lane >> 3), pch = lane & 7;
   const int kq0 = Tl::kchunk(crow, pch), kq1 = Tl::kchunk(crow + 8, pch);
   const int vq0 = vchunk(crow, pch), vq1 = vchunk(crow + 8, pch);
+  const unsigned rowb = (unsigned)(a.Hkv * D * (int)sizeof(T));   // bytes per K/V row
+  const unsigned ko0 = crow * rowb + 16 * kq0, ko1 = (crow + 8) * rowb + 16 * kq1;
+  const unsigned vo0 = crow * rowb + 16 * vq0, vo1 = (crow + 8) * rowb + 16 * vq1;
   const int ntiles = (key1 - key0 + 63) / 64, npairs = (ntiles + 1) / 2;
   // paged K/V: lane l holds the pool row of the item's tile l (at most 64
   // tiles per item), read with a uniform lane index when a tile is issued
   const int tile_row = a.paged && lane < ntiles ? a.dev.shared_tiles[prefix_row + (key0 >> 6) + lane] : 0;
   auto issue = [&](int j) {
-    unsigned char *st = lds + (j % S) * kPair + par * kTile;
-    const int k0 = key0 + 64 * (2 * j + par);
+    unsigned char *st = lds + (j % S) * kPair + par * kTile + 2048 * rw;
+    const int tj = 2 * j + par;
     // the last pair's missing odd tile re-reads the item's last tile
-    const int ti = min(2 * j + par, ntiles - 1), kt = key0 + 64 * ti;
+    const int ti = min(tj, ntiles - 1), kt = key0 + 64 * ti;
     const int64_t base = a.paged ? (int64_t)__builtin_amdgcn_readlane(tile_row, ti) : (int64_t)prefix_row + kt;
-    const int64_t r0 = base + (min(k0 + crow, key1 - 1) - kt), r1 = base + (min(k0 + crow + 8, key1 - 1) - kt);
-    dma16(kbase + r0 * stride + 8 * kq0, st + 1024 * (2 * rw));
-    dma16(kbase + r1 * stride + 8 * kq1, st + 1024 * (2 * rw + 1));
-    dma16(vbase + r0 * stride + 8 * vq0, st + kTileBytes + 1024 * (2 * rw));
-    dma16(vbase + r1 * stride + 8 * vq1, st + kTileBytes + 1024 * (2 * rw + 1));
+    const unsigned char *kr = (const unsigned char *)kbase + base * rowb;
+    const unsigned char *vr = (const unsigned char *)vbase + base * rowb;
+    unsigned k0o = ko0, k1o = ko1, v0o = vo0, v1o = vo1;
+    if (key0 + 64 * tj + 64 > key1) {
+      // rows past the item's last key (key1 - 1) are clamped to it
+      const int last = key1 - 1 - kt, r = key0 + 64 * tj - kt + crow;
+      const unsigned r0 = (unsigned)min(r, last) * rowb, r1 = (unsigned)min(r + 8, last) * rowb;
+      k0o = r0 + 16 * kq0; k1o = r1 + 16 * kq1; v0o = r0 + 16 * vq0; v1o = r1 + 16 * vq1;
+    }
+    dma16(kr + k0o, st);
+    dma16(kr + k1o, st + 1024);
+    dma16(vr + v0o, st + kTileBytes);
+    dma16(vr + v1o, st + kTileBytes + 1024);
   };
   // wait until pair j's copies (this wave's 4) have landed, with `ahead`
   // later pairs still in flight
@@ -831,9 +851,11 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   // key (fork offsets: the planner gives it no slot otherwise)
   const int my_prow = valid && limit > key0 ? (my_slots + slot) * a.Hq + hq : -1;
   ring_barrier();   // pair 0 visible to every wave
-  f32x16 s_cur[2], s_next[2];
-  if (wave_active && par < ntiles) w.qk_ring(lds + par * kTile, s_cur, lane);
-  for (int j = 0; j < npairs; ++j) {
+  // the raw scores of this wave's current tile and of its next one; the
+  // loop is unrolled twice so that the two swap roles without copies
+  f32x16 s_a[2], s_b[2];
+  if (wave_active && par < ntiles) w.qk_ring(lds + par * kTile, koff, s_a);
+  auto pair = [&](int j, f32x16 (&s_cur)[2], f32x16 (&s_next)[2]) {
     // pair j + 1 visible; the slot of pair j - 1 (read in iteration j - 1) is free
     if (j + 1 < npairs) {
       wait_pair(min(npairs - 1, j + 2) - (j + 1));
@@ -844,11 +866,13 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
     if (wave_active && ti < ntiles) {
       const unsigned char *kt_next = ti + 2 < ntiles ? lds + ((j + 1) % S) * kPair + par * kTile : nullptr;
       const int k0 = key0 + 64 * ti;
-      w.step_ring(kt_next, lds + (j % S) * kPair + par * kTile + kTileBytes, voff, s_cur, s_next, k0, limit,
-                  k0 + 64 > wmin, a.c, lane);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) { s_cur[0][r] = s_next[0][r]; s_cur[1][r] = s_next[1][r]; }
+      w.step_ring(kt_next, koff, lds + (j % S) * kPair + par * kTile + kTileBytes, voff, s_cur, s_next, k0, limit,
+                  k0 + 64 > wmin, a.c);
     }
+  };
+  for (int j = 0; j < npairs; j += 2) {
+    pair(j, s_a, s_b);
+    if (j + 1 < npairs) pair(j + 1, s_b, s_a);
   }
   ring_barrier();   // every wave is done with the ring; its LDS becomes scratch
   w.l = w.lsum[0];  // the query's whole sum (the row-sum MFMAs of step_ring)
@@ -921,7 +945,8 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_fork_kernel(AttnArgs a
   const int key0 = si.key0, key1 = si.key1, slot = si.slot, flags = si.flags;
   const int prefix_row = si.prefix_row, page_q_row = si.page_q_row;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // (wave-uniform, so that the ring's slot and copy addresses stay scalar)
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int rw = wave & 3, par = wave >> 2;             // row group, key-tile parity
   const int rloc = rw * 32 + (lane & 31);
   const bool valid = rloc < nrows;
@@ -938,32 +963,47 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_fork_kernel(AttnArgs a
   if (flags & SI_FLAG_FORK)
     ntw = __builtin_amdgcn_readfirstlane(max(0, (min(key1, wave_max(valid ? limit : key0)) - key0 + 63) / 64));
 
-  const int64_t stride = (int64_t)a.Hkv * D;
   const T *kbase = (const T *)a.shared_k + (int64_t)g * D;
   const T *vbase = (const T *)a.shared_v + (int64_t)g * D;
-  int voff[2];
+  int voff[2], koff[4];
   WaveAttn<T>::vt_offsets(lane, voff);
+  WaveAttn<T>::k_offsets(lane, koff);
 
   // copy instructions of this wave for a pair: its parity's tile, K and V
-  // rows 16 rw + lane / 8 and 16 rw + 8 + lane / 8, physical chunk lane % 8
+  // rows 16 rw + lane / 8 and 16 rw + 8 + lane / 8, physical chunk lane % 8.
+  // A tile's first row is a scalar address; each lane adds its 32-bit byte
+  // offset within the tile (the copies' scalar-base + vector-offset form),
+  // so the copies of a tile that lies wholly inside the item take no vector
+  // arithmetic.
   const int crow = 16 * rw + (lane >> 3), pch = lane & 7;
   const int kq0 = Tl::kchunk(crow, pch), kq1 = Tl::kchunk(crow + 8, pch);
   const int vq0 = vchunk(crow, pch), vq1 = vchunk(crow + 8, pch);
+  const unsigned rowb = (unsigned)(a.Hkv * D * (int)sizeof(T));   // bytes per K/V row
+  const unsigned ko0 = crow * rowb + 16 * kq0, ko1 = (crow + 8) * rowb + 16 * kq1;
+  const unsigned vo0 = crow * rowb + 16 * vq0, vo1 = (crow + 8) * rowb + 16 * vq1;
   const int ntiles = (key1 - key0 + 63) / 64, npairs = (ntiles + 1) / 2;
   // paged K/V: lane l holds the pool row of the item's tile l (at most 64
   // tiles per item), read with a uniform lane index when a tile is issued
   const int tile_row = a.paged && lane < ntiles ? a.dev.shared_tiles[prefix_row + (key0 >> 6) + lane] : 0;
   auto issue = [&](int j) {
-    unsigned char *st = lds + (j % S) * kPair + par * kTile;
-    const int k0 = key0 + 64 * (2 * j + par);
+    unsigned char *st = lds + (j % S) * kPair + par * kTile + 2048 * rw;
+    const int tj = 2 * j + par;
     // the last pair's missing odd tile re-reads the item's last tile
-    const int ti = min(2 * j + par, ntiles - 1), kt = key0 + 64 * ti;
+    const int ti = min(tj, ntiles - 1), kt = key0 + 64 * ti;
     const int64_t base = a.paged ? (int64_t)__builtin_amdgcn_readlane(tile_row, ti) : (int64_t)prefix_row + kt;
-    const int64_t r0 = base + (min(k0 + crow, key1 - 1) - kt), r1 = base + (min(k0 + crow + 8, key1 - 1) - kt);
-    dma16(kbase + r0 * stride + 8 * kq0, st + 1024 * (2 * rw));
-    dma16(kbase + r1 * stride + 8 * kq1, st + 1024 * (2 * rw + 1));
-    dma16(vbase + r0 * stride + 8 * vq0, st + kTileBytes + 1024 * (2 * rw));
-    dma16(vbase + r1 * stride + 8 * vq1, st + kTileBytes + 1024 * (2 * rw + 1));
+    const unsigned char *kr = (const unsigned char *)kbase + base * rowb;
+    const unsigned char *vr = (const unsigned char *)vbase + base * rowb;
+    unsigned k0o = ko0, k1o = ko1, v0o = vo0, v1o = vo1;
+    if (key0 + 64 * tj + 64 > key1) {
+      // rows past the item's last key (key1 - 1) are clamped to it
+      const int last = key1 - 1 - kt, r = key0 + 64 * tj - kt + crow;
+      const unsigned r0 = (unsigned)min(r, last) * rowb, r1 = (unsigned)min(r + 8, last) * rowb;
+      k0o = r0 + 16 * kq0; k1o = r1 + 16 * kq1; v0o = r0 + 16 * vq0; v1o = r1 + 16 * vq1;
+    }
+    dma16(kr + k0o, st);
+    dma16(kr + k1o, st + 1024);
+    dma16(vr + v0o, st + kTileBytes);
+    dma16(vr + v1o, st + kTileBytes + 1024);
   };
   // wait until pair j's copies (this wave's 4) have landed, with `ahead`
   // later pairs still in flight
@@ -987,9 +1027,11 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_fork_kernel(AttnArgs a
   // key (fork offsets: the planner gives it no slot otherwise)
   const int my_prow = valid && limit > key0 ? (my_slots + slot) * a.Hq + hq : -1;
   ring_barrier();   // pair 0 visible to every wave
-  f32x16 s_cur[2], s_next[2];
-  if (wave_active && par < ntw) w.qk_ring(lds + par * kTile, s_cur, lane);
-  for (int j = 0; j < npairs; ++j) {
+  // the raw scores of this wave's current tile and of its next one; the
+  // loop is unrolled twice so that the two swap roles without copies
+  f32x16 s_a[2], s_b[2];
+  if (wave_active && par < ntw) w.qk_ring(lds + par * kTile, koff, s_a);
+  auto pair = [&](int j, f32x16 (&s_cur)[2], f32x16 (&s_next)[2]) {
     // pair j + 1 visible; the slot of pair j - 1 (read in iteration j - 1) is free
     if (j + 1 < npairs) {
       wait_pair(min(npairs - 1, j + 2) - (j + 1));
@@ -1000,11 +1042,13 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_fork_kernel(AttnArgs a
     if (wave_active && ti < ntw) {
       const unsigned char *kt_next = ti + 2 < ntw ? lds + ((j + 1) % S) * kPair + par * kTile : nullptr;
       const int k0 = key0 + 64 * ti;
-      w.step_ring(kt_next, lds + (j % S) * kPair + par * kTile + kTileBytes, voff, s_cur, s_next, k0, limit,
-                  k0 + 64 > wmin, a.c, lane);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) { s_cur[0][r] = s_next[0][r]; s_cur[1][r] = s_next[1][r]; }
+      w.step_ring(kt_next, koff, lds + (j % S) * kPair + par * kTile + kTileBytes, voff, s_cur, s_next, k0, limit,
+                  k0 + 64 > wmin, a.c);
     }
+  };
+  for (int j = 0; j < npairs; j += 2) {
+    pair(j, s_a, s_b);
+    if (j + 1 < npairs) pair(j + 1, s_b, s_a);
   }
   ring_barrier();   // every wave is done with the ring; its LDS becomes scratch
   w.l = w.lsum[0];  // the query's whole sum (the row-sum MFMAs of step_ring)
