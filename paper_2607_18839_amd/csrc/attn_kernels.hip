@@ -509,18 +509,46 @@ template <typename T> struct WaveAttn {
     }
   }
 
-  // Folds the state of another wave that saw other keys of the same rows
-  // (same lane order) into this one.
-  __device__ __forceinline__ void combine(float m2, float l2, const f32x16 (&o2)[2]) {
-    const float m_new = fmaxf(m, m2);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float a1 = __builtin_amdgcn_exp2f(m - m_use), a2 = __builtin_amdgcn_exp2f(m2 - m_use);
-    m = m_new;
-    l = l * a1 + l2 * a2;
+  // Epilogue of the ring kernels, per wave.  The even-tile (P = 0) and
+  // odd-tile (P = 1) waves of a row group saw disjoint key tiles of the same
+  // 32 rows; wave P finishes head dims 32 P .. 32 P + 31.  It merges its own
+  // accumulators of that half with its partner's (ob2, with the partner's
+  // m2 and l2), taking the two states in the same order in both waves (the
+  // even one first) so that both normalise by the same sum, and writes the
+  // half rows as fp16 through its 2 KB of LDS scratch ([32 rows][32 dims],
+  // 16-byte chunk q of row r at q ^ ((r / 4) % 4)), 16 whole 64-byte half
+  // rows per store instruction.  The even wave also writes the lse.
+  // prow_of(r): as for write_f16.
+  template <int P, typename RowFn>
+  __device__ __forceinline__ void finish_half(float m2, float l2, const f32x16 &ob2, unsigned char *scratch,
+                                              _Float16 *part_o, float *part_lse, RowFn prow_of, int lane) {
+    typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+    const float me = P ? m2 : m, mo = P ? m : m2, le = P ? l2 : l, lo = P ? l : l2;
+    const float m_new = fmaxf(me, mo), m_use = m_new == -INFINITY ? 0.f : m_new;
+    const float ae = __builtin_amdgcn_exp2f(me - m_use), ao = __builtin_amdgcn_exp2f(mo - m_use);
+    const float l_tot = le * ae + lo * ao;
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const float a_own = (P ? ao : ae) * inv, a_other = (P ? ae : ao) * inv;
+    const int qr = lane & 31;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      o[0][r] = o[0][r] * a1 + o2[0][r] * a2;
-      o[1][r] = o[1][r] * a1 + o2[1][r] * a2;
+    for (int j = 0; j < 4; ++j) {
+      f16x4 v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = (_Float16)(o[P][4 * j + e] * a_own + ob2[4 * j + e] * a_other);
+      *(f16x4 *)(scratch + qr * 64 + 16 * (j ^ ((qr >> 2) & 3)) + 8 * half) = v;
+    }
+    if constexpr (P == 0) {
+      const int64_t pr_self = prow_of(qr);   // every lane calls prow_of (it may use cross-lane reads)
+      if (half == 0 && pr_self >= 0)
+        part_lse[pr_self] = l_tot > 0.f ? m_new + __builtin_amdgcn_logf(l_tot) : -INFINITY;
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wave's LDS writes precede its reads
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int row = 16 * k + (lane >> 2), c = lane & 3;
+      const u32x4 v = *(const u32x4 *)(scratch + row * 64 + 16 * (c ^ ((row >> 2) & 3)));
+      const int64_t pr = prow_of(row);
+      if (pr >= 0) *(u32x4 *)(part_o + pr * D + 32 * P + 8 * c) = v;
     }
   }
 
@@ -739,6 +767,38 @@ constexpr int kPrivWaveBytes = 2 * 64 * 128;
 static_assert(kPrivateChunkKeys <= 128, "a private item fits two tiles");
 __device__ __forceinline__ void private_item_ring(const AttnArgs &a, int item, int lane, unsigned char *lds);
 
+// The ring kernels' epilogue (after the ring's last barrier, its LDS free):
+// the two waves of row group rw hand each other (m, l) and their
+// accumulators of the partner's half of the head dims (18 x 64 floats per
+// wave), then each finishes its half (WaveAttn::finish_half).  my_prow: the
+// partial row of this lane's query (lanes 0..31), or -1.
+__device__ __forceinline__ void ring_epilogue(WaveAttn<__bf16> &w, unsigned char *lds, const AttnArgs &a, int rw,
+                                              int par, int lane, bool wave_active, int my_prow) {
+  constexpr int kXch = 18 * 64;   // floats handed over per wave
+  static_assert(8 * kXch * 4 + 8 * 2048 <= kPairRing * 4 * 64 * 128, "epilogue scratch within the ring's LDS");
+  float *mine = (float *)lds + (2 * rw + par) * kXch;
+  const float *theirs = (const float *)lds + (2 * rw + (par ^ 1)) * kXch;
+  if (wave_active) {
+    mine[lane] = w.m;
+    mine[64 + lane] = w.l;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mine[(2 + r) * 64 + lane] = par ? w.o[0][r] : w.o[1][r];
+  }
+  __syncthreads();
+  if (!wave_active) return;
+  f32x16 ob2;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) ob2[r] = theirs[(2 + r) * 64 + lane];
+  auto prow_of = [&](int r) -> int64_t { return __shfl(my_prow, r); };
+  unsigned char *scratch = lds + 8 * kXch * 4 + (2 * rw + par) * 2048;
+  if (par == 0)
+    w.finish_half<0>(theirs[lane], theirs[64 + lane], ob2, scratch, (_Float16 *)a.dev.part_o, a.dev.part_lse, prow_of,
+                     lane);
+  else
+    w.finish_half<1>(theirs[lane], theirs[64 + lane], ob2, scratch, (_Float16 *)a.dev.part_o, a.dev.part_lse, prow_of,
+                     lane);
+}
+
 __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   using T = __bf16;
   using Tl = Tile<T>;
@@ -876,30 +936,7 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_kernel(AttnArgs a) {
   }
   ring_barrier();   // every wave is done with the ring; its LDS becomes scratch
   w.l = w.lsum[0];  // the query's whole sum (the row-sum MFMAs of step_ring)
-  // odd-tile waves hand (m, l, O) to their even-tile partners
-  float *xch = (float *)lds + rw * (34 * 64);
-  if (par == 1 && wave_active) {
-    xch[lane] = w.m;
-    xch[64 + lane] = w.l;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      xch[(2 + r) * 64 + lane] = w.o[0][r];
-      xch[(18 + r) * 64 + lane] = w.o[1][r];
-    }
-  }
-  __syncthreads();
-  if (par == 1 || !wave_active) return;
-  {
-    f32x16 o2[2];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      o2[0][r] = xch[(2 + r) * 64 + lane];
-      o2[1][r] = xch[(18 + r) * 64 + lane];
-    }
-    w.combine(xch[lane], xch[64 + lane], o2);
-  }
-  auto prow_of = [&](int r) -> int64_t { return __shfl(my_prow, r); };
-  w.write_f16(lds + 4 * 34 * 64 * 4 + rw * 4096, (_Float16 *)a.dev.part_o, a.dev.part_lse, prow_of, lane, true);
+  ring_epilogue(w, lds, a, rw, par, lane, wave_active, my_prow);
 }
 
 // The bf16 kernel for plans with fork offsets: the same work as
@@ -1052,30 +1089,7 @@ __global__ __launch_bounds__(512) void shared_prefix_ring_fork_kernel(AttnArgs a
   }
   ring_barrier();   // every wave is done with the ring; its LDS becomes scratch
   w.l = w.lsum[0];  // the query's whole sum (the row-sum MFMAs of step_ring)
-  // odd-tile waves hand (m, l, O) to their even-tile partners
-  float *xch = (float *)lds + rw * (34 * 64);
-  if (par == 1 && wave_active) {
-    xch[lane] = w.m;
-    xch[64 + lane] = w.l;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      xch[(2 + r) * 64 + lane] = w.o[0][r];
-      xch[(18 + r) * 64 + lane] = w.o[1][r];
-    }
-  }
-  __syncthreads();
-  if (par == 1 || !wave_active) return;
-  {
-    f32x16 o2[2];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      o2[0][r] = xch[(2 + r) * 64 + lane];
-      o2[1][r] = xch[(18 + r) * 64 + lane];
-    }
-    w.combine(xch[lane], xch[64 + lane], o2);
-  }
-  auto prow_of = [&](int r) -> int64_t { return __shfl(my_prow, r); };
-  w.write_f16(lds + 4 * 34 * 64 * 4 + rw * 4096, (_Float16 *)a.dev.part_o, a.dev.part_lse, prow_of, lane, true);
+  ring_epilogue(w, lds, a, rw, par, lane, wave_active, my_prow);
 }
 
 // One private work item on one wave of the bf16 kernel.  Every load of the
