@@ -84,7 +84,12 @@ def add_box_peak(roof, peaks):
         return roof
     bp = None
     if peaks:
-        bp = peaks.get("mfma_bf16_tflops") if roof["unit"] == "TFLOP/s" else peaks.get("read_gbs")
+        # the microbenchmark measures bf16 MFMA and HBM reads only: a kernel
+        # priced against another peak (fp32) has no box denominator
+        if roof["unit"] == "GB/s":
+            bp = peaks.get("read_gbs")
+        elif roof["unit"] == "TFLOP/s" and roof.get("peak") == BF16_PEAK_TFLOPS:
+            bp = peaks.get("mfma_bf16_tflops")
     roof["box_peak"] = bp
     roof["box_frac"] = roof["achieved"] / bp if bp and roof.get("achieved") else None
     return roof

@@ -58,3 +58,18 @@ def test_code_digest_ignores_comments_only(tmp_path):
     b.write_text("/* header */\n// a note\nint f(int x) {\n\n  return 2 * x;   // the same code\n}\n")
     c.write_text("int f(int x) {\n  return 3 * x;\n}\n")
     assert bench.code_digest(str(a)) == bench.code_digest(str(b)) != bench.code_digest(str(c))
+
+
+def test_box_peak_only_for_the_measured_units():
+    """The box's own peaks cover bf16 MFMA and HBM reads: a bf16 or HBM
+    roofline gets the second denominator, an fp32 one gets none."""
+    sys.path.insert(0, ROOT)
+    import bench
+    pk = {"read_gbs": 6400.0, "mfma_bf16_tflops": 2340.0}
+    r = bench.add_box_peak({"unit": "TFLOP/s", "peak": bench.BF16_PEAK_TFLOPS, "achieved": 234.0}, pk)
+    assert r["box_peak"] == 2340.0 and abs(r["box_frac"] - 0.1) < 1e-12
+    r = bench.add_box_peak({"unit": "GB/s", "peak": 8000.0, "achieved": 3200.0}, pk)
+    assert r["box_peak"] == 6400.0 and abs(r["box_frac"] - 0.5) < 1e-12
+    r = bench.add_box_peak({"unit": "TFLOP/s", "peak": bench.FP32_PEAK_TFLOPS, "achieved": 0.3}, pk)
+    assert r["box_peak"] is None and r["box_frac"] is None
+    assert bench.add_box_peak(None, pk) is None
