@@ -3,8 +3,16 @@
 // dense bf16 MFMA rate, v_exp_f32 rate and dependent-load latency.
 //
 //   peaks [copy_mib]      prints one JSON object
+//   peaks copy N          N MiB copies only (the reference for scaling
+//                         memory-traffic counters)
+//   peaks read K1 K2 ...  streaming-read rate of a single launch that reads
+//                         K KiB, from buffers rotated over 512 MiB (beyond the
+//                         Infinity Cache), each launch timed by its own
+//                         dispatch events: the rate a kernel of that size can
+//                         reach at all
 //
 // Every kernel has a fixed trip count and touches only its own buffers.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
@@ -140,6 +148,44 @@ template <typename F> float time_ms(F launch, int reps) {
 int main(int argc, char **argv) {
   // "peaks copy N": only N MiB copies (3 launches), the reference for
   // scaling memory-traffic counters; otherwise "peaks [N]" runs everything.
+  if (argc > 1 && std::string(argv[1]) == "read") {
+    const size_t pool = (size_t)512 << 20;
+    f32x4 *buf;
+    float *sk;
+    CHECK(hipMalloc(&buf, pool));
+    CHECK(hipMalloc(&sk, 64));
+    CHECK(hipMemset(buf, 0, pool));
+    hipDeviceProp_t pr;
+    CHECK(hipGetDeviceProperties(&pr, 0));
+    hipEvent_t e0, e1;
+    CHECK(hipEventCreate(&e0));
+    CHECK(hipEventCreate(&e1));
+    std::string kib_s, gbs_s, us_s;
+    for (int i = 2; i < argc; ++i) {
+      const size_t kib = std::strtoul(argv[i], nullptr, 10), bytes = kib << 10, n4 = bytes / 16;
+      if (bytes == 0 || bytes > pool / 2) continue;
+      const size_t nbuf = pool / bytes;   // the launches rotate over every slice of the pool
+      const int reps = 64;
+      double total_ms = 0.0;
+      for (int r = -8; r < reps; ++r) {   // 8 untimed launches first
+        const f32x4 *src = buf + (size_t)((r + 8) % nbuf) * (bytes / 16);
+        hipExtLaunchKernelGGL(read_kernel, dim3(pr.multiProcessorCount * 8), dim3(256), 0, 0, e0, e1, 0, src, n4, sk);
+        CHECK(hipGetLastError());
+        CHECK(hipEventSynchronize(e1));
+        float ms = 0.f;
+        CHECK(hipEventElapsedTime(&ms, e0, e1));
+        if (r >= 0) total_ms += ms;
+      }
+      const double us = total_ms * 1e3 / reps;
+      char b[64];
+      std::snprintf(b, sizeof b, "%s%zu", kib_s.empty() ? "" : ", ", kib); kib_s += b;
+      std::snprintf(b, sizeof b, "%s%.1f", gbs_s.empty() ? "" : ", ", bytes / (us * 1e3)); gbs_s += b;
+      std::snprintf(b, sizeof b, "%s%.2f", us_s.empty() ? "" : ", ", us); us_s += b;
+    }
+    std::printf("{\"read_kib\": [%s], \"read_gbs\": [%s], \"read_us\": [%s]}\n", kib_s.c_str(), gbs_s.c_str(),
+                us_s.c_str());
+    return 0;
+  }
   const bool copy_only = argc > 1 && std::string(argv[1]) == "copy";
   const int size_arg = copy_only ? 2 : 1;
   const size_t mib = argc > size_arg ? std::strtoul(argv[size_arg], nullptr, 10) : 1024;
