@@ -10,6 +10,10 @@
 //                         Infinity Cache), each launch timed by its own
 //                         dispatch events: the rate a kernel of that size can
 //                         reach at all
+//   peaks mfma M1 M2 ...  the same for bf16 MFMA work: one launch of one
+//                         256-thread workgroup per CU doing about M MFLOP of
+//                         v_mfma_f32_32x32x16_bf16 (4 independent chains per
+//                         wave), timed by its dispatch events
 //
 // Every kernel has a fixed trip count and touches only its own buffers.
 #include <hip/hip_ext.h>
@@ -183,6 +187,41 @@ int main(int argc, char **argv) {
       std::snprintf(b, sizeof b, "%s%.2f", us_s.empty() ? "" : ", ", us); us_s += b;
     }
     std::printf("{\"read_kib\": [%s], \"read_gbs\": [%s], \"read_us\": [%s]}\n", kib_s.c_str(), gbs_s.c_str(),
+                us_s.c_str());
+    return 0;
+  }
+  if (argc > 1 && std::string(argv[1]) == "mfma") {
+    float *sk;
+    CHECK(hipMalloc(&sk, 64));
+    hipDeviceProp_t pr;
+    CHECK(hipGetDeviceProperties(&pr, 0));
+    hipEvent_t e0, e1;
+    CHECK(hipEventCreate(&e0));
+    CHECK(hipEventCreate(&e1));
+    const int cus = pr.multiProcessorCount;
+    const double per_iter = (double)cus * 4 /*waves*/ * 4 /*MFMAs*/ * (32.0 * 32 * 16 * 2);
+    std::string m_s, t_s, us_s;
+    for (int i = 2; i < argc; ++i) {
+      const double mflop = std::strtod(argv[i], nullptr);
+      const int iters = (int)(mflop * 1e6 / per_iter + 0.5);
+      if (iters < 1 || iters > (1 << 20)) continue;
+      const int reps = 64;
+      double total_ms = 0.0;
+      for (int r = -8; r < reps; ++r) {
+        hipExtLaunchKernelGGL(mfma32_kernel, dim3(cus), dim3(256), 0, 0, e0, e1, 0, iters, sk);
+        CHECK(hipGetLastError());
+        CHECK(hipEventSynchronize(e1));
+        float ms = 0.f;
+        CHECK(hipEventElapsedTime(&ms, e0, e1));
+        if (r >= 0) total_ms += ms;
+      }
+      const double us = total_ms * 1e3 / reps, flop = iters * per_iter;
+      char b[64];
+      std::snprintf(b, sizeof b, "%s%.0f", m_s.empty() ? "" : ", ", flop / 1e6); m_s += b;
+      std::snprintf(b, sizeof b, "%s%.1f", t_s.empty() ? "" : ", ", flop / (us * 1e6)); t_s += b;
+      std::snprintf(b, sizeof b, "%s%.2f", us_s.empty() ? "" : ", ", us); us_s += b;
+    }
+    std::printf("{\"mfma_mflop\": [%s], \"mfma_tflops\": [%s], \"mfma_us\": [%s]}\n", m_s.c_str(), t_s.c_str(),
                 us_s.c_str());
     return 0;
   }
