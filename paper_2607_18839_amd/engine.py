@@ -92,7 +92,9 @@ class Engine:
         self._vp = [t.data_ptr() for t in self.v_pool]
         self.workspace = torch.empty(0, dtype=torch.uint8, device=self.device)
         self._buf = {}
-        self.host_s = dict(schedule=0.0, plan=0.0, commit=0.0)
+        # host seconds per phase: the scheduler, planning and upload, enqueueing
+        # the step's launches (embedding, decode step, verification), the commit
+        self.host_s = dict(schedule=0.0, plan=0.0, enqueue=0.0, commit=0.0)
         self.steps = 0
         self.on_results = None   # optional hook(batch, verified, n_acc, draft_out) before the commit
 
@@ -132,23 +134,26 @@ class Engine:
         ws, ws_bytes = self.workspace.data_ptr(), self.workspace.numel()
         s = _stream(None)
         _lib.hpd_plan_upload(plan, ws, ws_bytes, s)
-        self.host_s["plan"] += time.perf_counter() - t2
+        t_enq = time.perf_counter()
+        self.host_s["plan"] += t_enq - t2
         tok = self._buffer("tokens", T, torch.int32)
         tok.copy_(torch.from_numpy(batch["tokens_in"].astype(np.int32)))
         h_in = self._buffer("h_in", T * self.hidden, torch.float32)
         h_out = self._buffer("h_out", T * self.hidden, torch.float32)
-        ver = self._buffer("verified", T, torch.int32)
-        nacc = self._buffer("n_acc", nb, torch.int32)
-        drafts = self._buffer("drafts", nb * _lib.HPD_MAX_K, torch.int32)
+        # the three results share one buffer, read back with one copy
+        res = self._buffer("results", T + nb + nb * _lib.HPD_MAX_K, torch.int32)
+        ver, nacc, drafts = res[:T], res[T:T + nb], res[T + nb:]
         _lib.hpd_embed_tokens(self._p["embed"].data_ptr(), self.vocab, self.hidden, tok.data_ptr(), T,
                               h_in.data_ptr(), s)
         _lib.hpd_decode_step(self.model, plan, h_in.data_ptr(), h_out.data_ptr(), self._kp, self._vp, self._kp,
                              self._vp, ws, ws_bytes, s)
         _lib.hpd_verify_draft_step(self.model, self.pmtp, plan, h_out.data_ptr(), tok.data_ptr(), ver.data_ptr(),
                                    nacc.data_ptr(), drafts.data_ptr(), ws, ws_bytes, s)
-        batch["verified"] = ver.cpu().numpy()
-        batch["n_acc"] = nacc.cpu().numpy()
-        batch["draft_out"] = drafts.cpu().numpy().reshape(nb, _lib.HPD_MAX_K)
+        self.host_s["enqueue"] += time.perf_counter() - t_enq
+        host = res.cpu().numpy()
+        batch["verified"] = host[:T]
+        batch["n_acc"] = host[T:T + nb]
+        batch["draft_out"] = host[T + nb:].reshape(nb, _lib.HPD_MAX_K)
         batch["hidden_out"] = h_out
         batch["plan"] = plan
         if self.on_results is not None:
