@@ -746,8 +746,9 @@ __device__ __forceinline__ void shared_item_staged(const AttnArgs &a, int item, 
 
 // bf16 shared-prefix kernel: same items and arithmetic as shared_item_staged,
 // on 8 waves: waves w and w + 4 own the same 32 rows and take the even and
-// odd key tiles of the item, so two waves share each SIMD; their states are
-// combined through LDS at the end.  K and V stream through an LDS ring of
+// odd key tiles of the item, so two waves share each SIMD; at the end they
+// exchange their states through LDS and each merges and writes one half of
+// the head dims (ring_epilogue).  K and V stream through an LDS ring of
 // kPairRing tile pairs filled by direct global -> LDS copies, up to three pairs
 // ahead.  Each wave is software-pipelined by one tile: the QK^T MFMAs of its
 // next tile are issued before the softmax of the current one, so they run on
