@@ -216,10 +216,12 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   std::vector<std::vector<int32_t>> group_fork(np);
   for (int p = 0; p < np; ++p) {
     const int R = P.page_T[p] * G;
+    group_fork[p].reserve(ceil_div(R, group_rows));
     for (int r0 = 0; r0 < R; r0 += group_rows) {
+      // the stacked positions of rows r0 .. r1 - 1
       int f = 0;
-      for (int r = r0; r < std::min(R, r0 + group_rows); ++r)
-        f = std::max(f, P.pos_token[2 * (size_t)(P.page_q_row[p] + r / G) + 1]);
+      const int i1 = (std::min(R, r0 + group_rows) - 1) / G;
+      for (int i = r0 / G; i <= i1; ++i) f = std::max(f, P.pos_token[2 * (size_t)(P.page_q_row[p] + i) + 1]);
       group_fork[p].push_back(f);
     }
   }
@@ -295,6 +297,11 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   // item no row of which sees its first key is not emitted, and a row writes
   // its partial of the split only if it sees the split's first key (the
   // kernels apply the same rule).
+  {
+    size_t n = 0;   // an upper bound: items trimmed by fork offsets are not emitted
+    for (int p = 0; p < np; ++p) n += (size_t)Hkv * page_splits[p] * group_fork[p].size();
+    P.shared_items.reserve(n * SI_NFIELDS);
+  }
   for (int p = 0; p < np; ++p) {
     const int Pp = P.prefix_len[p];
     const int R = P.page_T[p] * G;
@@ -336,6 +343,13 @@ hpd_status build_plan(const hpd_attn_desc *attn, const hpd_batch_desc *batch, Pl
   }
 
   // ---- private work items: (branch, kv head, row tile, key chunk)
+  {
+    size_t n = 0;
+    for (int i = 0; i < nb; ++i)
+      n += (size_t)Hkv * ceil_div(P.num_new[i] * G, kTileRows) *
+           ceil_div((int64_t)P.past_len[i] + P.num_new[i], kPrivateChunkKeys);
+    P.private_items.reserve(n * PI_NFIELDS);
+  }
   for (int i = 0; i < nb; ++i) {
     const int keys = P.past_len[i] + P.num_new[i];
     const int R = P.num_new[i] * G;
